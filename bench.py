@@ -1,0 +1,291 @@
+#!/usr/bin/env python3
+"""Throughput of the Partial FC head step on one MI355X class shard.
+
+One step = sampling + remap, gather + normalise, cosine contraction, margin
+softmax cross-entropy, backward and the sparse momentum update, for one batch
+of synthetic inputs already resident in HBM.  Default workload: the 8M-class
+shard (one GPU's share of 64M classes), B = 1024, d = 512, r = 0.1, fp16
+weights, ArcFace s = 64, m = 0.5; step t uses sampler seed t.
+
+Prints ONE JSON line (last line of stdout) with the throughput, a roofline
+entry for the step's dominant kernel (timed with HIP events inside the timed
+region) and the CPU oracle timed on this host on a bounded sample.
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "samples/sec & ms/step, PFC head fwd+bwd+update, C_shard=8M r=0.1; %MFMA/%HBM peak"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+KERNEL_SOURCES = {"sample": "sample.hip", "prep": "prep.hip", "fwd_gemm": "fwd.hip",
+                  "lse": "fwd.hip", "dx_gemm": "bwd.hip", "dx_final": "bwd.hip",
+                  "dw_update": "bwd.hip"}
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_sha(name):
+    path = os.path.join(ROOT, "paper_2010_05222_amd", "csrc", KERNEL_SOURCES[name])
+    h = hashlib.sha256()
+    for p in (path, os.path.join(ROOT, "paper_2010_05222_amd", "csrc", "pfc_device.h")):
+        with open(p, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def algorithmic_work(name, cfg, K):
+    """(flops, bytes) the method must spend in one launch of a kernel."""
+    from paper_2010_05222_amd import costmodel as cm
+    B, d, dt = cfg["B"], cfg["d"], cfg["dtype"]
+    xb = cm.DTYPE_BYTES[dt]
+    if name in ("fwd_gemm", "dx_gemm"):
+        return cm.contraction_flops(B, d, K), 0
+    if name == "dw_update":
+        return cm.contraction_flops(B, d, K), cm.update_bytes(K, d, dt, cfg["master"])
+    if name == "prep":
+        return 0, cm.gather_bytes(K, d, dt) + B * d * xb
+    return 0, 0
+
+
+def roofline_entry(name, cfg, K, avg_ms, traffic):
+    from paper_2010_05222_amd import costmodel as cm
+    flops, nbytes = algorithmic_work(name, cfg, K)
+    peak_tf = cm.PEAK_TFLOPS[cfg["dtype"]]
+    t_mfma = flops / (peak_tf * 1e12)
+    t_hbm = nbytes / (cm.PEAK_HBM_GBPS * 1e9)
+    sec = avg_ms * 1e-3
+    if t_hbm >= t_mfma:
+        achieved = nbytes / sec / 1e9
+        entry = {"bound": "hbm", "achieved": achieved, "peak": cm.PEAK_HBM_GBPS, "unit": "GB/s"}
+    else:
+        achieved = flops / sec / 1e12
+        entry = {"bound": "mfma", "achieved": achieved, "peak": peak_tf, "unit": "TFLOP/s"}
+    entry["frac"] = entry["achieved"] / entry["peak"]
+    entry["traffic"] = traffic
+    entry["kernel"] = name
+    entry["avg_ms"] = avg_ms
+    return entry
+
+
+def measured_traffic(name, workload):
+    """HBM bytes per launch from committed counter runs, if they match the current kernel."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            rec = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    ent = rec.get(name)
+    if not ent or ent.get("workload") != workload:
+        return None
+    if ent.get("source_sha256") != kernel_source_sha(name):
+        return None
+    return ent.get("bytes_per_launch")
+
+
+def cpu_baseline(cfg, W_dev, rows):
+    """The CPU oracle, as it stands, on a bounded sample of the workload.
+
+    Sample: the full shard's sampling (all C classes) and the full update of
+    the |S| active rows, plus forward and backward of `rows` batch rows
+    against all |S| active classes; the per-row part is scaled to the full
+    batch.  Returns the baseline entry (samples/s) and the phase timings."""
+    import numpy as np
+    import torch
+    from oracle import pfc_oracle as O
+    import workloads
+
+    X, labels = workloads.make_batch(cfg, 0)
+    tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[cfg["dtype"]]
+    Xs = torch.from_numpy(X[:rows]).to(tdt).double().numpy()
+    Ls = labels[:rows]
+    W = W_dev.cpu().numpy() if cfg["dtype"] != "bf16" else W_dev.float().cpu().numpy()
+    C, d = cfg["C"], cfg["d"]
+    t0 = time.perf_counter()
+    active, mapped, _ = O.sample_active(Ls, C, cfg["a"], cfg["r"], 0)
+    t1 = time.perf_counter()
+    Ws = np.asarray(W[active], dtype=np.float64)
+    fw = O.forward(Xs, Ws, mapped, cfg["s"], cfg["m"], cfg["margin"])
+    O.grad_x(Xs, Ws, mapped, fw["lse"], rows, cfg["s"], cfg["m"], cfg["margin"])
+    g = O.grad_w(Xs, Ws, np.arange(len(active)), mapped, fw["lse"], rows, cfg["s"], cfg["m"],
+                 cfg["margin"])
+    t2 = time.perf_counter()
+    M = np.zeros((C, d), dtype=np.float32)
+    O.momentum_update(W, M, active, g, cfg["lr"], cfg["mu"], cfg["dtype"])
+    t3 = time.perf_counter()
+    t_step = (t1 - t0) + (t3 - t2) + (t2 - t1) * cfg["B"] / rows
+    threads = 1
+    try:
+        import threadpoolctl
+        info = threadpoolctl.threadpool_info()
+        threads = max([i.get("num_threads", 1) for i in info] + [1])
+    except Exception:  # noqa: BLE001 - threadpoolctl is optional
+        pass
+    entry = {"value": cfg["B"] / t_step, "unit": "samples/s", "cores": threads, "kind": "oracle",
+             "sample": (f"full sampling over C={C} and full update of |S|={len(active)} rows, "
+                        f"forward+backward of {rows} of {cfg['B']} rows against all |S| classes, "
+                        f"row part scaled x{cfg['B'] // rows}; float64 NumPy, BLAS threads "
+                        f"{threads}, host affinity {len(os.sched_getaffinity(0))} cpus"),
+             "phase_s": {"sample": t1 - t0, "rows": t2 - t1, "update": t3 - t2},
+             "cpu_seconds": t3 - t0}
+    return entry
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="massive")
+    ap.add_argument("--kernel-steps", type=int, default=5,
+                    help="steps per untimed per-kernel timing pass")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=32)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 1 GiB device copy (counter calibration)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU's class shard only (asked for --gpus {args.gpus}, "
+              f"WORLD_SIZE {world}); multi-GPU runs are not part of this build.", flush=True)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import workloads
+    from paper_2010_05222_amd import pfc as abi
+    from paper_2010_05222_amd.head import PfcShard
+
+    cfg = workloads.config(args.workload)
+    dev = torch.device("cuda:0")
+    tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[cfg["dtype"]]
+    B, d, C = cfg["B"], cfg["d"], cfg["C"]
+    log(f"[bench] workload {cfg['name']}: B={B} d={d} C={C} r={cfg['r']} {cfg['dtype']}")
+
+    W, master = workloads.make_weights_device(cfg, dev)
+    M = torch.zeros((C, d), dtype=torch.float32, device=dev)
+    shard = PfcShard(B, d, C, cfg["r"], dtype=cfg["dtype"], class_offset=cfg["a"], s=cfg["s"],
+                     m=cfg["m"], margin=cfg["margin"], lr=cfg["lr"], mu=cfg["mu"], device=dev)
+    n_extra = args.warmup + args.kernel_steps * len(abi.KERNEL_NAMES)
+    batches = []
+    for t in range(args.steps):
+        X, L = workloads.make_batch(cfg, t)
+        batches.append((torch.from_numpy(X).to(tdt).to(dev), torch.from_numpy(L).to(dev), t))
+    extra = []
+    for i in range(n_extra):
+        X, L = workloads.make_batch(cfg, 10**6 + i)
+        extra.append((torch.from_numpy(X).to(tdt).to(dev), torch.from_numpy(L).to(dev),
+                      10**6 + i))
+    torch.cuda.synchronize()
+    log(f"[bench] inputs resident: W {W.numel() * W.element_size() / 2**30:.2f} GiB, "
+        f"momentum {M.numel() * 4 / 2**30:.2f} GiB, workspace {shard.ws_bytes / 2**30:.2f} GiB")
+
+    def run(batch):
+        X, L, seed = batch
+        shard.step(X, L, W, M, seed, master)
+
+    it = iter(extra)
+    for _ in range(args.warmup):
+        run(next(it))
+    torch.cuda.synchronize()
+    log("[bench] warm-up done")
+
+    # Untimed per-kernel passes: mean duration of each kernel (HIP events).
+    stage_ms = {}
+    for kid, name in abi.KERNEL_NAMES.items():
+        abi.pfc_timing_begin(kid, args.kernel_steps)
+        for _ in range(args.kernel_steps):
+            run(next(it))
+        torch.cuda.synchronize()
+        tot, n = abi.pfc_timing_end()
+        stage_ms[name] = tot / max(n, 1)
+    K = int(shard.n_active.item())
+    contenders = {k: v for k, v in stage_ms.items() if k != "sample"}
+    dominant = max(contenders, key=contenders.get)
+    dom_id = {v: k for k, v in abi.KERNEL_NAMES.items()}[dominant]
+    log(f"[bench] |S|={K}; per-kernel ms: " +
+        ", ".join(f"{k}={v:.4f}" for k, v in stage_ms.items()) + f"; dominant {dominant}")
+
+    # Timed region: exactly `steps` steps; the dominant kernel bracketed by HIP events.
+    abi.pfc_timing_begin(dom_id, args.steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for b in batches:
+        run(b)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    dom_total, dom_n = abi.pfc_timing_end()
+    dom_avg = dom_total / max(dom_n, 1)
+    loss = float(shard.loss.item())
+    ms_per_step = elapsed * 1e3 / args.steps
+    log(f"[bench] timed {args.steps} steps: {ms_per_step:.4f} ms/step, last loss {loss:.4f}, "
+        f"{dominant} avg {dom_avg:.4f} ms over {dom_n} launches")
+    if not np.isfinite(loss):
+        raise RuntimeError("non-finite loss")
+
+    if args.copy_calibration:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        log("[bench] copy calibration: 3 x 1 GiB device copies")
+
+    from paper_2010_05222_amd import costmodel as cm
+    roof = roofline_entry(dominant, cfg, K, dom_avg, measured_traffic(dominant, cfg["name"]))
+    step_fl = cm.step_flops(B, d, K)
+    upd_b = cm.update_bytes(K, d, cfg["dtype"], cfg["master"])
+    stage_roofs = {}
+    for name, ms in stage_ms.items():
+        fl, nb = algorithmic_work(name, cfg, K)
+        if fl or nb:
+            stage_roofs[name] = roofline_entry(name, cfg, K, ms, None)["frac"]
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(f"[bench] CPU oracle on a bounded sample ({args.cpu_rows} rows)...")
+        cpu = cpu_baseline(cfg, W, args.cpu_rows)
+        log(f"[bench] CPU oracle: {cpu['value']:.3f} samples/s ({cpu['cpu_seconds']:.1f} s)")
+
+    out = {
+        "metric": METRIC,
+        "value": B * args.steps / elapsed,
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg["dtype"],
+        "data": "synthetic",
+        "config": {"workload": f"{cfg['name']}: B={B} d={d} C_shard={C} r={cfg['r']} "
+                               f"|S|={K} {cfg['margin']} s={cfg['s']} m={cfg['m']}",
+                   "global_batch": B, "d": d, "C_shard": C, "r": cfg["r"], "active": K,
+                   "margin": cfg["margin"], "w_dtype": cfg["dtype"], "momentum": "f32",
+                   "parallelism": "one class shard on one GPU"},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "stage_ms": stage_ms,
+        "stage_roofline_frac": stage_roofs,
+        "step_mfma_frac": step_fl / (ms_per_step * 1e-3) / (cm.PEAK_TFLOPS[cfg["dtype"]] * 1e12),
+        "update_hbm_frac": upd_b / (stage_ms["dw_update"] * 1e-3) / (cm.PEAK_HBM_GBPS * 1e9),
+        "last_loss": loss,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,117 @@
+// Internal declarations shared by the HIP translation units of libpfc.
+// Not part of the public ABI (include/pfc.h is).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace pfc {
+
+// ----------------------------------------------------------------- sampler
+
+enum SampleMode : uint32_t { kSelectNone = 0, kSelectKeys = 1, kSelectAll = 2 };
+
+// Device-resident sampler state of one step (lives in the workspace).
+struct SampleState {
+  uint32_t n_pos;       // |P|: distinct owned labels
+  uint32_t mode;        // SampleMode
+  uint32_t cand_count;  // candidates collected in the threshold's top bucket
+  uint32_t top_digit;   // value of the top key bits holding the threshold
+  int64_t n_neg;        // max(b - |P|, 0)
+  int64_t k_rem;        // keys equal to `thresh` still to take (class order)
+  uint64_t thresh;      // n_neg-th smallest non-positive key
+};
+
+// Compaction works on groups of kCompactClasses consecutive classes.
+constexpr int kCompactThreads = 256;
+constexpr int kCompactClasses = 4 * kCompactThreads;
+constexpr int kTopBitsMax = 12;
+
+struct SampleWs {
+  uint32_t* bitmap;      // ceil(C/32) words: bit c set iff class c is positive
+  uint32_t* hist;        // 2^kTopBitsMax bins
+  SampleState* state;
+  uint64_t* keys;        // C keys (only in kSelectKeys mode)
+  uint32_t* cand;        // C candidate class ids (worst case)
+  uint32_t* grp_sure;    // per compaction group: classes surely selected
+  uint32_t* grp_tie;     // per compaction group: non-positive keys == thresh
+  uint32_t* grp_out;     // per compaction group: output offset
+  uint32_t* grp_tie_off; // per compaction group: ties before the group
+};
+
+// ----------------------------------------------------------------- step
+
+// Quantised cosine store of the 16-bit paths: q = round(cos * 2^15),
+// clamped to [-32767, 32767]; cos = q * 2^-15.
+constexpr float kCosQuant = 32768.0f;
+constexpr float kCosDequant = 1.0f / 32768.0f;
+
+struct StepWs {
+  float* inv_x;          // [B]      1/max(||x_n||, eps)
+  void* xT;              // [d x ldb] X transposed in bf16, zero for n >= B (16-bit paths)
+  int64_t ldb;           // row stride of xT: B rounded up to 32
+  float* inv_w;          // [ld_cos] 1/max(||W[S_j]||, eps)
+  void* cosq;            // [B x ld_cos] quantised cosines (int16) or fp32 cosines
+  int64_t ld_cos;        // row stride of cosq: cap rounded up to 256
+  float2* stats;         // [B x n_ctiles] per class tile: (max, sum exp(f - max))
+  int64_t n_ctiles;      // class tiles of the forward contraction
+  float* tgt;            // [B] margined target logit
+  float* dx_part;        // [n_split x B x d] split-K partial sums of dX_hat
+  int n_split;
+  float* loss_part;      // [B] per-row loss terms
+};
+
+// Layout of the whole workspace (offsets in bytes from its base).
+struct WsLayout {
+  size_t bytes;
+  size_t sample_bytes;   // prefix used by the sampler
+  size_t off_bitmap, off_hist, off_state, off_keys, off_cand;
+  size_t off_grp_sure, off_grp_tie, off_grp_out, off_grp_tie_off;
+  size_t off_inv_x, off_xT, off_inv_w, off_cos, off_stats, off_tgt, off_dx, off_loss;
+  int64_t ldb, ld_cos, n_ctiles, n_groups;
+  int n_split;
+  int top_bits;
+};
+
+WsLayout ws_layout(int64_t B, int64_t d, int64_t C, int64_t cap, int compute);
+SampleWs sample_ws(void* ws, const WsLayout& L);
+StepWs step_ws(void* ws, const WsLayout& L);
+
+hipError_t launch_sample(const int64_t* labels, int64_t B, int64_t C,
+                         int64_t a, int64_t budget, uint64_t seed,
+                         int top_bits, int64_t n_groups, const SampleWs& w,
+                         int32_t* active, int32_t* n_active,
+                         int32_t* labels_mapped, hipStream_t stream);
+
+struct StepArgs {
+  const void* X;
+  void* W;
+  float* W_master;
+  float* M;
+  const int32_t* active;
+  const int32_t* n_active;
+  const int32_t* labels_mapped;
+  const float* row_lse;
+  float* loss;
+  float* row_lse_out;
+  float* dX;
+  int64_t B, d, C, cap;
+  int dtype;      // pfc_dtype of X, W and the compute
+  float s, m;
+  int margin;     // pfc_margin
+  float lr, mu;
+};
+
+hipError_t launch_prep(const StepArgs& a, const StepWs& w, hipStream_t stream);
+hipError_t launch_forward(const StepArgs& a, const StepWs& w, hipStream_t stream);
+hipError_t launch_backward(const StepArgs& a, const StepWs& w, hipStream_t stream);
+
+// Measurement hook (pfc_timing_begin / pfc_timing_end): launchers bracket a
+// kernel id's launches with these calls; both are no-ops unless armed.
+void timing_start(int kernel, hipStream_t stream);
+void timing_stop(int kernel, hipStream_t stream);
+
+__host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+}  // namespace pfc

@@ -1,0 +1,494 @@
+// Positive-preserving negative sampling and label remap on one class shard
+// (Partial FC, Sec. 3.3.1-3.3.2, Eq. local_sampling).
+//
+// S = P  union  {the n_neg = max(b - |P|, 0) non-positive classes with the
+// smallest 64-bit Philox keys, ties to the lower class id}, sorted ascending,
+// then labels_mapped = searchsorted(S, y - a).
+//
+// Kernel sequence (no host synchronisation; every kernel reads the
+// device-side mode and returns early when it has nothing to do):
+//   clear -> mark positives (bitmap, |P|) -> plan (mode, n_neg)
+//   -> keys + top-bit histogram (one Philox pass, keys kept in the workspace)
+//   -> pick the top bucket holding the n_neg-th key -> collect that bucket
+//   -> resolve the remaining key bits inside one workgroup (exact threshold)
+//   -> count / scan / write compaction in class order (wavefront ballots),
+//      which yields S already sorted -> remap by binary search.
+#include "pfc_internal.h"
+
+namespace pfc {
+namespace {
+
+// Philox4x64-10 (Salmon et al., SC'11): multipliers and Weyl key increments
+// of the 4x64 variant.
+constexpr uint64_t kPhiloxM0 = 0xD2E7470EE14C6C93ull;
+constexpr uint64_t kPhiloxM1 = 0xCA5A826395121157ull;
+constexpr uint64_t kPhiloxW0 = 0x9E3779B97F4A7C15ull;
+constexpr uint64_t kPhiloxW1 = 0xBB67AE8584CAA73Bull;
+
+struct U64x4 {
+  uint64_t v[4];
+};
+
+__device__ __forceinline__ U64x4 philox4x64_10(uint64_t c0, uint64_t seed) {
+  uint64_t x0 = c0, x1 = 0, x2 = 0, x3 = 0;
+  uint64_t k0 = seed, k1 = 0;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k0 += kPhiloxW0;
+      k1 += kPhiloxW1;
+    }
+    const uint64_t hi0 = __umul64hi(kPhiloxM0, x0);
+    const uint64_t lo0 = kPhiloxM0 * x0;
+    const uint64_t hi1 = __umul64hi(kPhiloxM1, x2);
+    const uint64_t lo1 = kPhiloxM1 * x2;
+    const uint64_t n0 = hi1 ^ x1 ^ k0;
+    const uint64_t n2 = hi0 ^ x3 ^ k1;
+    x0 = n0;
+    x1 = lo1;
+    x2 = n2;
+    x3 = lo0;
+  }
+  U64x4 out;
+  out.v[0] = x0;
+  out.v[1] = x1;
+  out.v[2] = x2;
+  out.v[3] = x3;
+  return out;
+}
+
+__device__ __forceinline__ bool is_positive(const uint32_t* bitmap, int64_t c) {
+  return (bitmap[c >> 5] >> (c & 31)) & 1u;
+}
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+
+__device__ __forceinline__ uint32_t popc_below(uint64_t mask) {
+  const uint64_t below = (1ull << lane_id()) - 1ull;
+  return (uint32_t)__popcll(mask & below);
+}
+
+// Exclusive prefix sum of `v` over the block (blockDim.x a multiple of 64,
+// at most 1024 threads); `total` receives the block sum.  Uses `smem` of
+// (blockDim.x / 64) entries.
+__device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* smem, uint32_t* total) {
+  const int lane = lane_id();
+  const int wave = threadIdx.x >> 6;
+  const int nwaves = blockDim.x >> 6;
+  uint32_t incl = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t t = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += t;
+  }
+  if (lane == 63) smem[wave] = incl;
+  __syncthreads();
+  uint32_t wave_off = 0, sum = 0;
+  for (int w = 0; w < nwaves; ++w) {
+    const uint32_t t = smem[w];
+    if (w < wave) wave_off += t;
+    sum += t;
+  }
+  __syncthreads();
+  *total = sum;
+  return wave_off + incl - v;
+}
+
+// Same for 64-bit sums.
+__device__ uint64_t block_exclusive_scan64(uint64_t v, uint64_t* smem, uint64_t* total) {
+  const int lane = lane_id();
+  const int wave = threadIdx.x >> 6;
+  const int nwaves = blockDim.x >> 6;
+  uint64_t incl = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint64_t t = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += t;
+  }
+  if (lane == 63) smem[wave] = incl;
+  __syncthreads();
+  uint64_t wave_off = 0, sum = 0;
+  for (int w = 0; w < nwaves; ++w) {
+    const uint64_t t = smem[w];
+    if (w < wave) wave_off += t;
+    sum += t;
+  }
+  __syncthreads();
+  *total = sum;
+  return wave_off + incl - v;
+}
+
+// Find the bin holding the k-th (1-based) element of an LDS histogram of
+// `nbins` bins (nbins a multiple of blockDim.x).  Returns through shared
+// out[0] = bin, out[1] = count before the bin, out[2] = count of the bin.
+__device__ void find_kth_bin(const uint32_t* hist, int nbins, int64_t k,
+                             uint64_t* scan_smem, int64_t* out) {
+  const int per = nbins / blockDim.x;
+  const int b0 = threadIdx.x * per;
+  uint64_t local = 0;
+  for (int i = 0; i < per; ++i) local += hist[b0 + i];
+  uint64_t total;
+  uint64_t before = block_exclusive_scan64(local, scan_smem, &total);
+  if ((int64_t)before < k && k <= (int64_t)(before + local)) {
+    for (int i = 0; i < per; ++i) {
+      const uint64_t h = hist[b0 + i];
+      if ((int64_t)(before + h) >= k) {
+        out[0] = b0 + i;
+        out[1] = (int64_t)before;
+        out[2] = (int64_t)h;
+        break;
+      }
+      before += h;
+    }
+  }
+  __syncthreads();
+}
+
+// ----------------------------------------------------------------- kernels
+
+__global__ void k_sample_clear(uint32_t* bitmap, int64_t nwords, uint32_t* hist,
+                               SampleState* st) {
+  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = tid; i < nwords; i += stride) bitmap[i] = 0u;
+  for (int64_t i = tid; i < (1 << kTopBitsMax); i += stride) hist[i] = 0u;
+  if (tid == 0) {
+    st->n_pos = 0;
+    st->mode = kSelectNone;
+    st->cand_count = 0;
+    st->top_digit = 0;
+    st->n_neg = 0;
+    st->k_rem = 0;
+    st->thresh = 0;
+  }
+}
+
+__global__ void k_mark_positives(const int64_t* labels, int64_t B, int64_t C,
+                                 int64_t a, uint32_t* bitmap, SampleState* st) {
+  const int64_t n = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (n >= B) return;
+  const int64_t y = labels[n];
+  if (y < a || y >= a + C) return;
+  const int64_t c = y - a;
+  const uint32_t bit = 1u << (c & 31);
+  const uint32_t old = atomicOr(&bitmap[c >> 5], bit);
+  if (!(old & bit)) atomicAdd(&st->n_pos, 1u);
+}
+
+__global__ void k_sample_plan(SampleState* st, int64_t budget, int64_t C) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  const int64_t n_pos = st->n_pos;
+  const int64_t n_neg = budget > n_pos ? budget - n_pos : 0;
+  const int64_t pool = C - n_pos;
+  st->n_neg = n_neg;
+  if (n_neg == 0) {
+    st->mode = kSelectNone;
+    st->thresh = 0;
+    st->k_rem = 0;
+  } else if (n_neg >= pool) {
+    st->mode = kSelectAll;
+    st->thresh = ~0ull;
+    st->k_rem = INT64_MAX;
+  } else {
+    st->mode = kSelectKeys;
+    st->k_rem = n_neg;
+  }
+}
+
+// One Philox block per thread: global ids 4q .. 4q+3, q = q_lo + thread.
+__global__ void __launch_bounds__(256) k_keys_hist(uint64_t seed, int64_t a, int64_t C,
+                                                   int top_bits, const uint32_t* bitmap,
+                                                   uint64_t* keys, uint32_t* hist,
+                                                   const SampleState* st) {
+  if (st->mode != kSelectKeys) return;
+  __shared__ uint32_t lhist[1 << kTopBitsMax];
+  const int nbins = 1 << top_bits;
+  for (int i = threadIdx.x; i < nbins; i += blockDim.x) lhist[i] = 0u;
+  __syncthreads();
+  const int64_t q_lo = a >> 2;
+  const int64_t q_hi = (a + C - 1) >> 2;
+  const int64_t q = q_lo + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q <= q_hi) {
+    const U64x4 w = philox4x64_10((uint64_t)q, seed);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t c = 4 * q + i - a;
+      if (c < 0 || c >= C) continue;
+      keys[c] = w.v[i];
+      if (!is_positive(bitmap, c)) atomicAdd(&lhist[w.v[i] >> (64 - top_bits)], 1u);
+    }
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < nbins; i += blockDim.x) {
+    const uint32_t h = lhist[i];
+    if (h) atomicAdd(&hist[i], h);
+  }
+}
+
+// One workgroup of 1024 threads: the top bucket holding the n_neg-th key.
+__global__ void __launch_bounds__(1024) k_select_top(const uint32_t* hist, int top_bits,
+                                                     SampleState* st) {
+  if (st->mode != kSelectKeys) return;
+  __shared__ uint32_t lh[1 << kTopBitsMax];
+  __shared__ uint64_t scan_smem[16];
+  __shared__ int64_t found[3];
+  const int nbins = 1 << top_bits;
+  const int nb = nbins < (int)blockDim.x ? (int)blockDim.x : nbins;
+  for (int i = threadIdx.x; i < nb; i += blockDim.x) lh[i] = i < nbins ? hist[i] : 0u;
+  __syncthreads();
+  find_kth_bin(lh, nb, st->k_rem, scan_smem, found);
+  if (threadIdx.x == 0) {
+    st->top_digit = (uint32_t)found[0];
+    st->k_rem -= found[1];
+    st->cand_count = 0;
+  }
+}
+
+// Collect the non-positive classes whose key's top bits equal the bucket.
+__global__ void __launch_bounds__(256) k_collect(const uint64_t* keys, const uint32_t* bitmap,
+                                                 int64_t C, int top_bits, SampleState* st,
+                                                 uint32_t* cand) {
+  if (st->mode != kSelectKeys) return;
+  const uint64_t digit = st->top_digit;
+  const int64_t c0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t c = c0 + i;
+    bool take = false;
+    if (c < C) take = !is_positive(bitmap, c) && (keys[c] >> (64 - top_bits)) == digit;
+    const uint64_t mask = __ballot(take);
+    if (mask == 0) continue;
+    uint32_t base = 0;
+    const int leader = __ffsll((unsigned long long)mask) - 1;
+    if (lane_id() == leader) base = atomicAdd(&st->cand_count, (uint32_t)__popcll(mask));
+    base = __shfl(base, leader, 64);
+    if (take) cand[base + popc_below(mask)] = (uint32_t)c;
+  }
+}
+
+// One workgroup: resolve the remaining 64 - top_bits bits of the threshold
+// among the collected candidates, 11 bits per round.
+__global__ void __launch_bounds__(1024) k_refine(const uint64_t* keys, const uint32_t* cand,
+                                                 int top_bits, SampleState* st) {
+  if (st->mode != kSelectKeys) return;
+  constexpr int kBits = 11;
+  __shared__ uint32_t lh[1 << kBits];
+  __shared__ uint64_t scan_smem[16];
+  __shared__ int64_t found[3];
+  const uint32_t n = st->cand_count;
+  uint64_t prefix = st->top_digit;
+  int known = top_bits;
+  int64_t k = st->k_rem;
+  while (known < 64) {
+    const int bits = (64 - known) < kBits ? (64 - known) : kBits;
+    const int shift = 64 - known - bits;
+    for (int i = threadIdx.x; i < (1 << kBits); i += blockDim.x) lh[i] = 0u;
+    __syncthreads();
+    for (uint32_t i = threadIdx.x; i < n; i += blockDim.x) {
+      const uint64_t key = keys[cand[i]];
+      if ((key >> (64 - known)) == prefix)
+        atomicAdd(&lh[(key >> shift) & ((1u << bits) - 1u)], 1u);
+    }
+    __syncthreads();
+    find_kth_bin(lh, 1 << kBits, k, scan_smem, found);
+    prefix = (prefix << bits) | (uint64_t)found[0];
+    k -= found[1];
+    known += bits;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    st->thresh = prefix;
+    st->k_rem = k;
+  }
+}
+
+// Per class of one thread: bit i of `sure` / `tie` for class c0 + i.
+__device__ __forceinline__ void class_flags(const uint64_t* keys, const uint32_t* bitmap,
+                                            int64_t C, uint32_t mode, uint64_t thresh,
+                                            int64_t c0, uint32_t* sure, uint32_t* tie) {
+  uint32_t s = 0, t = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t c = c0 + i;
+    if (c >= C) continue;
+    if (is_positive(bitmap, c)) {
+      s |= 1u << i;
+    } else if (mode == kSelectAll) {
+      s |= 1u << i;
+    } else if (mode == kSelectKeys) {
+      const uint64_t key = keys[c];
+      if (key < thresh) s |= 1u << i;
+      else if (key == thresh) t |= 1u << i;
+    }
+  }
+  *sure = s;
+  *tie = t;
+}
+
+__global__ void __launch_bounds__(kCompactThreads) k_compact_count(
+    const uint64_t* keys, const uint32_t* bitmap, int64_t C, const SampleState* st,
+    uint32_t* grp_sure, uint32_t* grp_tie) {
+  __shared__ uint32_t smem[kCompactThreads / 64];
+  const int64_t c0 = ((int64_t)blockIdx.x * kCompactThreads + threadIdx.x) * 4;
+  uint32_t s, t;
+  class_flags(keys, bitmap, C, st->mode, st->thresh, c0, &s, &t);
+  uint32_t tot_s, tot_t;
+  block_exclusive_scan((uint32_t)__popc(s), smem, &tot_s);
+  block_exclusive_scan((uint32_t)__popc(t), smem, &tot_t);
+  if (threadIdx.x == 0) {
+    grp_sure[blockIdx.x] = tot_s;
+    grp_tie[blockIdx.x] = tot_t;
+  }
+}
+
+// One workgroup of 1024 threads: per-group tie offsets, selected counts and
+// output offsets; n_active.
+__global__ void __launch_bounds__(1024) k_compact_scan(const uint32_t* grp_sure,
+                                                       const uint32_t* grp_tie,
+                                                       int64_t n_groups, const SampleState* st,
+                                                       uint32_t* grp_out, uint32_t* grp_tie_off,
+                                                       int32_t* n_active) {
+  __shared__ uint64_t smem[16];
+  const int64_t per = ceil_div(n_groups, (int64_t)blockDim.x);
+  const int64_t g0 = (int64_t)threadIdx.x * per;
+  const int64_t g1 = g0 + per < n_groups ? g0 + per : n_groups;
+  const int64_t k_rem = st->k_rem;
+  // Ties before each group.
+  uint64_t local_t = 0;
+  for (int64_t g = g0; g < g1; ++g) local_t += grp_tie[g];
+  uint64_t tot;
+  uint64_t tie_before = block_exclusive_scan64(local_t, smem, &tot);
+  // Selected count of each group: sure + the ties whose class-order rank is below k_rem.
+  uint64_t local_sel = 0;
+  {
+    uint64_t tb = tie_before;
+    for (int64_t g = g0; g < g1; ++g) {
+      const uint64_t t = grp_tie[g];
+      int64_t take = k_rem - (int64_t)tb;
+      take = take < 0 ? 0 : (take > (int64_t)t ? (int64_t)t : take);
+      local_sel += grp_sure[g] + (uint64_t)take;
+      tb += t;
+    }
+  }
+  uint64_t total_sel;
+  uint64_t out_before = block_exclusive_scan64(local_sel, smem, &total_sel);
+  uint64_t tb = tie_before, ob = out_before;
+  for (int64_t g = g0; g < g1; ++g) {
+    const uint64_t t = grp_tie[g];
+    int64_t take = k_rem - (int64_t)tb;
+    take = take < 0 ? 0 : (take > (int64_t)t ? (int64_t)t : take);
+    grp_tie_off[g] = (uint32_t)tb;
+    grp_out[g] = (uint32_t)ob;
+    ob += grp_sure[g] + (uint64_t)take;
+    tb += t;
+  }
+  if (threadIdx.x == 0) *n_active = (int32_t)total_sel;
+}
+
+// Exclusive class-order prefix of the flag bits over the workgroup, where
+// thread t owns classes 4t .. 4t+3: per-class rank in bit order, via one
+// wavefront ballot per class slot plus a cross-wave offset.
+__device__ __forceinline__ void ordered_ranks(uint32_t flags, uint32_t* wave_tot_smem,
+                                              uint32_t rank[4], uint32_t* total) {
+  uint32_t before_lanes = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) before_lanes += popc_below(__ballot((flags >> i) & 1u));
+  const uint32_t mine = (uint32_t)__popc(flags);
+  // Wave total = before_lanes of lane 63 + its own count.
+  const int wave = threadIdx.x >> 6;
+  if (lane_id() == 63) wave_tot_smem[wave] = before_lanes + mine;
+  __syncthreads();
+  uint32_t wave_off = 0, sum = 0;
+  for (int w = 0; w < (int)(blockDim.x >> 6); ++w) {
+    const uint32_t t = wave_tot_smem[w];
+    if (w < wave) wave_off += t;
+    sum += t;
+  }
+  __syncthreads();
+  uint32_t r = wave_off + before_lanes;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    rank[i] = r;
+    r += (flags >> i) & 1u;
+  }
+  *total = sum;
+}
+
+__global__ void __launch_bounds__(kCompactThreads) k_compact_write(
+    const uint64_t* keys, const uint32_t* bitmap, int64_t C, const SampleState* st,
+    const uint32_t* grp_out, const uint32_t* grp_tie_off, int32_t* active) {
+  __shared__ uint32_t smem[kCompactThreads / 64];
+  const int64_t c0 = ((int64_t)blockIdx.x * kCompactThreads + threadIdx.x) * 4;
+  uint32_t s, t;
+  class_flags(keys, bitmap, C, st->mode, st->thresh, c0, &s, &t);
+  uint32_t trank[4], ttot;
+  ordered_ranks(t, smem, trank, &ttot);
+  const int64_t tie_base = grp_tie_off[blockIdx.x];
+  const int64_t k_rem = st->k_rem;
+  uint32_t sel = s;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    if (((t >> i) & 1u) && tie_base + (int64_t)trank[i] < k_rem) sel |= 1u << i;
+  uint32_t srank[4], stot;
+  ordered_ranks(sel, smem, srank, &stot);
+  const int64_t out_base = grp_out[blockIdx.x];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    if ((sel >> i) & 1u) active[out_base + srank[i]] = (int32_t)(c0 + i);
+}
+
+__global__ void k_remap(const int64_t* labels, int64_t B, int64_t C, int64_t a,
+                        const int32_t* active, const int32_t* n_active,
+                        int32_t* labels_mapped) {
+  const int64_t n = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (n >= B) return;
+  const int64_t y = labels[n];
+  if (y < a || y >= a + C) {
+    labels_mapped[n] = -1;
+    return;
+  }
+  const int32_t c = (int32_t)(y - a);
+  int32_t lo = 0, hi = *n_active;  // first index with active[idx] >= c
+  while (lo < hi) {
+    const int32_t mid = lo + ((hi - lo) >> 1);
+    if (active[mid] < c) lo = mid + 1;
+    else hi = mid;
+  }
+  labels_mapped[n] = lo;
+}
+
+}  // namespace
+
+hipError_t launch_sample(const int64_t* labels, int64_t B, int64_t C, int64_t a,
+                         int64_t budget, uint64_t seed, int top_bits, int64_t n_groups,
+                         const SampleWs& w, int32_t* active, int32_t* n_active,
+                         int32_t* labels_mapped, hipStream_t stream) {
+  timing_start(0, stream);
+  const int64_t nwords = ceil_div(C, 32);
+  const int clear_blocks = (int)(ceil_div(nwords, 256) < 4096 ? ceil_div(nwords, 256) : 4096);
+  hipLaunchKernelGGL(k_sample_clear, dim3(clear_blocks > 0 ? clear_blocks : 1), dim3(256), 0,
+                     stream, w.bitmap, nwords, w.hist, w.state);
+  hipLaunchKernelGGL(k_mark_positives, dim3((unsigned)ceil_div(B, 256)), dim3(256), 0, stream,
+                     labels, B, C, a, w.bitmap, w.state);
+  hipLaunchKernelGGL(k_sample_plan, dim3(1), dim3(64), 0, stream, w.state, budget, C);
+  const int64_t n_blocks_philox = ((a + C - 1) >> 2) - (a >> 2) + 1;
+  hipLaunchKernelGGL(k_keys_hist, dim3((unsigned)ceil_div(n_blocks_philox, 256)), dim3(256), 0,
+                     stream, seed, a, C, top_bits, w.bitmap, w.keys, w.hist, w.state);
+  hipLaunchKernelGGL(k_select_top, dim3(1), dim3(1024), 0, stream, w.hist, top_bits, w.state);
+  hipLaunchKernelGGL(k_collect, dim3((unsigned)ceil_div(C, 1024)), dim3(256), 0, stream, w.keys,
+                     w.bitmap, C, top_bits, w.state, w.cand);
+  hipLaunchKernelGGL(k_refine, dim3(1), dim3(1024), 0, stream, w.keys, w.cand, top_bits,
+                     w.state);
+  hipLaunchKernelGGL(k_compact_count, dim3((unsigned)n_groups), dim3(kCompactThreads), 0, stream,
+                     w.keys, w.bitmap, C, w.state, w.grp_sure, w.grp_tie);
+  hipLaunchKernelGGL(k_compact_scan, dim3(1), dim3(1024), 0, stream, w.grp_sure, w.grp_tie,
+                     n_groups, w.state, w.grp_out, w.grp_tie_off, n_active);
+  hipLaunchKernelGGL(k_compact_write, dim3((unsigned)n_groups), dim3(kCompactThreads), 0, stream,
+                     w.keys, w.bitmap, C, w.state, w.grp_out, w.grp_tie_off, active);
+  hipLaunchKernelGGL(k_remap, dim3((unsigned)ceil_div(B, 256)), dim3(256), 0, stream, labels, B,
+                     C, a, active, n_active, labels_mapped);
+  timing_stop(0, stream);
+  return hipGetLastError();
+}
+
+}  // namespace pfc

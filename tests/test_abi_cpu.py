@@ -1,0 +1,163 @@
+"""Host-side checks of the C ABI: the library loads, exports every symbol the
+header declares, sizes its workspace as documented and rejects bad arguments
+before touching the GPU (no kernel is ever launched by these tests)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+import torch
+
+from oracle import pfc_oracle as O
+import workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pfc.h")
+
+pfc = pytest.importorskip("paper_2010_05222_amd.pfc", reason="libpfc.so not built")
+
+FAKE = 0x1000        # never dereferenced: every call below fails its checks first
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pfc_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    names = _declared_functions()
+    assert set(names) == set(pfc.EXPORTS)
+    lib = ctypes.CDLL(pfc.LIB_PATH)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings():
+    for st in range(6):
+        assert pfc.pfc_status_string(st) not in ("", "unknown status")
+    assert pfc.pfc_status_string(99) == "unknown status"
+
+
+@pytest.mark.parametrize("name", list(workloads.CONFIGS))
+def test_workspace_and_capacity_of_each_workload(name):
+    cfg = workloads.config(name)
+    code = {"f32": pfc.PFC_F32, "bf16": pfc.PFC_BF16, "f16": pfc.PFC_F16}[cfg["dtype"]]
+    nbytes, cap = pfc.pfc_workspace_bytes(cfg["B"], cfg["d"], cfg["C"], cfg["r"], code)
+    b = O.budget(cfg["r"], cfg["C"])
+    assert cap == max(b, min(cfg["B"], cfg["C"]))
+    # Dominated by the quantised cosines [B x cap] and the sampler keys [C].
+    elt = 4 if code == pfc.PFC_F32 else 2
+    assert nbytes >= cfg["B"] * cap * elt + cfg["C"] * 12
+    assert nbytes < 2 * (cfg["B"] * cap * elt + cfg["C"] * 12) + (256 << 20)
+
+
+def test_capacity_when_positives_exceed_budget():
+    _, cap = pfc.pfc_workspace_bytes(512, 128, 1000, 0.05, pfc.PFC_BF16)
+    assert cap == 512                     # max(b = 50, min(B, C) = 512)
+    _, cap = pfc.pfc_workspace_bytes(4, 128, 3, 0.5, pfc.PFC_BF16)
+    assert cap == 3
+
+
+@pytest.mark.parametrize("args,status", [
+    ((0, 128, 100, 0.1, 1), pfc.PFC_ERR_INVALID_ARG),      # B = 0
+    ((8, 0, 100, 0.1, 1), pfc.PFC_ERR_INVALID_ARG),        # d = 0
+    ((8, 12, 100, 0.1, 0), pfc.PFC_ERR_INVALID_ARG),       # d not a multiple of 8
+    ((8, 128, 0, 0.1, 1), pfc.PFC_ERR_INVALID_ARG),        # C = 0
+    ((8, 128, 100, 0.0, 1), pfc.PFC_ERR_INVALID_ARG),      # r = 0
+    ((8, 128, 100, 1.5, 1), pfc.PFC_ERR_INVALID_ARG),      # r > 1
+    ((8, 128, 100, float("nan"), 1), pfc.PFC_ERR_INVALID_ARG),
+    ((8, 128, 100, 0.1, 7), pfc.PFC_ERR_UNSUPPORTED),      # unknown dtype
+    ((8, 64, 100, 0.1, 1), pfc.PFC_ERR_UNSUPPORTED),       # 16-bit path needs d % 128 == 0
+    ((8, 1024, 100, 0.1, 2), pfc.PFC_ERR_UNSUPPORTED),     # 16-bit path needs d <= 512
+    ((8192, 128, 100, 0.1, 0), pfc.PFC_ERR_UNSUPPORTED),   # fp32 path limited to B <= 4096
+])
+def test_workspace_rejects(args, status):
+    with pytest.raises(pfc.PfcError) as e:
+        pfc.pfc_workspace_bytes(*args)
+    assert e.value.status == status
+
+
+def _sample_args(**kw):
+    a = dict(labels=FAKE, B=16, C=1000, class_offset=0, r=0.1, seed=0, active=FAKE,
+             active_cap=100, n_active=FAKE, labels_mapped=FAKE, ws=FAKE, ws_bytes=1 << 30,
+             stream=0)
+    a.update(kw)
+    return a
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(labels=0), pfc.PFC_ERR_INVALID_ARG),
+    (dict(active=0), pfc.PFC_ERR_INVALID_ARG),
+    (dict(B=0), pfc.PFC_ERR_INVALID_ARG),
+    (dict(C=-1), pfc.PFC_ERR_INVALID_ARG),
+    (dict(class_offset=-5), pfc.PFC_ERR_INVALID_ARG),
+    (dict(r=0.0), pfc.PFC_ERR_INVALID_ARG),
+    (dict(active_cap=99), pfc.PFC_ERR_CAPACITY),
+    (dict(ws=0), pfc.PFC_ERR_WORKSPACE),
+    (dict(ws_bytes=1024), pfc.PFC_ERR_WORKSPACE),
+])
+def test_sample_rejects_before_launch(kw, status):
+    with pytest.raises(pfc.PfcError) as e:
+        pfc.pfc_sample(**_sample_args(**kw))
+    assert e.value.status == status
+
+
+def _fwd_args(**kw):
+    a = dict(X=FAKE, x_dtype=1, B=16, d=128, W=FAKE, w_dtype=1, C=1000, active=FAKE,
+             n_active=FAKE, active_cap=100, labels_mapped=FAKE, compute_dtype=1, s=64.0, m=0.5,
+             margin=1, loss=FAKE, row_lse=FAKE, ws=FAKE, ws_bytes=1 << 40, stream=0)
+    a.update(kw)
+    return a
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(X=0), pfc.PFC_ERR_INVALID_ARG),
+    (dict(s=0.0), pfc.PFC_ERR_INVALID_ARG),
+    (dict(s=float("inf")), pfc.PFC_ERR_INVALID_ARG),
+    (dict(m=-0.1), pfc.PFC_ERR_INVALID_ARG),
+    (dict(m=3.2), pfc.PFC_ERR_INVALID_ARG),              # ArcFace margin must be < pi
+    (dict(margin=5), pfc.PFC_ERR_INVALID_ARG),
+    (dict(x_dtype=2), pfc.PFC_ERR_UNSUPPORTED),          # mixed operand types
+    (dict(active_cap=0), pfc.PFC_ERR_CAPACITY),
+    (dict(active_cap=1001), pfc.PFC_ERR_CAPACITY),
+    (dict(ws_bytes=4096), pfc.PFC_ERR_WORKSPACE),
+])
+def test_forward_rejects_before_launch(kw, status):
+    with pytest.raises(pfc.PfcError) as e:
+        pfc.pfc_forward_loss(**_fwd_args(**kw))
+    assert e.value.status == status
+
+
+def _bwd_args(**kw):
+    a = dict(X=FAKE, x_dtype=1, B=16, d=128, W=FAKE, w_dtype=1, W_master=0, momentum=FAKE,
+             C=1000, active=FAKE, n_active=FAKE, active_cap=100, labels_mapped=FAKE,
+             compute_dtype=1, s=64.0, m=0.5, margin=1, row_lse=FAKE, lr=0.1, mu=0.9, dX=FAKE,
+             ws=FAKE, ws_bytes=1 << 40, stream=0)
+    a.update(kw)
+    return a
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(momentum=0), pfc.PFC_ERR_INVALID_ARG),
+    (dict(dX=0), pfc.PFC_ERR_INVALID_ARG),
+    (dict(row_lse=0), pfc.PFC_ERR_INVALID_ARG),
+    (dict(lr=0.0), pfc.PFC_ERR_INVALID_ARG),
+    (dict(mu=1.0), pfc.PFC_ERR_INVALID_ARG),
+    (dict(mu=-0.5), pfc.PFC_ERR_INVALID_ARG),
+    (dict(d=256, x_dtype=0, w_dtype=1, compute_dtype=1), pfc.PFC_ERR_UNSUPPORTED),
+    (dict(ws=0), pfc.PFC_ERR_WORKSPACE),
+])
+def test_backward_rejects_before_launch(kw, status):
+    with pytest.raises(pfc.PfcError) as e:
+        pfc.pfc_backward_update(**_bwd_args(**kw))
+    assert e.value.status == status
+
+
+@pytest.mark.skipif(torch.cuda.device_count() > 0, reason="only meaningful without a GPU")
+def test_no_device_reports_hip_error():
+    """With no HIP device the launch fails and the ABI reports PFC_ERR_HIP."""
+    with pytest.raises(pfc.PfcError) as e:
+        pfc.pfc_sample(**_sample_args())
+    assert e.value.status == pfc.PFC_ERR_HIP

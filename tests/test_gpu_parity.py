@@ -1,0 +1,146 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Integer outputs (active set, |S|, remapped labels) must match bit for bit;
+floating point within the stated bar and the derived bounds of _gpu_util.
+Sizes span several tiles of every kernel and leave ragged tails in the batch
+and in |S|.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import workloads
+from oracle import pfc_oracle as O
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2010_05222_amd import pfc  # noqa: F401  (fails loudly if libpfc.so is missing)
+    return torch.device("cuda:0")
+
+
+def _shard(B, d, C, r, dtype, margin, m, class_offset=0, dev="cuda:0"):
+    from paper_2010_05222_amd.head import PfcShard
+    return PfcShard(B, d, C, r, dtype=dtype, class_offset=class_offset, s=64.0, m=m,
+                    margin=margin, lr=0.1, mu=0.9, device=dev)
+
+
+def _case(dev, B, d, C, r, dtype, margin, m, seed, class_offset=0, label_span=None,
+          random_m=True, master=False, labels=None):
+    from _gpu_util import make_problem, run_and_compare
+    print(f"\ncase B={B} d={d} C={C} r={r} dtype={dtype} margin={margin} seed={seed} "
+          f"offset={class_offset} master={master}", flush=True)
+    Xd, Wd, Md, Pd, Ld = make_problem(B, d, C, dtype, seed, class_offset, label_span, random_m,
+                                      master, labels, dev)
+    shard = _shard(B, d, C, r, dtype, margin, m, class_offset, dev)
+    out = run_and_compare(shard, Xd, Wd, Md, Pd, Ld, seed, margin)
+    print(out, flush=True)
+    return out
+
+
+def test_tiny_workload_fp32(dev):
+    """The parity-scale workload (B=64, d=128, C=10,000, r=0.1, fp32, CosFace)."""
+    cfg = workloads.config("tiny")
+    from _gpu_util import run_and_compare
+    X, labels = workloads.make_batch(cfg, 0)
+    W = workloads.make_weights_host(cfg)
+    Xd = torch.from_numpy(X).to(dev)
+    Wd = torch.from_numpy(W).to(dev)
+    Ld = torch.from_numpy(labels).to(dev)
+    for random_m in (False, True):
+        Md = torch.from_numpy(workloads.make_momentum_host(cfg, random=random_m)).to(dev)
+        shard = _shard(cfg["B"], cfg["d"], cfg["C"], cfg["r"], "f32", cfg["margin"], cfg["m"],
+                       dev=dev)
+        out = run_and_compare(shard, Xd, Wd.clone(), Md, None, Ld, 0, cfg["margin"])
+        assert out["K"] == 1000
+        print(out, flush=True)
+
+
+@pytest.mark.parametrize("margin,m", [("cosface", 0.4), ("arcface", 0.5)])
+def test_bf16_ragged(dev, margin, m):
+    # B not a multiple of any tile; |S| = 300 not a multiple of 32/64/128.
+    _case(dev, 100, 128, 3000, 0.1, "bf16", margin, m, seed=1)
+
+
+def test_bf16_master(dev):
+    _case(dev, 96, 256, 4000, 0.2, "bf16", "arcface", 0.5, seed=2, master=True)
+
+
+def test_f16_ragged(dev):
+    _case(dev, 70, 256, 5000, 0.2, "f16", "arcface", 0.5, seed=3)
+
+
+def test_bf16_d512_several_tiles(dev):
+    _case(dev, 300, 512, 20000, 0.1, "bf16", "cosface", 0.4, seed=4, random_m=False)
+
+
+def test_f16_d512_zero_momentum(dev):
+    _case(dev, 260, 512, 12000, 0.1, "f16", "arcface", 0.5, seed=5, random_m=False)
+
+
+def test_positives_exceed_budget(dev):
+    out = _case(dev, 512, 128, 1000, 0.05, "bf16", "cosface", 0.4, seed=6)
+    assert out["K"] == out["n_pos"] > 50
+
+
+def test_r1_full_softmax(dev):
+    out = _case(dev, 64, 128, 2000, 1.0, "bf16", "arcface", 0.5, seed=7)
+    assert out["K"] == 2000
+
+
+def test_unowned_labels_and_offset(dev):
+    # Shard [1000, 3000) of a larger head; a third of the labels fall outside it.
+    _case(dev, 128, 128, 2000, 0.1, "bf16", "arcface", 0.5, seed=8, class_offset=1000,
+          label_span=(0, 4000))
+
+
+def test_no_owned_labels(dev):
+    _case(dev, 32, 128, 2000, 0.1, "bf16", "cosface", 0.4, seed=9, class_offset=5000,
+          label_span=(0, 4000))
+
+
+def test_duplicated_positives(dev):
+    rng = np.random.default_rng(10)
+    labels = rng.choice(np.array([3, 17, 17, 17, 250, 999]), size=200)
+    _case(dev, 200, 128, 1000, 0.1, "bf16", "cosface", 0.4, seed=10, labels=labels)
+
+
+def test_single_row_and_tiny_shard(dev):
+    _case(dev, 1, 128, 7, 0.5, "bf16", "arcface", 0.5, seed=11)
+
+
+def test_repeat_is_deterministic(dev):
+    """Same inputs twice: bit-identical outputs (no floating-point atomics)."""
+    from _gpu_util import make_problem
+    outs = []
+    for _ in range(2):
+        Xd, Wd, Md, Pd, Ld = make_problem(200, 256, 6000, "bf16", 12, device=dev)
+        shard = _shard(200, 256, 6000, 0.1, "bf16", "arcface", 0.5, dev=dev)
+        shard.step(Xd, Ld, Wd, Md, 12)
+        torch.cuda.synchronize()
+        outs.append((shard.loss.clone(), shard.dX.clone(), Wd.clone(), Md.clone()))
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("name", ["one_shard", "zipf", "massive"])
+def test_sampler_full_size(dev, name):
+    """Bit-exact active set and remap at the workloads' full shard sizes."""
+    cfg = workloads.config(name)
+    _, labels = workloads.make_batch(cfg, 0)
+    print(f"\nsampler {name}: B={cfg['B']} C={cfg['C']} r={cfg['r']}", flush=True)
+    shard = _shard(cfg["B"], cfg["d"], cfg["C"], cfg["r"], cfg["dtype"], cfg["margin"], cfg["m"],
+                   dev=dev)
+    Ld = torch.from_numpy(labels).to(dev)
+    shard.sample(Ld, 0)
+    torch.cuda.synchronize()
+    active_ref, mapped_ref, info = O.sample_active(labels, cfg["C"], cfg["a"], cfg["r"], 0)
+    K = int(shard.n_active.item())
+    assert K == len(active_ref) == max(O.budget(cfg["r"], cfg["C"]), info["n_pos"])
+    assert np.array_equal(shard.active[:K].cpu().numpy(), active_ref)
+    assert np.array_equal(shard.labels_mapped.cpu().numpy(), mapped_ref)
