@@ -45,8 +45,8 @@ int check_shape(int64_t B, int64_t d, int64_t C, int compute) {
   if (!dtype_ok(compute)) return PFC_ERR_UNSUPPORTED;
   if (compute == PFC_F32) {
     if (B > 4096) return PFC_ERR_UNSUPPORTED;      // fp32 path is for parity-scale problems
-  } else if (d % 128 != 0 || d > 512) {
-    return PFC_ERR_UNSUPPORTED;                    // 16-bit MFMA kernels: d in {128, ..., 512}
+  } else if (d != 128 && d != 256 && d != 512) {
+    return PFC_ERR_UNSUPPORTED;                    // 16-bit MFMA kernels: d in {128, 256, 512}
   }
   return PFC_OK;
 }
@@ -82,27 +82,30 @@ WsLayout ws_layout(int64_t B, int64_t d, int64_t C, int64_t cap, int compute) {
   L.off_grp_tie_off = take((size_t)L.n_groups * 4);
   L.sample_bytes = off;
 
-  L.ldb = round_up(B, 32);
   L.ld_cos = round_up(cap, 256);
-  L.n_ctiles = ceil_div(cap, 128);
+  L.n_ctiles = ceil_div(cap, kFwdClassTile);
   if (compute == PFC_F32) {
     L.n_split = 1;
   } else {
-    const int64_t n_rt = ceil_div(B, 64);
+    // Split-K of the feature-gradient contraction: ~256 workgroups of
+    // 128 batch rows, one per CU.
+    const int64_t n_rt = ceil_div(B, 128);
     const int64_t chunks = ceil_div(cap, 32);
-    int64_t ns = ceil_div(768, n_rt);
+    int64_t ns = ceil_div(256, n_rt);
     ns = ns > chunks ? chunks : ns;
     L.n_split = (int)(ns < 1 ? 1 : ns);
   }
   const size_t cos_elt = compute == PFC_F32 ? 4 : 2;
   L.off_inv_x = take((size_t)B * 4);
-  L.off_xT = take(compute == PFC_F32 ? 0 : (size_t)d * L.ldb * 2);
+  L.off_xb = take(compute == PFC_F32 ? 0 : (size_t)B * d * 2);
+  L.off_wmax = take(4);
   L.off_inv_w = take((size_t)L.ld_cos * 4);
   L.off_cos = take((size_t)B * L.ld_cos * cos_elt);
   L.off_stats = take((size_t)B * L.n_ctiles * 8);
   L.off_tgt = take((size_t)B * 4);
   L.off_dx = take((size_t)L.n_split * B * d * 4);
   L.off_loss = take((size_t)B * 4);
+  L.off_rec = take((size_t)B * 16);
   L.bytes = off;
   return L;
 }
@@ -126,8 +129,8 @@ StepWs step_ws(void* ws, const WsLayout& L) {
   char* b = (char*)ws;
   StepWs w;
   w.inv_x = (float*)(b + L.off_inv_x);
-  w.xT = b + L.off_xT;
-  w.ldb = L.ldb;
+  w.xb = b + L.off_xb;
+  w.inv_w_max = (float*)(b + L.off_wmax);
   w.inv_w = (float*)(b + L.off_inv_w);
   w.cosq = b + L.off_cos;
   w.ld_cos = L.ld_cos;
@@ -137,6 +140,7 @@ StepWs step_ws(void* ws, const WsLayout& L) {
   w.dx_part = (float*)(b + L.off_dx);
   w.n_split = L.n_split;
   w.loss_part = (float*)(b + L.off_loss);
+  w.row_rec = (float4*)(b + L.off_rec);
   return w;
 }
 

@@ -3,215 +3,377 @@
 // (Partial FC Eq. proxy_update, Eq. pfc_center_update, Sec. 3.2.1 matrix form:
 // G = (P - Y)/B, dW = X^T G, dX = G W^T, restricted to the active set S).
 //
-// The softmax gradient is rebuilt on the fly from the forward's quantised
-// cosines and lse_n; its coefficient without the s/B factor is
-//   g'_{nj} = (p_{nj} - [j = y_n]) * slope_{nj}.
+// With dcos = (s/B) g and g_{nj} = (p_{nj} - [j = y_n]) * slope_{nj}, the
+// contractions run over the non-target part p_{nj} only (p <= 1, which keeps
+// the 16-bit operands in range), rebuilt on the fly from the forward's
+// quantised cosines and lse_n.  The single target term of each row,
+// (p_t - 1) * slope_t, is added exactly in fp32 outside the MFMA loops.
 //
-// dX (k_dx16): split-K MFMA GEMM, dX_hat^T[i][n] = sum_j W[S_j][i] *
-//   (g'_{nj} / ||w_j||).  A workgroup owns 64 batch rows x all of d and a slice
-//   of the classes; the gathered W rows are transposed into LDS so both MFMA
-//   operands are contiguous along the class axis.  Split partials are summed
-//   in a fixed order by k_dx_final, which also applies the normalisation
-//   backward of x.
-// dW + update (k_dw16): a workgroup owns 64 active classes x all of d and
-//   reduces over the whole batch (dW_hat_j = sum_n g'_{nj} x_hat_n), so its
-//   epilogue has complete rows: tangent projection, momentum, weight step
-//   and the scatter back into the persistent W / momentum rows (unique rows,
-//   no atomics).  Runs after k_dx16, which still reads the old W.
-#include "pfc_device.h"
+// dX (k_dx16): split-K MFMA contraction over classes, dX_hat^T[i][n] =
+//   sum_j W[S_j][i] * p_{nj} / ||w_j||.  A workgroup owns 128 batch rows x all
+//   of d and a slice of the classes.  The gathered W rows go straight from
+//   HBM into a three-stage LDS ring (direct-to-LDS loads) and are read as MFMA
+//   operands with transposing LDS reads, so they are never staged in
+//   registers.  k_dx_final sums the split partials in a fixed order, adds the
+//   target terms and applies the normalisation backward of x.
+// dW + update (k_dw16): a workgroup owns 128 active classes x all of d and
+//   reduces over the whole batch, so its epilogue has complete rows: target
+//   terms, tangent projection, momentum, weight step and the scatter into the
+//   persistent W / momentum rows (unique rows, no atomics).  It runs after
+//   the dX kernels, which read the old W.
+#include "pfc_gemm.h"
 
 namespace pfc {
 namespace {
 
-constexpr int kDMax = 512;      // widest d of the 16-bit kernels
-constexpr int kDxNT = 64;       // batch rows per dX tile
-constexpr int kDxJK = 32;       // classes per reduction chunk
-constexpr int kDxLds = kDxJK + 8;
-constexpr int kDwJT = 64;       // classes per dW tile
-constexpr int kDwNK = 32;       // batch rows per reduction chunk
-constexpr int kDwLds = kDwNK + 8;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kBwKC = 32;          // reduction chunk: classes (dX) or batch rows (dW)
+constexpr int kRowLd = 528;        // LDS row stride of a DMA'd row of up to 512 (1 KB + 32 B)
+constexpr int kRowStage = kBwKC * kRowLd;
+constexpr int kDxRows = 128;       // batch rows of a dX workgroup
+constexpr int kDwCls = 128;        // classes of a dW workgroup
+constexpr int kGLd = kDwCls + 16;  // LDS row stride of the dW coefficient tile (288 B)
+
+// Every operand reaches LDS through direct-to-LDS loads into three-stage
+// rings (one array per stage, so the compiler can keep later stages in
+// flight while a stage is read); the coefficient producer reads the raw
+// quantised cosines from LDS and writes the 16-bit MFMA operand back to LDS.
+//
+// dX: W rows, raw cosines [128 rows x 32 classes], 1/||w|| of the chunk, and
+// the coefficient tile (K-major, 64-byte rows).
+__shared__ __attribute__((aligned(1024))) uint16_t xW0[kRowStage], xW1[kRowStage], xW2[kRowStage];
+__shared__ __attribute__((aligned(1024))) int16_t xR0[kDxRows * kBwKC], xR1[kDxRows * kBwKC],
+    xR2[kDxRows * kBwKC];
+__shared__ __attribute__((aligned(16))) float xI0[kBwKC], xI1[kBwKC], xI2[kBwKC];
+__shared__ __attribute__((aligned(1024))) uint16_t xG0[kDxRows * kBwKC], xG1[kDxRows * kBwKC],
+    xG2[kDxRows * kBwKC];
+// dW: X rows (bf16), raw cosines [32 rows x 128 classes], per-row records
+// (lse log2 e, 1/||x||, label, -), and the coefficient tile (MN-major).
+__shared__ __attribute__((aligned(1024))) uint16_t wX0[kRowStage], wX1[kRowStage], wX2[kRowStage];
+__shared__ __attribute__((aligned(1024))) int16_t wR0[kBwKC * kDwCls], wR1[kBwKC * kDwCls],
+    wR2[kBwKC * kDwCls];
+__shared__ __attribute__((aligned(16))) float4 wQ0[kBwKC], wQ1[kBwKC], wQ2[kBwKC];
+__shared__ __attribute__((aligned(1024))) uint16_t wG0[kBwKC * kGLd], wG1[kBwKC * kGLd],
+    wG2[kBwKC * kGLd];
+__shared__ float wDot[4][kDwCls];
+
+#define PFC_STAGE3(name, T, a0, a1, a2)          \
+  template <int S>                               \
+  __device__ __forceinline__ T* name() {         \
+    if constexpr (S == 0) return a0;             \
+    else if constexpr (S == 1) return a1;        \
+    else return a2;                              \
+  }
+PFC_STAGE3(dx_w, uint16_t, xW0, xW1, xW2)
+PFC_STAGE3(dx_r, int16_t, xR0, xR1, xR2)
+PFC_STAGE3(dx_i, float, xI0, xI1, xI2)
+PFC_STAGE3(dx_g, uint16_t, xG0, xG1, xG2)
+PFC_STAGE3(dw_x, uint16_t, wX0, wX1, wX2)
+PFC_STAGE3(dw_r, int16_t, wR0, wR1, wR2)
+PFC_STAGE3(dw_q, float4, wQ0, wQ1, wQ2)
+PFC_STAGE3(dw_g, uint16_t, wG0, wG1, wG2)
+#undef PFC_STAGE3
 
 template <typename Tag>
-__device__ __forceinline__ uint16_t to_bf16_bits(uint16_t h);
-template <>
-__device__ __forceinline__ uint16_t to_bf16_bits<Bf16Tag>(uint16_t h) { return h; }
-template <>
-__device__ __forceinline__ uint16_t to_bf16_bits<F16Tag>(uint16_t h) {
-  return float_to_bf16(f16_to_float(h));
+__device__ __forceinline__ float load16(const void* p, int64_t idx) {
+  return to_float<Tag>(((const uint16_t*)p)[idx]);
 }
 
 __device__ __forceinline__ uint16_t u16_at(const uint4& v, int e) {
   return reinterpret_cast<const uint16_t*>(&v)[e];
 }
 
+// Non-target softmax probability from a quantised cosine, in base 2:
+// p = 2^(q * s log2(e) / 32767 - lse log2(e)).
+__device__ __forceinline__ float p_of(int16_t q, float s2q, float lse2) {
+  return __builtin_amdgcn_exp2f(fmaf((float)q, s2q, -lse2));
+}
+
+// Target term of a row, (p_t - 1) * slope_t, from the quantised target cosine.
+__device__ __forceinline__ float target_coef(const Margin& mg, int16_t q, float lse) {
+  const float c = dequantise_cos(q);
+  const float p = __expf(target_logit(mg, c) - lse);
+  return (p - 1.0f) * target_slope(mg, c);
+}
+
+// Scale of the fp16 coefficient operand of dX: a power of two that keeps
+// p / ||w_j|| * scale inside the fp16 range for every active class (p <= 1).
+__device__ __forceinline__ float dx_operand_scale(F16Tag, float inv_w_max) {
+  return exp2f(floorf(log2f(60000.0f / fmaxf(inv_w_max, 1e-30f))));
+}
+__device__ __forceinline__ float dx_operand_scale(Bf16Tag, float) { return 1.0f; }
+
 template <typename Tag>
-__global__ void __launch_bounds__(256) k_dx16(
-    const uint16_t* __restrict__ W, const int32_t* __restrict__ active,
-    const int32_t* __restrict__ n_active_p, const int32_t* __restrict__ yhat,
-    const float* __restrict__ row_lse, const float* __restrict__ inv_w,
-    const int16_t* __restrict__ cosq, int64_t ld_cos, int B, int d, int n_rt, int n_split,
-    int64_t n_tiles, int64_t per_xcd, Margin mg, float* __restrict__ dx_part) {
-  // The batch-row tiles of one split share its class range: keep them on one XCD.
-  const int64_t t = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-  if (t >= n_tiles) return;
-  const int split = (int)(t / n_rt);
-  const int rt = (int)(t % n_rt);
-  const int n0 = rt * kDxNT;
-  const int K = *n_active_p;
-  const int64_t n_chunks = ceil_div((int64_t)K, (int64_t)kDxJK);
-  const int64_t per = ceil_div(n_chunks, (int64_t)n_split);
-  const int64_t c_begin = split * per;
-  const int64_t c_end = c_begin + per < n_chunks ? c_begin + per : n_chunks;
+__device__ __forceinline__ uint32_t pack2(float a, float b) {
+  return (uint32_t)from_float<Tag>(a) | ((uint32_t)from_float<Tag>(b) << 16);
+}
 
-  __shared__ __attribute__((aligned(16))) uint16_t Wt[kDMax * kDxLds];   // [i][j]
-  __shared__ __attribute__((aligned(16))) uint16_t A1[kDxNT * kDxLds];   // [n][j]
+template <typename Tag>
+__device__ __forceinline__ uint4 pack8(const float (&v)[8]) {
+  uint4 o;
+  o.x = pack2<Tag>(v[0], v[1]);
+  o.y = pack2<Tag>(v[2], v[3]);
+  o.z = pack2<Tag>(v[4], v[5]);
+  o.w = pack2<Tag>(v[6], v[7]);
+  return o;
+}
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int half = lane >> 5, l32 = lane & 31;
-  // W-load role: 8 columns of d, two groups of 4 consecutive classes.
-  const int colchunk = tid & 63;
-  const bool col_ok = colchunk * 8 < d;
-  const int quad0 = tid >> 6;
-  // Coefficient role: one batch row, 8 consecutive classes.
-  const int rl = tid >> 2;
-  const int jc = (tid & 3) * 8;
-  const int rn = n0 + rl;
-  const bool rvalid = rn < B;
-  const float lse_n = rvalid ? row_lse[rn] : 0.0f;
-  const int yh = rvalid ? yhat[rn] : -1;
+// An MFMA operand from the two halves of a transposing read pair.
+__device__ __forceinline__ uint4 frag_of(const u32x2_t& lo, const u32x2_t& hi) {
+  return make_uint4(lo.x, lo.y, hi.x, hi.y);
+}
+__device__ __forceinline__ uint4 as_uint4(const u32x4_t& v) { return make_uint4(v.x, v.y, v.z, v.w); }
 
-  const uint4 zero = make_uint4(0, 0, 0, 0);
-  uint4 wv[2][4];
-  uint4 cq;
-  float4 iw0, iw1;
-  auto gload = [&](int64_t c) {
-    const int64_t jb = c * kDxJK;
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int64_t jj = jb + 4 * (quad0 + 4 * u) + e;
-        wv[u][e] = (jj < K && col_ok)
-                       ? *reinterpret_cast<const uint4*>(W + (int64_t)active[jj] * d + 8 * colchunk)
-                       : zero;
-      }
-    const bool cvalid = rvalid && jb + jc < K;
-    cq = cvalid ? *reinterpret_cast<const uint4*>(cosq + (int64_t)rn * ld_cos + jb + jc) : zero;
-    iw0 = *reinterpret_cast<const float4*>(inv_w + jb + jc);
-    iw1 = *reinterpret_cast<const float4*>(inv_w + jb + jc + 4);
-  };
-  auto swrite = [&](int64_t c) {
-    const int64_t jb = c * kDxJK;
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int e8 = 0; e8 < 8; ++e8) {
-        uint2 p;
-        p.x = (uint32_t)to_bf16_bits<Tag>(u16_at(wv[u][0], e8)) |
-              ((uint32_t)to_bf16_bits<Tag>(u16_at(wv[u][1], e8)) << 16);
-        p.y = (uint32_t)to_bf16_bits<Tag>(u16_at(wv[u][2], e8)) |
-              ((uint32_t)to_bf16_bits<Tag>(u16_at(wv[u][3], e8)) << 16);
-        *reinterpret_cast<uint2*>(&Wt[(8 * colchunk + e8) * kDxLds + 4 * (quad0 + 4 * u)]) = p;
-      }
-    const float iwv[8] = {iw0.x, iw0.y, iw0.z, iw0.w, iw1.x, iw1.y, iw1.z, iw1.w};
-    uint16_t o[8];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int64_t j = jb + jc + k;
-      float coef = 0.0f;
-      if (rvalid && j < K) {
-        const float cd = dequantise_cos((int16_t)u16_at(cq, k));
-        coef = grad_coef(mg, cd, j == yh, lse_n) * iwv[k];
-      }
-      o[k] = float_to_bf16(coef);
-    }
-    uint4 ov;
-    __builtin_memcpy(&ov, o, 16);
-    *reinterpret_cast<uint4*>(&A1[rl * kDxLds + jc]) = ov;
-  };
-
-  f32x16_t acc[4][2];
+template <typename T>
+__device__ __forceinline__ void zero_acc(T (&acc)[4][2]) {
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.0f;
-  const int i_base = wave * 128;
+}
 
-  if (c_begin < c_end) gload(c_begin);
-  for (int64_t c = c_begin; c < c_end; ++c) {
-    swrite(c);
-    __syncthreads();
-    if (c + 1 < c_end) gload(c + 1);
-    if (i_base < d) {
+// ------------------------------------------------------------------ dX
+
+// D = 128 * WI; 2 * WI waves: wave (wi, wn) owns d entries [128 wi, +128) and
+// batch rows [64 wn, +64) of the workgroup's 128 (4 x 2 MFMA blocks).
+// Pipeline per chunk c (32 classes): the raw cosines and 1/||w|| of chunk
+// c + 3 and the W rows of chunk c + 2 are requested, the coefficients of
+// chunk c + 1 are produced, and chunk c is contracted.
+template <typename Tag, int WI>
+__global__ void __launch_bounds__(128 * WI) k_dx16(
+    const uint16_t* __restrict__ W, const int32_t* __restrict__ active,
+    const int32_t* __restrict__ n_active_p, const int32_t* __restrict__ yhat,
+    const float* __restrict__ row_lse, const float* __restrict__ inv_w,
+    const float* __restrict__ inv_w_max, const int16_t* __restrict__ cosq, int64_t ld_cos, int B,
+    int n_rt, int n_split, int64_t n_tiles, int64_t per_xcd, float s,
+    float* __restrict__ dx_part) {
+  constexpr int D = 128 * WI;
+  constexpr int NT = 128 * WI;              // threads
+  constexpr int NW = 2 * WI;                // waves
+  constexpr int WROWS = kBwKC / NW;         // W rows DMA'd by each wave per chunk
+  constexpr int RDMA = 8 / NW;              // 1-KB raw-cosine blocks DMA'd by each wave
+  constexpr int GROUPS = 512 / NT;          // 8-coefficient groups per thread per chunk
+  constexpr int PER_ITER = WROWS + RDMA + 1;  // DMAs a wave issues per chunk
+  const int64_t t = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  if (t >= n_tiles) return;
+  // The batch-row tiles of one split share its class range: they run on one
+  // XCD so the split's W rows are fetched from HBM once.
+  const int split = (int)(t / n_rt);
+  const int n0 = (int)(t % n_rt) * kDxRows;
+  const int K = *n_active_p;
+  const int64_t n_chunks = ceil_div((int64_t)K, (int64_t)kBwKC);
+  const int64_t per = ceil_div(n_chunks, (int64_t)n_split);
+  const int64_t c_begin = split * per;
+  const int64_t c_end = c_begin + per < n_chunks ? c_begin + per : n_chunks;
+  const int64_t c_stop =
+      c_begin + ceil_div(c_end > c_begin ? c_end - c_begin : 0, (int64_t)3) * 3;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wi = wave >> 1, wn = wave & 1;
+  const float s2q = s * kLog2e * kCosDequant;
+  const float scale = dx_operand_scale(Tag{}, *inv_w_max);
+
+  // Coefficient-producer rows of this thread (fixed for the whole kernel).
+  int prow[GROUPS], pchunk[GROUPS], pyh[GROUPS];
+  float plse2[GROUPS], pkeep[GROUPS];
 #pragma unroll
-      for (int kk = 0; kk < kDxJK / 16; ++kk) {
-        uint4 af[4], bf[2];
+  for (int u = 0; u < GROUPS; ++u) {
+    const int q = tid + NT * u;
+    prow[u] = q >> 2;
+    pchunk[u] = q & 3;
+    const int n = n0 + prow[u];
+    const bool ok = n < B;
+    pyh[u] = ok ? yhat[n] : -1;
+    plse2[u] = ok ? row_lse[n] * kLog2e : 0.0f;
+    pkeep[u] = ok ? scale : 0.0f;
+  }
+  // Raw-cosine DMA of this lane: block b holds rows 16 b .. 16 b + 15.
+  int64_t rsrc[RDMA];
 #pragma unroll
-        for (int mb = 0; mb < 4; ++mb)
-          af[mb] = *reinterpret_cast<const uint4*>(
-              &Wt[(i_base + mb * 32 + l32) * kDxLds + kk * 16 + 8 * half]);
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
-          bf[nb] = *reinterpret_cast<const uint4*>(&A1[(nb * 32 + l32) * kDxLds + kk * 16 + 8 * half]);
-#pragma unroll
-        for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-          for (int nb = 0; nb < 2; ++nb)
-            acc[mb][nb] = mfma_32x32x16(af[mb], bf[nb], acc[mb][nb], Bf16Tag{});
-      }
-    }
-    __syncthreads();
+  for (int v = 0; v < RDMA; ++v) {
+    const int r = 16 * (wave * RDMA + v) + (lane >> 2);
+    const int n = n0 + r < B ? n0 + r : B - 1;
+    rsrc[v] = (int64_t)n * ld_cos + 8 * (lane & 3);
   }
 
-  if (i_base >= d) return;
+  auto dma_raw = [&](auto st, int64_t c) {
+    constexpr int S = decltype(st)::value;
+    const int64_t jb = (c < n_chunks ? c : n_chunks - 1) * kBwKC;
+#pragma unroll
+    for (int v = 0; v < RDMA; ++v)
+      dma16(cosq + rsrc[v] + jb, dx_r<S>() + 512 * (wave * RDMA + v));
+    // 1/||w|| of the chunk's 32 classes: 8 / NW 16-byte pieces per wave.
+    if (lane < 8 / NW) dma16(inv_w + jb + 4 * (wave * (8 / NW) + lane), dx_i<S>() + 4 * wave * (8 / NW));
+  };
+  // Active-set indices of the W rows this wave DMAs for a chunk, loaded one
+  // chunk ahead of their DMA (wave-uniform: scalar loads).
+  int32_t rows_pf[WROWS];
+  auto load_rows = [&](int64_t c) {
+    const int64_t jb = c * kBwKC;
+#pragma unroll
+    for (int v = 0; v < WROWS; ++v) {
+      const int64_t j = jb + wave * WROWS + v;
+      rows_pf[v] = active[__builtin_amdgcn_readfirstlane((int)(j < K ? j : K - 1))];
+    }
+  };
+  auto dma_w = [&](auto st) {
+    constexpr int S = decltype(st)::value;
+#pragma unroll
+    for (int v = 0; v < WROWS; ++v) {
+      const int r = wave * WROWS + v;
+      if (lane < D / 8) dma16(W + (int64_t)rows_pf[v] * D + 8 * lane, dx_w<S>() + r * kRowLd);
+    }
+  };
+  auto produce = [&](auto st, int64_t c) {
+    constexpr int S = decltype(st)::value;
+    const int64_t jb = c * kBwKC;
+    const bool cvalid = c < c_end;
+#pragma unroll
+    for (int u = 0; u < GROUPS; ++u) {
+      const int64_t jg = jb + 8 * pchunk[u];
+      const int tpos = pyh[u] - (int)jg;  // the row's target, if it is one of these 8 classes
+      const uint4 q = *reinterpret_cast<const uint4*>(dx_r<S>() + prow[u] * kBwKC + 8 * pchunk[u]);
+      const float4 i0 = *reinterpret_cast<const float4*>(dx_i<S>() + 8 * pchunk[u]);
+      const float4 i1 = *reinterpret_cast<const float4*>(dx_i<S>() + 8 * pchunk[u] + 4);
+      const float iw[8] = {i0.x, i0.y, i0.z, i0.w, i1.x, i1.y, i1.z, i1.w};
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const bool keep = cvalid && tpos != e && jg + e < K;
+        v[e] = p_of((int16_t)u16_at(q, e), s2q, plse2[u]) * (keep ? iw[e] * pkeep[u] : 0.0f);
+      }
+      *reinterpret_cast<uint4*>(dx_g<S>() + k_major32_offset(prow[u], pchunk[u])) = pack8<Tag>(v);
+    }
+  };
+
+  // Per-lane byte offsets of the fragment reads (see frag_mn_major and
+  // frag_k_major32): W rows MN-major, coefficients K-major.
+  const int fg = lane >> 4, fsrc = lane & 15;
+  const uint32_t a_lane =
+      ((8 * (fg >> 1) + (fsrc >> 2)) * kRowLd + 16 * (fg & 1) + 4 * (fsrc & 3) + 128 * wi) * 2;
+  const uint32_t b_lane0 = k_major32_offset(64 * wn + (lane & 31), lane >> 5) * 2;
+  const uint32_t b_lane1 = k_major32_offset(64 * wn + (lane & 31), 2 + (lane >> 5)) * 2;
+
+  f32x16_t acc[4][2];
+  zero_acc(acc);
+
+  if (c_begin < c_stop) {
+    using S0 = std::integral_constant<int, 0>;
+    using S1 = std::integral_constant<int, 1>;
+    using S2 = std::integral_constant<int, 2>;
+    // Prologue: raw data of chunks 0..2, W rows of chunks 0, 1; coefficients of chunk 0.
+    load_rows(c_begin);
+    dma_raw(S0{}, c_begin);
+    dma_w(S0{});
+    load_rows(c_begin + 1);
+    dma_raw(S1{}, c_begin + 1);
+    dma_w(S1{});
+    load_rows(c_begin + 2);
+    dma_raw(S2{}, c_begin + 2);
+    wait_vmcnt_lgkm0<2 * (RDMA + 1) + WROWS>();
+    stage_barrier();
+    produce(S0{}, c_begin);
+    for (int64_t c = c_begin; c < c_stop; c += 3) {
+      static_for<0, 3>([&](auto uu) {
+        constexpr int u = decltype(uu)::value;
+        const int64_t cu = c + u;
+        // Landed: W rows of chunk cu, raw data of chunk cu + 1; this wave's
+        // coefficient writes of the previous iteration are complete.
+        wait_vmcnt_lgkm0<PER_ITER>();
+        stage_barrier();
+        // Fragments of chunk cu (both 16-class k-steps) are requested first...
+        const uint32_t wb = lds_addr(dx_w<u>()) + a_lane;
+        const uint32_t gb0 = lds_addr(dx_g<u>()) + b_lane0;
+        const uint32_t gb1 = lds_addr(dx_g<u>()) + b_lane1;
+        u32x2_t alo[2][4], ahi[2][4];
+        u32x4_t bq[2][2];
+        static_for<0, 4>([&](auto mm) {
+          constexpr int mb = decltype(mm)::value;
+          ds_read_tr_b64<(0 * kRowLd + 32 * mb) * 2>(alo[0][mb], wb);
+          ds_read_tr_b64<(4 * kRowLd + 32 * mb) * 2>(ahi[0][mb], wb);
+        });
+        ds_read_128<0>(bq[0][0], gb0);
+        ds_read_128<32 * 64>(bq[0][1], gb0);
+        static_for<0, 4>([&](auto mm) {
+          constexpr int mb = decltype(mm)::value;
+          ds_read_tr_b64<(16 * kRowLd + 32 * mb) * 2>(alo[1][mb], wb);
+          ds_read_tr_b64<(20 * kRowLd + 32 * mb) * 2>(ahi[1][mb], wb);
+        });
+        ds_read_128<0>(bq[1][0], gb1);
+        ds_read_128<32 * 64>(bq[1][1], gb1);
+        // ... then later chunks' loads and the next coefficients, while they land.
+        dma_raw(std::integral_constant<int, u>{}, cu + 3);
+        dma_w(std::integral_constant<int, (u + 2) % 3>{});
+        load_rows(cu + 3);
+        produce(std::integral_constant<int, (u + 1) % 3>{}, cu + 1);
+        static_for<0, 2>([&](auto kq) {
+          constexpr int kk = decltype(kq)::value;
+          if constexpr (kk == 0)
+            lgkm_wait<10>(alo[0][0], alo[0][1], alo[0][2], alo[0][3], ahi[0][0], ahi[0][1],
+                          ahi[0][2], ahi[0][3], bq[0][0], bq[0][1]);
+          else
+            lgkm_wait<0>(alo[1][0], alo[1][1], alo[1][2], alo[1][3], ahi[1][0], ahi[1][1],
+                         ahi[1][2], ahi[1][3], bq[1][0], bq[1][1]);
+#pragma unroll
+          for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+            for (int nb = 0; nb < 2; ++nb)
+              acc[mb][nb] = mfma_32x32x16(frag_of(alo[kk][mb], ahi[kk][mb]), as_uint4(bq[kk][nb]),
+                                          acc[mb][nb], Tag{});
+        });
+      });
+    }
+    wait_vmcnt<0>();
+  }
+
+  const float inv_scale = 1.0f / scale;
+  const int half = lane >> 5, l32 = lane & 31;
 #pragma unroll
   for (int nb = 0; nb < 2; ++nb) {
-    const int n = n0 + nb * 32 + l32;
+    const int n = n0 + 64 * wn + 32 * nb + l32;
     if (n >= B) continue;
-    float* out = dx_part + ((int64_t)split * B + n) * d;
+    float* out = dx_part + ((int64_t)split * B + n) * D;
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int i = i_base + mb * 32 + 8 * g + 4 * half;
-        if (i < d)
-          *reinterpret_cast<float4*>(out + i) =
-              make_float4(acc[mb][nb][4 * g], acc[mb][nb][4 * g + 1], acc[mb][nb][4 * g + 2],
-                          acc[mb][nb][4 * g + 3]);
+        const int i = 128 * wi + 32 * mb + 8 * g + 4 * half;
+        *reinterpret_cast<float4*>(out + i) =
+            make_float4(acc[mb][nb][4 * g] * inv_scale, acc[mb][nb][4 * g + 1] * inv_scale,
+                        acc[mb][nb][4 * g + 2] * inv_scale, acc[mb][nb][4 * g + 3] * inv_scale);
       }
   }
 }
 
-// Sum the split partials of a row in split order and apply the normalisation
-// backward: dx = (dX_hat - x_hat (x_hat . dX_hat)) / ||x||, dX_hat = (s/B) * sum.
+// Sum the split partials of a row in split order, add the row's target term
+// g_t * W[S_t] / ||w_t||, and apply the normalisation backward:
+// dx = (dX_hat - x_hat (x_hat . dX_hat)) / ||x||, dX_hat = (s/B) * sum.
+// Also writes the row record (lse log2 e, 1/||x||, label) the dW kernel reads.
 template <typename Tag>
-__device__ __forceinline__ float load_x(const void* X, int64_t idx);
-template <>
-__device__ __forceinline__ float load_x<Bf16Tag>(const void* X, int64_t idx) {
-  return bf16_to_float(((const uint16_t*)X)[idx]);
-}
-template <>
-__device__ __forceinline__ float load_x<F16Tag>(const void* X, int64_t idx) {
-  return f16_to_float(((const uint16_t*)X)[idx]);
-}
-struct F32Tag {};
-template <>
-__device__ __forceinline__ float load_x<F32Tag>(const void* X, int64_t idx) {
-  return ((const float*)X)[idx];
-}
-
-template <typename Tag>
-__global__ void __launch_bounds__(256) k_dx_final(const float* __restrict__ dx_part, int n_split,
-                                                  const void* __restrict__ X,
-                                                  const float* __restrict__ inv_x, int B, int d,
-                                                  float sB, float* __restrict__ dX) {
-  constexpr int kMaxPer = 16;  // d <= 1024
+__global__ void __launch_bounds__(256) k_dx_final(
+    const float* __restrict__ dx_part, int n_split, const void* __restrict__ X,
+    const void* __restrict__ W, const int32_t* __restrict__ active,
+    const int32_t* __restrict__ yhat, const float* __restrict__ row_lse,
+    const float* __restrict__ inv_x, const float* __restrict__ inv_w,
+    const int16_t* __restrict__ cosq, int64_t ld_cos, int B, int d, Margin mg, float sB,
+    float* __restrict__ dX, float4* __restrict__ row_rec) {
+  constexpr int kMaxPer = 8;  // d <= 512
   const int lane = threadIdx.x & 63;
   const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (n >= B) return;
   const float ix = inv_x[n];
+  const int yt = yhat[n];
+  const float lse = row_lse[n];
+  if (lane == 0) row_rec[n] = make_float4(lse * kLog2e, ix, (float)yt, 0.0f);
+  float gt = 0.0f;
+  int64_t wbase = 0;
+  if (yt >= 0) {
+    gt = target_coef(mg, cosq[(int64_t)n * ld_cos + yt], lse) * inv_w[yt];
+    wbase = (int64_t)active[yt] * d;
+  }
   float v[kMaxPer], xh[kMaxPer];
   float dot = 0.0f;
 #pragma unroll
@@ -222,8 +384,9 @@ __global__ void __launch_bounds__(256) k_dx_final(const float* __restrict__ dx_p
     if (i < d) {
       float sum = 0.0f;
       for (int s = 0; s < n_split; ++s) sum += dx_part[((int64_t)s * B + n) * d + i];
+      if (yt >= 0) sum = fmaf(gt, load16<Tag>(W, wbase + i), sum);
       v[k] = sB * sum;
-      xh[k] = load_x<Tag>(X, (int64_t)n * d + i) * ix;
+      xh[k] = load16<Tag>(X, (int64_t)n * d + i) * ix;
       dot = fmaf(xh[k], v[k], dot);
     }
   }
@@ -235,122 +398,210 @@ __global__ void __launch_bounds__(256) k_dx_final(const float* __restrict__ dx_p
   }
 }
 
-template <typename Tag>
-__global__ void __launch_bounds__(256) k_dw16(
-    const uint16_t* __restrict__ xT, int ldb, uint16_t* __restrict__ W,
+// ------------------------------------------------------------------ dW
+
+// D = 128 * WI; 2 * WI waves: wave (wi, wj) owns d entries [128 wi, +128) and
+// classes [64 wj, +64) of the workgroup's 128.  Pipeline per chunk c (32
+// batch rows): raw cosines and row records of chunk c + 3 and X rows of chunk
+// c + 2 requested, coefficients of chunk c + 1 produced, chunk c contracted.
+template <typename Tag, int WI>
+__global__ void __launch_bounds__(128 * WI) k_dw16(
+    const uint16_t* __restrict__ xb, const void* __restrict__ X, uint16_t* __restrict__ W,
     float* __restrict__ W_master, float* __restrict__ M, const int32_t* __restrict__ active,
     const int32_t* __restrict__ n_active_p, const int32_t* __restrict__ yhat,
     const float* __restrict__ row_lse, const float* __restrict__ inv_x,
-    const float* __restrict__ inv_w, const int16_t* __restrict__ cosq, int64_t ld_cos, int B,
-    int d, Margin mg, float sB, float lr, float mu) {
+    const float* __restrict__ inv_w, const float4* __restrict__ row_rec,
+    const int16_t* __restrict__ cosq, int64_t ld_cos, int B, Margin mg, float sB, float lr,
+    float mu) {
+  constexpr int D = 128 * WI;
+  constexpr int NT = 128 * WI;
+  constexpr int NW = 2 * WI;
+  constexpr int XROWS = kBwKC / NW;     // X rows DMA'd by each wave per chunk
+  constexpr int RDMA = 8 / NW;          // 1-KB raw-cosine blocks (4 rows) per wave
+  constexpr int GROUPS = 512 / NT;
+  constexpr int PER_ITER = XROWS + RDMA + 1;
   const int K = *n_active_p;
-  const int64_t j0 = (int64_t)blockIdx.x * kDwJT;
+  const int64_t j0 = (int64_t)blockIdx.x * kDwCls;
   if (j0 >= K) return;
 
-  __shared__ __attribute__((aligned(16))) uint16_t Xs[kDMax * kDwLds];   // [i][n]
-  __shared__ __attribute__((aligned(16))) uint16_t A2[kDwJT * kDwLds];   // [j][n]
-  __shared__ float dred[4][kDwJT];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wi = wave >> 1, wj = wave & 1;
   const int half = lane >> 5, l32 = lane & 31;
-  // X-load role: 8 batch rows of 8 columns of d each.
-  const int part = tid & 3;
-  const int irow = tid >> 2;
-  // Coefficient role: one batch row, 8 consecutive classes.
-  const int rl = tid >> 3;
-  const int jc = (tid & 7) * 8;
+  const float s2q = mg.s * kLog2e * kCosDequant;
+  const int n_chunks = (int)ceil_div(B, kBwKC);
+  const int c_stop = (int)ceil_div(n_chunks, 3) * 3;
 
-  const uint4 zero = make_uint4(0, 0, 0, 0);
-  uint4 xv[8];
-  uint4 cq;
-  float lse_n = 0.0f, ix_n = 0.0f;
-  int yh = -1;
-  bool rvalid = false;
-  auto gload = [&](int n0) {
+  int prow[GROUPS], pcol[GROUPS];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int i = irow + 64 * u;
-      xv[u] = i < d ? *reinterpret_cast<const uint4*>(xT + (int64_t)i * ldb + n0 + 8 * part) : zero;
-    }
-    const int rn = n0 + rl;
-    rvalid = rn < B;
-    cq = rvalid ? *reinterpret_cast<const uint4*>(cosq + (int64_t)rn * ld_cos + j0 + jc) : zero;
-    lse_n = rvalid ? row_lse[rn] : 0.0f;
-    ix_n = rvalid ? inv_x[rn] : 0.0f;
-    yh = rvalid ? yhat[rn] : -1;
-  };
-  auto swrite = [&]() {
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int i = irow + 64 * u;
-      if (i < d) *reinterpret_cast<uint4*>(&Xs[i * kDwLds + 8 * part]) = xv[u];
-    }
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int64_t j = j0 + jc + k;
-      float coef = 0.0f;
-      if (rvalid && j < K) {
-        const float cd = dequantise_cos((int16_t)u16_at(cq, k));
-        coef = grad_coef(mg, cd, j == yh, lse_n) * ix_n;
-      }
-      A2[(jc + k) * kDwLds + rl] = float_to_bf16(coef);
-    }
-  };
-
-  f32x16_t acc[4][2];
-#pragma unroll
-  for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.0f;
-  const int i_base = wave * 128;
-
-  gload(0);
-  for (int n0 = 0; n0 < ldb; n0 += kDwNK) {
-    swrite();
-    __syncthreads();
-    if (n0 + kDwNK < ldb) gload(n0 + kDwNK);
-    if (i_base < d) {
-#pragma unroll
-      for (int kk = 0; kk < kDwNK / 16; ++kk) {
-        uint4 af[4], bf[2];
-#pragma unroll
-        for (int mb = 0; mb < 4; ++mb)
-          af[mb] = *reinterpret_cast<const uint4*>(
-              &Xs[(i_base + mb * 32 + l32) * kDwLds + kk * 16 + 8 * half]);
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
-          bf[nb] = *reinterpret_cast<const uint4*>(&A2[(nb * 32 + l32) * kDwLds + kk * 16 + 8 * half]);
-#pragma unroll
-        for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-          for (int nb = 0; nb < 2; ++nb)
-            acc[mb][nb] = mfma_32x32x16(af[mb], bf[nb], acc[mb][nb], Bf16Tag{});
-      }
-    }
-    __syncthreads();
+  for (int u = 0; u < GROUPS; ++u) {
+    const int q = tid + NT * u;
+    prow[u] = q >> 4;        // batch row within the chunk
+    pcol[u] = (q & 15) * 8;  // first of 8 classes
   }
 
+  auto dma_raw = [&](auto st, int c) {
+    constexpr int S = decltype(st)::value;
+    const int cc = c < n_chunks ? c : n_chunks - 1;
+#pragma unroll
+    for (int v = 0; v < RDMA; ++v) {
+      const int r = 4 * (wave * RDMA + v) + (lane >> 4);
+      int n = cc * kBwKC + r;
+      n = n < B ? n : B - 1;
+      dma16(cosq + (int64_t)n * ld_cos + j0 + 8 * (lane & 15), dw_r<S>() + 512 * (wave * RDMA + v));
+    }
+    const int rr = (kBwKC / NW) * wave + lane;  // row records: kBwKC / NW rows per wave
+    int nr = cc * kBwKC + rr;
+    nr = nr < B ? nr : B - 1;
+    if (lane < kBwKC / NW) dma16(row_rec + nr, dw_q<S>() + (kBwKC / NW) * wave);
+  };
+  auto dma_x = [&](auto st, int c) {
+    constexpr int S = decltype(st)::value;
+#pragma unroll
+    for (int v = 0; v < XROWS; ++v) {
+      const int r = wave * XROWS + v;
+      int n = c * kBwKC + r;
+      n = n < B ? n : B - 1;
+      if (lane < D / 8) dma16(xb + (int64_t)n * D + 8 * lane, dw_x<S>() + r * kRowLd);
+    }
+  };
+  auto produce = [&](auto st, int c) {
+    constexpr int S = decltype(st)::value;
+#pragma unroll
+    for (int u = 0; u < GROUPS; ++u) {
+      const int64_t jg = j0 + pcol[u];
+      const float4 rec = dw_q<S>()[prow[u]];
+      const bool rok = c * kBwKC + prow[u] < B;
+      const int tpos = (int)rec.z - (int)jg;
+      const uint4 q = *reinterpret_cast<const uint4*>(dw_r<S>() + prow[u] * kDwCls + pcol[u]);
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const bool keep = rok && tpos != e && jg + e < K;
+        v[e] = p_of((int16_t)u16_at(q, e), s2q, rec.x) * (keep ? rec.y : 0.0f);
+      }
+      *reinterpret_cast<uint4*>(dw_g<S>() + prow[u] * kGLd + pcol[u]) = pack8<Bf16Tag>(v);
+    }
+  };
+
+  const int fg = lane >> 4, fsrc = lane & 15;
+  const uint32_t a_lane =
+      ((8 * (fg >> 1) + (fsrc >> 2)) * kRowLd + 16 * (fg & 1) + 4 * (fsrc & 3) + 128 * wi) * 2;
+  const uint32_t b_lane =
+      ((8 * (fg >> 1) + (fsrc >> 2)) * kGLd + 16 * (fg & 1) + 4 * (fsrc & 3) + 64 * wj) * 2;
+
+  f32x16_t acc[4][2];
+  zero_acc(acc);
+
+  {
+    using S0 = std::integral_constant<int, 0>;
+    using S1 = std::integral_constant<int, 1>;
+    using S2 = std::integral_constant<int, 2>;
+    dma_raw(S0{}, 0);
+    dma_x(S0{}, 0);
+    dma_raw(S1{}, 1);
+    dma_x(S1{}, 1);
+    dma_raw(S2{}, 2);
+    wait_vmcnt_lgkm0<2 * (RDMA + 1) + XROWS>();
+    stage_barrier();
+    produce(S0{}, 0);
+  }
+  for (int c = 0; c < c_stop; c += 3) {
+    static_for<0, 3>([&](auto uu) {
+      constexpr int u = decltype(uu)::value;
+      const int cu = c + u;
+      // Landed: X rows of chunk cu, raw data of chunk cu + 1; this wave's
+      // coefficient writes of the previous iteration are complete.
+      wait_vmcnt_lgkm0<PER_ITER>();
+      stage_barrier();
+      const uint32_t xbs = lds_addr(dw_x<u>()) + a_lane;
+      const uint32_t gbs = lds_addr(dw_g<u>()) + b_lane;
+      u32x2_t alo[2][4], ahi[2][4], blo[2][2], bhi[2][2];
+      static_for<0, 2>([&](auto kq) {
+        constexpr int kk = decltype(kq)::value;
+        static_for<0, 4>([&](auto mm) {
+          constexpr int mb = decltype(mm)::value;
+          ds_read_tr_b64<((16 * kk) * kRowLd + 32 * mb) * 2>(alo[kk][mb], xbs);
+          ds_read_tr_b64<((16 * kk + 4) * kRowLd + 32 * mb) * 2>(ahi[kk][mb], xbs);
+        });
+        static_for<0, 2>([&](auto nn) {
+          constexpr int nb = decltype(nn)::value;
+          ds_read_tr_b64<((16 * kk) * kGLd + 32 * nb) * 2>(blo[kk][nb], gbs);
+          ds_read_tr_b64<((16 * kk + 4) * kGLd + 32 * nb) * 2>(bhi[kk][nb], gbs);
+        });
+      });
+      dma_raw(std::integral_constant<int, u>{}, cu + 3);
+      dma_x(std::integral_constant<int, (u + 2) % 3>{}, cu + 2);
+      produce(std::integral_constant<int, (u + 1) % 3>{}, cu + 1);
+      static_for<0, 2>([&](auto kq) {
+        constexpr int kk = decltype(kq)::value;
+        if constexpr (kk == 0)
+          lgkm_wait<12>(alo[0][0], alo[0][1], alo[0][2], alo[0][3], ahi[0][0], ahi[0][1],
+                        ahi[0][2], ahi[0][3], blo[0][0], blo[0][1], bhi[0][0], bhi[0][1]);
+        else
+          lgkm_wait<0>(alo[1][0], alo[1][1], alo[1][2], alo[1][3], ahi[1][0], ahi[1][1],
+                       ahi[1][2], ahi[1][3], blo[1][0], blo[1][1], bhi[1][0], bhi[1][1]);
+        if (cu < n_chunks) {
+#pragma unroll
+          for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+            for (int nb = 0; nb < 2; ++nb)
+              acc[mb][nb] = mfma_32x32x16(frag_of(alo[kk][mb], ahi[kk][mb]),
+                                          frag_of(blo[kk][nb], bhi[kk][nb]), acc[mb][nb],
+                                          Bf16Tag{});
+        }
+      });
+    });
+  }
+  wait_vmcnt<0>();
+
   // ---- epilogue: lane owns class j (per nb) and 64 of its d entries.
+  // Target terms of the rows labelled with one of this wave's 64 classes.
+  const int64_t jw = j0 + 64 * wj;
+  for (int nbase = 0; nbase < B; nbase += 64) {
+    const int n = nbase + lane;
+    const int yv = n < B ? yhat[n] : -1;
+    uint64_t mask = __ballot(yv >= jw && yv < jw + 64);
+    while (mask) {
+      const int bit = __ffsll((unsigned long long)mask) - 1;
+      mask &= mask - 1;
+      const int nn = nbase + bit;
+      const int yt = __shfl(yv, bit, 64);
+      const float gt = target_coef(mg, cosq[(int64_t)nn * ld_cos + yt], row_lse[nn]) * inv_x[nn];
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) {
+        if (jw + 32 * nb + l32 != yt) continue;
+#pragma unroll
+        for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+          for (int g = 0; g < 4; ++g)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const int i = 128 * wi + 32 * mb + 8 * g + 4 * half + e;
+              acc[mb][nb][4 * g + e] =
+                  fmaf(gt, load16<Tag>(X, (int64_t)nn * D + i), acc[mb][nb][4 * g + e]);
+            }
+      }
+    }
+  }
+
   int64_t arow[2];
   float iwj[2];
   bool jvalid[2];
 #pragma unroll
   for (int nb = 0; nb < 2; ++nb) {
-    const int64_t j = j0 + nb * 32 + l32;
+    const int64_t j = jw + 32 * nb + l32;
     jvalid[nb] = j < K;
     arow[nb] = jvalid[nb] ? (int64_t)active[j] : 0;
     iwj[nb] = jvalid[nb] ? inv_w[j] : 0.0f;
     float dot = 0.0f;
-    if (jvalid[nb] && i_base < d) {
-      const uint16_t* wrow = W + arow[nb] * d;
+    if (jvalid[nb]) {
+      const uint16_t* wrow = W + arow[nb] * D;
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const int i = i_base + mb * 32 + 8 * g + 4 * half;
-          if (i >= d) continue;
+          const int i = 128 * wi + 32 * mb + 8 * g + 4 * half;
           const uint2 w4 = *reinterpret_cast<const uint2*>(wrow + i);
           const uint16_t* wh = reinterpret_cast<const uint16_t*>(&w4);
 #pragma unroll
@@ -359,24 +610,24 @@ __global__ void __launch_bounds__(256) k_dw16(
         }
     }
     dot += __shfl_xor(dot, 32, 64);
-    if (half == 0) dred[wave][nb * 32 + l32] = dot;
+    if (half == 0) wDot[wi][64 * wj + 32 * nb + l32] = dot;
   }
   __syncthreads();
-  if (i_base >= d) return;
 #pragma unroll
   for (int nb = 0; nb < 2; ++nb) {
     if (!jvalid[nb]) continue;
-    const int jl = nb * 32 + l32;
-    const float dot = dred[0][jl] + dred[1][jl] + dred[2][jl] + dred[3][jl];
-    uint16_t* wrow = W + arow[nb] * d;
-    float* mrow = M + arow[nb] * d;
-    float* prow = W_master ? W_master + arow[nb] * d : nullptr;
+    const int jl = 64 * wj + 32 * nb + l32;
+    float dot = 0.0f;
+#pragma unroll
+    for (int w = 0; w < WI; ++w) dot += wDot[w][jl];
+    uint16_t* wrow = W + arow[nb] * D;
+    float* mrow = M + arow[nb] * D;
+    float* prow_m = W_master ? W_master + arow[nb] * D : nullptr;
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int i = i_base + mb * 32 + 8 * g + 4 * half;
-        if (i >= d) continue;
+        const int i = 128 * wi + 32 * mb + 8 * g + 4 * half;
         const uint2 w4 = *reinterpret_cast<const uint2*>(wrow + i);
         const uint16_t* wh = reinterpret_cast<const uint16_t*>(&w4);
         float4 m4 = *reinterpret_cast<const float4*>(mrow + i);
@@ -384,13 +635,13 @@ __global__ void __launch_bounds__(256) k_dw16(
         float wnew[4];
         float4 p4;
         float* pv = reinterpret_cast<float*>(&p4);
-        if (prow) p4 = *reinterpret_cast<const float4*>(prow + i);
+        if (prow_m) p4 = *reinterpret_cast<const float4*>(prow_m + i);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const float w = to_float<Tag>(wh[e]);
           const float gr = iwj[nb] * (sB * acc[mb][nb][4 * g + e] - w * iwj[nb] * dot);
           mv[e] = mu * mv[e] + gr;
-          if (prow) {
+          if (prow_m) {
             pv[e] = pv[e] - lr * mv[e];
             wnew[e] = pv[e];
           } else {
@@ -398,10 +649,10 @@ __global__ void __launch_bounds__(256) k_dw16(
           }
         }
         *reinterpret_cast<float4*>(mrow + i) = m4;
-        if (prow) *reinterpret_cast<float4*>(prow + i) = p4;
+        if (prow_m) *reinterpret_cast<float4*>(prow_m + i) = p4;
         uint2 o;
-        o.x = (uint32_t)from_float<Tag>(wnew[0]) | ((uint32_t)from_float<Tag>(wnew[1]) << 16);
-        o.y = (uint32_t)from_float<Tag>(wnew[2]) | ((uint32_t)from_float<Tag>(wnew[3]) << 16);
+        o.x = pack2<Tag>(wnew[0], wnew[1]);
+        o.y = pack2<Tag>(wnew[2], wnew[3]);
         *reinterpret_cast<uint2*>(wrow + i) = o;
       }
   }
@@ -430,6 +681,36 @@ __global__ void __launch_bounds__(256) k_dx32(const float* __restrict__ W,
     acc = fmaf(coef, W[(int64_t)active[j] * d + i], acc);
   }
   out[(int64_t)n * d + i] = acc;
+}
+
+__global__ void __launch_bounds__(256) k_dx_final32(const float* __restrict__ dx_part,
+                                                    const float* __restrict__ X,
+                                                    const float* __restrict__ inv_x, int B, int d,
+                                                    float sB, float* __restrict__ dX) {
+  constexpr int kMaxPer = 16;  // d <= 1024
+  const int lane = threadIdx.x & 63;
+  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (n >= B) return;
+  const float ix = inv_x[n];
+  float v[kMaxPer], xh[kMaxPer];
+  float dot = 0.0f;
+#pragma unroll
+  for (int k = 0; k < kMaxPer; ++k) {
+    const int i = lane + 64 * k;
+    v[k] = 0.0f;
+    xh[k] = 0.0f;
+    if (i < d) {
+      v[k] = sB * dx_part[(int64_t)n * d + i];
+      xh[k] = X[(int64_t)n * d + i] * ix;
+      dot = fmaf(xh[k], v[k], dot);
+    }
+  }
+  dot = wave_sum(dot);
+#pragma unroll
+  for (int k = 0; k < kMaxPer; ++k) {
+    const int i = lane + 64 * k;
+    if (i < d) dX[(int64_t)n * d + i] = ix * (v[k] - xh[k] * dot);
+  }
 }
 
 __global__ void __launch_bounds__(256) k_dw32(const float* __restrict__ X, float* __restrict__ W,
@@ -489,6 +770,43 @@ __global__ void __launch_bounds__(256) k_dw32(const float* __restrict__ X, float
   }
 }
 
+template <typename Tag, int WI>
+void launch_bwd16(const StepArgs& a, const StepWs& w, const Margin& mg, float sB,
+                  hipStream_t stream) {
+  const int B = (int)a.B;
+  const int n_rt = (int)ceil_div(B, kDxRows);
+  const int64_t n_tiles = (int64_t)n_rt * w.n_split;
+  const int64_t per_xcd = ceil_div(n_tiles, 8);
+  timing_start(4, stream);
+  hipLaunchKernelGGL((k_dx16<Tag, WI>), dim3((unsigned)(8 * per_xcd)), dim3(128 * WI), 0, stream,
+                     (const uint16_t*)a.W, a.active, a.n_active, a.labels_mapped, a.row_lse,
+                     w.inv_w, w.inv_w_max, (const int16_t*)w.cosq, w.ld_cos, B, n_rt, w.n_split,
+                     n_tiles, per_xcd, a.s, w.dx_part);
+  timing_stop(4, stream);
+  timing_start(5, stream);
+  hipLaunchKernelGGL(k_dx_final<Tag>, dim3((unsigned)ceil_div(B, 4)), dim3(256), 0, stream,
+                     w.dx_part, w.n_split, a.X, a.W, a.active, a.labels_mapped, a.row_lse,
+                     w.inv_x, w.inv_w, (const int16_t*)w.cosq, w.ld_cos, B, (int)a.d, mg, sB,
+                     a.dX, w.row_rec);
+  timing_stop(5, stream);
+  timing_start(6, stream);
+  hipLaunchKernelGGL((k_dw16<Tag, WI>), dim3((unsigned)ceil_div(a.cap, kDwCls)), dim3(128 * WI),
+                     0, stream, (const uint16_t*)w.xb, a.X, (uint16_t*)a.W, a.W_master, a.M,
+                     a.active, a.n_active, a.labels_mapped, a.row_lse, w.inv_x, w.inv_w,
+                     w.row_rec, (const int16_t*)w.cosq, w.ld_cos, B, mg, sB, a.lr, a.mu);
+  timing_stop(6, stream);
+}
+
+template <typename Tag>
+void launch_bwd16_d(const StepArgs& a, const StepWs& w, const Margin& mg, float sB,
+                    hipStream_t stream) {
+  switch (a.d) {
+    case 128: launch_bwd16<Tag, 1>(a, w, mg, sB, stream); break;
+    case 256: launch_bwd16<Tag, 2>(a, w, mg, sB, stream); break;
+    default: launch_bwd16<Tag, 4>(a, w, mg, sB, stream); break;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_backward(const StepArgs& a, const StepWs& w, hipStream_t stream) {
@@ -502,8 +820,8 @@ hipError_t launch_backward(const StepArgs& a, const StepWs& w, hipStream_t strea
                        a.row_lse, w.inv_w, (const float*)w.cosq, w.ld_cos, B, d, mg, w.dx_part);
     timing_stop(4, stream);
     timing_start(5, stream);
-    hipLaunchKernelGGL(k_dx_final<F32Tag>, dim3((unsigned)ceil_div(B, 4)), dim3(256), 0, stream,
-                       w.dx_part, 1, a.X, w.inv_x, B, d, sB, a.dX);
+    hipLaunchKernelGGL(k_dx_final32, dim3((unsigned)ceil_div(B, 4)), dim3(256), 0, stream,
+                       w.dx_part, (const float*)a.X, w.inv_x, B, d, sB, a.dX);
     timing_stop(5, stream);
     timing_start(6, stream);
     hipLaunchKernelGGL(k_dw32, dim3((unsigned)a.cap), dim3(256), 0, stream, (const float*)a.X,
@@ -511,47 +829,11 @@ hipError_t launch_backward(const StepArgs& a, const StepWs& w, hipStream_t strea
                        a.row_lse, w.inv_x, w.inv_w, (const float*)w.cosq, w.ld_cos, B, d, mg, sB,
                        a.lr, a.mu);
     timing_stop(6, stream);
-    return hipGetLastError();
-  }
-  const int n_rt = (int)ceil_div(B, kDxNT);
-  const int64_t n_tiles = (int64_t)n_rt * w.n_split;
-  const int64_t per_xcd = ceil_div(n_tiles, 8);
-  const unsigned dx_grid = (unsigned)(8 * per_xcd);
-  const unsigned dw_grid = (unsigned)ceil_div(a.cap, kDwJT);
-  if (a.dtype == 1) {
-    timing_start(4, stream);
-    hipLaunchKernelGGL(k_dx16<Bf16Tag>, dim3(dx_grid), dim3(256), 0, stream,
-                       (const uint16_t*)a.W, a.active, a.n_active, a.labels_mapped, a.row_lse,
-                       w.inv_w, (const int16_t*)w.cosq, w.ld_cos, B, d, n_rt, w.n_split, n_tiles,
-                       per_xcd, mg, w.dx_part);
-    timing_stop(4, stream);
-    timing_start(5, stream);
-    hipLaunchKernelGGL(k_dx_final<Bf16Tag>, dim3((unsigned)ceil_div(B, 4)), dim3(256), 0, stream,
-                       w.dx_part, w.n_split, a.X, w.inv_x, B, d, sB, a.dX);
-    timing_stop(5, stream);
-    timing_start(6, stream);
-    hipLaunchKernelGGL(k_dw16<Bf16Tag>, dim3(dw_grid), dim3(256), 0, stream,
-                       (const uint16_t*)w.xT, (int)w.ldb, (uint16_t*)a.W, a.W_master, a.M,
-                       a.active, a.n_active, a.labels_mapped, a.row_lse, w.inv_x, w.inv_w,
-                       (const int16_t*)w.cosq, w.ld_cos, B, d, mg, sB, a.lr, a.mu);
+  } else if (a.dtype == 1) {
+    launch_bwd16_d<Bf16Tag>(a, w, mg, sB, stream);
   } else {
-    timing_start(4, stream);
-    hipLaunchKernelGGL(k_dx16<F16Tag>, dim3(dx_grid), dim3(256), 0, stream,
-                       (const uint16_t*)a.W, a.active, a.n_active, a.labels_mapped, a.row_lse,
-                       w.inv_w, (const int16_t*)w.cosq, w.ld_cos, B, d, n_rt, w.n_split, n_tiles,
-                       per_xcd, mg, w.dx_part);
-    timing_stop(4, stream);
-    timing_start(5, stream);
-    hipLaunchKernelGGL(k_dx_final<F16Tag>, dim3((unsigned)ceil_div(B, 4)), dim3(256), 0, stream,
-                       w.dx_part, w.n_split, a.X, w.inv_x, B, d, sB, a.dX);
-    timing_stop(5, stream);
-    timing_start(6, stream);
-    hipLaunchKernelGGL(k_dw16<F16Tag>, dim3(dw_grid), dim3(256), 0, stream,
-                       (const uint16_t*)w.xT, (int)w.ldb, (uint16_t*)a.W, a.W_master, a.M,
-                       a.active, a.n_active, a.labels_mapped, a.row_lse, w.inv_x, w.inv_w,
-                       (const int16_t*)w.cosq, w.ld_cos, B, d, mg, sB, a.lr, a.mu);
+    launch_bwd16_d<F16Tag>(a, w, mg, sB, stream);
   }
-  timing_stop(6, stream);
   return hipGetLastError();
 }
 

@@ -11,26 +11,164 @@
 // fixed point (the logits' only write), applies the margin at the target,
 // and emits one (max, sum exp) pair per (row, class tile).  A small kernel
 // merges the pairs into lse_n and the loss.
-#include "pfc_device.h"
+#include "pfc_gemm.h"
 
 namespace pfc {
 namespace {
 
-constexpr int kFwdBM = 128;                   // classes per tile
-constexpr int kFwdBN = 128;                   // batch rows per tile
-constexpr int kFwdBK = 64;                    // reduction slice of d per stage
-constexpr int kFwdLds = kFwdBK + 8;           // padded LDS row (uint16 elements)
+constexpr int kFwdBM = 256;       // classes per tile (MFMA M)
+constexpr int kFwdBN = 256;       // batch rows per tile (MFMA N)
+constexpr int kFwdKC = 32;        // slice of d per pipeline stage
+constexpr int kFwdThreads = 512;  // 8 waves: 2 (classes) x 4 (rows), 128 x 64 each
+constexpr int kFwdStage = kFwdBM * kFwdKC;  // uint16 elements per operand per stage
+constexpr float kLog2e = 1.4426950408889634f;
 
-template <typename Tag>
-__global__ void __launch_bounds__(256) k_fwd16(
+// Four-stage LDS ring per operand, one array per stage so the compiler can
+// keep the direct-to-LDS loads of later stages in flight while a stage is
+// read.  Row r of a stage holds 32 elements (64 B) as four 16-byte chunks;
+// chunk c is stored at position c ^ ((r >> 1) & 3), so the eight lanes of a
+// 16-byte LDS read that address eight consecutive rows hit distinct banks.
+__shared__ __attribute__((aligned(1024))) uint16_t fA0[kFwdStage], fA1[kFwdStage],
+    fA2[kFwdStage], fA3[kFwdStage];
+__shared__ __attribute__((aligned(1024))) uint16_t fB0[kFwdStage], fB1[kFwdStage],
+    fB2[kFwdStage], fB3[kFwdStage];
+__shared__ float2 fRed[2][kFwdBN];
+
+template <int S>
+__device__ __forceinline__ uint16_t* fwd_a() {
+  if constexpr (S == 0) return fA0;
+  else if constexpr (S == 1) return fA1;
+  else if constexpr (S == 2) return fA2;
+  else return fA3;
+}
+template <int S>
+__device__ __forceinline__ uint16_t* fwd_b() {
+  if constexpr (S == 0) return fB0;
+  else if constexpr (S == 1) return fB1;
+  else if constexpr (S == 2) return fB2;
+  else return fB3;
+}
+
+// Each wave loads rows 16*(2*wave + u) + lane/4, u = 0, 1, of both operands:
+// four 16-byte loads per thread per stage.
+template <int S>
+__device__ __forceinline__ void fwd_issue(const uint16_t* const ap[2], const uint16_t* const bp[2],
+                                          int k0, int wave) {
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    dma16(ap[u] + k0, fwd_a<S>() + (2 * wave + u) * 16 * kFwdKC);
+    dma16(bp[u] + k0, fwd_b<S>() + (2 * wave + u) * 16 * kFwdKC);
+  }
+}
+
+template <int S, typename Tag>
+__device__ __forceinline__ void fwd_compute(f32x16_t (&acc)[4][2], int wm, int wn, int lane) {
+  const uint16_t* A = fwd_a<S>();
+  const uint16_t* Bm = fwd_b<S>();
+  const int r32 = lane & 31;
+  const int sw = (lane >> 1) & 3;
+#pragma unroll
+  for (int kk = 0; kk < kFwdKC / 16; ++kk) {
+    const int pos = ((2 * kk + (lane >> 5)) ^ sw) * 8;
+    uint4 af[4], bf[2];
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+      af[mb] = *reinterpret_cast<const uint4*>(A + (128 * wm + 32 * mb + r32) * kFwdKC + pos);
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+      bf[nb] = *reinterpret_cast<const uint4*>(Bm + (64 * wn + 32 * nb + r32) * kFwdKC + pos);
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) acc[mb][nb] = mfma_32x32x16(af[mb], bf[nb], acc[mb][nb], Tag{});
+  }
+}
+
+__device__ __forceinline__ const float* iw_base(const float* inv_w, int64_t j) { return inv_w + j; }
+
+// Epilogue of one lane for one 32-row block (nb): the lane's row n and its
+// 64 classes j = jb + 32 mb + 8 g + e (jb = first class of the lane's
+// pattern, e < 4).  Stores the quantised cosines, leaves the base-2 logits
+// in acc, and returns the lane pair's (max, sum 2^(f - max)) over the
+// wave's 128 classes.  CHECK_J masks classes past |S|; CHECK_T handles a
+// target column in the lane's pattern (tpos = y - jb).
+template <bool CHECK_J, bool CHECK_T>
+__device__ __forceinline__ void fwd_epilogue_rows(f32x16_t (&acc)[4][2], int nb, float ix,
+                                                  const float* iwp, int K, int64_t jb, int tpos,
+                                                  const Margin& mg, bool nvalid, int16_t* qrow,
+                                                  float* mx_out, float* sm_out, float* tgt_out) {
+  const float s2 = mg.s * kLog2e;
+  float mx = -INFINITY;
+  float ct = 0.0f;
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int o = 32 * mb + 8 * g;
+      const float4 iw4 = *reinterpret_cast<const float4*>(iwp + o);
+      const float iwv[4] = {iw4.x, iw4.y, iw4.z, iw4.w};
+      float cv[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float c = acc[mb][nb][4 * g + e] * ix * iwv[e];
+        if (CHECK_J && jb + o + e >= K) c = 0.0f;
+        cv[e] = c;
+        float f2 = c * s2;
+        if (CHECK_J && jb + o + e >= K) f2 = -INFINITY;
+        if (CHECK_T && tpos == o + e) {
+          ct = c;
+          f2 = -INFINITY;   // the margined target logit is merged below
+        }
+        acc[mb][nb][4 * g + e] = f2;
+        mx = fmaxf(mx, f2);
+      }
+      if (nvalid) {
+        const auto q01 = __builtin_amdgcn_cvt_pknorm_i16(cv[0], cv[1]);
+        const auto q23 = __builtin_amdgcn_cvt_pknorm_i16(cv[2], cv[3]);
+        uint2 packed;
+        __builtin_memcpy(&packed.x, &q01, 4);
+        __builtin_memcpy(&packed.y, &q23, 4);
+        *reinterpret_cast<uint2*>(qrow + o) = packed;
+      }
+    }
+  }
+  float ft2 = -INFINITY;
+  if (CHECK_T && tgt_out) {
+    const float ft = target_logit(mg, ct);
+    *tgt_out = ft;
+    ft2 = ft * kLog2e;
+    mx = fmaxf(mx, ft2);
+  }
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  float sm = 0.0f;
+  if (mx != -INFINITY) {
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sm += __builtin_amdgcn_exp2f(acc[mb][nb][r] - mx);
+    if (CHECK_T && tgt_out) sm += __builtin_amdgcn_exp2f(ft2 - mx);
+  }
+  sm += __shfl_xor(sm, 32, 64);
+  *mx_out = mx;
+  *sm_out = sm;
+}
+
+// Tile: 256 active classes x 256 batch rows, the whole of d (= 32 * NK).
+// Epilogue, per (row, class): c = acc / (||x|| ||w||); the 16-bit fixed-point
+// cosine round(c * 32767) is stored once; the row's (max, sum) over the tile
+// is accumulated in base 2 from the fp32 logit s*c (the margined logit at
+// the target), and the target logit itself goes to tgt[n].
+template <typename Tag, int NK>
+__global__ void __launch_bounds__(kFwdThreads) k_fwd16(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
     const int32_t* __restrict__ active, const int32_t* __restrict__ n_active_p,
     const int32_t* __restrict__ yhat, const float* __restrict__ inv_x,
-    const float* __restrict__ inv_w, int B, int d, int64_t ld_cos, int64_t n_ctiles, int n_rt,
+    const float* __restrict__ inv_w, int B, int64_t ld_cos, int64_t n_ctiles, int n_rt,
     int64_t n_tiles, int64_t per_xcd, Margin mg, int16_t* __restrict__ cosq,
     float2* __restrict__ stats, float* __restrict__ tgt) {
-  // Tiles of one class tile (all batch-row tiles) run on the same XCD, so the
-  // gathered W rows are fetched from HBM once and re-read from that XCD's L2.
+  constexpr int D = NK * kFwdKC;
+  // All batch-row tiles of a class tile run on one XCD: the gathered W rows
+  // come from HBM once and are re-read from that XCD's L2.
   const int64_t t = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
   if (t >= n_tiles) return;
   const int64_t ct = t / n_rt;
@@ -40,144 +178,70 @@ __global__ void __launch_bounds__(256) k_fwd16(
   if (j0 >= K) return;
   const int n0 = rt * kFwdBN;
 
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][kFwdBM * kFwdLds];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][kFwdBN * kFwdLds];
-  __shared__ float2 red[2][kFwdBN];
-
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave >> 2, wn = wave & 3;
   const int half = lane >> 5, l32 = lane & 31;
 
-  const int lrow = tid >> 3;
-  const int lcol = (tid & 7) * 8;
-  const uint16_t* a_ptr[4];
-  const uint16_t* b_ptr[4];
+  // Per-lane source rows of the two DMA segments; rows past the end are
+  // clamped to a valid row (their results are masked in the epilogue).
+  const int cidx = (lane & 3) ^ ((lane >> 3) & 3);
+  const uint16_t* ap[2];
+  const uint16_t* bp[2];
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int64_t jr = j0 + lrow + 32 * q;
-    a_ptr[q] = jr < K ? W + (int64_t)active[jr] * d + lcol : nullptr;
-    const int nr = n0 + lrow + 32 * q;
-    b_ptr[q] = nr < B ? X + (int64_t)nr * d + lcol : nullptr;
+  for (int u = 0; u < 2; ++u) {
+    const int row = 16 * (2 * wave + u) + (lane >> 2);
+    const int64_t jr = j0 + row < K ? j0 + row : K - 1;
+    ap[u] = W + (int64_t)active[jr] * D + 8 * cidx;
+    const int nr = n0 + row < B ? n0 + row : B - 1;
+    bp[u] = X + (int64_t)nr * D + 8 * cidx;
   }
-  uint4 ra[4], rb[4];
-  const uint4 zero = make_uint4(0, 0, 0, 0);
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      ra[q] = a_ptr[q] ? *reinterpret_cast<const uint4*>(a_ptr[q] + k0) : zero;
-      rb[q] = b_ptr[q] ? *reinterpret_cast<const uint4*>(b_ptr[q] + k0) : zero;
-    }
-  };
-  auto swrite = [&](int s) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      *reinterpret_cast<uint4*>(&As[s][(lrow + 32 * q) * kFwdLds + lcol]) = ra[q];
-      *reinterpret_cast<uint4*>(&Bs[s][(lrow + 32 * q) * kFwdLds + lcol]) = rb[q];
-    }
-  };
 
-  f32x16_t acc[2][2];
+  f32x16_t acc[4][2];
 #pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
+  for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.0f;
 
-  const int nk = d / kFwdBK;
-  gload(0);
-  swrite(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int s = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * kFwdBK);
-#pragma unroll
-    for (int kk = 0; kk < kFwdBK / 16; ++kk) {
-      uint4 af[2], bf[2];
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-        af[mb] = *reinterpret_cast<const uint4*>(
-            &As[s][(wm * 64 + mb * 32 + l32) * kFwdLds + kk * 16 + 8 * half]);
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
-        bf[nb] = *reinterpret_cast<const uint4*>(
-            &Bs[s][(wn * 64 + nb * 32 + l32) * kFwdLds + kk * 16 + 8 * half]);
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb) acc[mb][nb] = mfma_32x32x16(af[mb], bf[nb], acc[mb][nb], Tag{});
-    }
-    if (kt + 1 < nk) swrite(s ^ 1);
-    __syncthreads();
-  }
+  fwd_issue<0>(ap, bp, 0, wave);
+  if constexpr (NK > 1) fwd_issue<1>(ap, bp, kFwdKC, wave);
+  if constexpr (NK > 2) fwd_issue<2>(ap, bp, 2 * kFwdKC, wave);
+  static_for<0, NK>([&](auto cc) {
+    constexpr int c = decltype(cc)::value;
+    constexpr int ahead = (NK - 1 - c) < 2 ? (NK - 1 - c) : 2;
+    wait_vmcnt<4 * ahead>();
+    stage_barrier();
+    if constexpr (c + 3 < NK) fwd_issue<(c + 3) & 3>(ap, bp, (c + 3) * kFwdKC, wave);
+    fwd_compute<c & 3, Tag>(acc, wm, wn, lane);
+  });
 
   // ---- epilogue
-  float iw[2][16];
-#pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int64_t j = j0 + wm * 64 + mb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-      iw[mb][r] = j < K ? inv_w[j] : 0.0f;
-    }
+  const int64_t jlo = j0 + 128 * wm;
+  const bool full = jlo + 128 <= (int64_t)K;   // wave-uniform: no class past |S|
 #pragma unroll
   for (int nb = 0; nb < 2; ++nb) {
-    const int nl = wn * 64 + nb * 32 + l32;
+    const int nl = 64 * wn + 32 * nb + l32;
     const int n = n0 + nl;
     const bool nvalid = n < B;
     const float ix = nvalid ? inv_x[n] : 0.0f;
     const int yh = nvalid ? yhat[n] : -1;
-    float fv[2][16];
-    float mx = -INFINITY;
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb) {
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        int16_t q4[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = 4 * g + e;
-          const int64_t j = j0 + wm * 64 + mb * 32 + 8 * g + 4 * half + e;
-          float f = -INFINITY;
-          int16_t q = 0;
-          if (j < K) {
-            q = quantise_cos(acc[mb][nb][r] * ix * iw[mb][r]);
-            const float c = dequantise_cos(q);
-            if (j == yh) {
-              f = target_logit(mg, c);
-              if (nvalid) tgt[n] = f;
-            } else {
-              f = mg.s * c;
-            }
-          }
-          q4[e] = q;
-          fv[mb][r] = f;
-          mx = fmaxf(mx, f);
-        }
-        if (nvalid) {
-          uint2 packed;
-          packed.x = (uint32_t)(uint16_t)q4[0] | ((uint32_t)(uint16_t)q4[1] << 16);
-          packed.y = (uint32_t)(uint16_t)q4[2] | ((uint32_t)(uint16_t)q4[3] << 16);
-          *reinterpret_cast<uint2*>(&cosq[(int64_t)n * ld_cos + j0 + wm * 64 + mb * 32 + 8 * g +
-                                          4 * half]) = packed;
-        }
-      }
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    float sm = 0.0f;
-    if (mx != -INFINITY) {
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sm += __expf(fv[mb][r] - mx);
-    }
-    sm += __shfl_xor(sm, 32, 64);
-    if (half == 0) red[wm][nl] = make_float2(mx, sm);
+    const int tpos = yh - (int)(jlo + 4 * half);   // target's offset in this lane's class pattern
+    const bool has_t = yh >= jlo && yh < jlo + 128 && ((tpos & 4) == 0);
+    int16_t* qrow = cosq + (int64_t)(nvalid ? n : 0) * ld_cos + jlo + 4 * half;
+    float mx, sm;
+    if (full && !__any(has_t))
+      fwd_epilogue_rows<false, false>(acc, nb, ix, iw_base(inv_w, jlo + 4 * half), K, jlo + 4 * half,
+                                      tpos, mg, nvalid, qrow, &mx, &sm, nullptr);
+    else
+      fwd_epilogue_rows<true, true>(acc, nb, ix, iw_base(inv_w, jlo + 4 * half), K, jlo + 4 * half,
+                                    tpos, mg, nvalid, qrow, &mx, &sm, has_t ? tgt + n : nullptr);
+    if (half == 0) fRed[wm][nl] = make_float2(mx, sm);
   }
   __syncthreads();
   if (tid < kFwdBN) {
     const int n = n0 + tid;
-    if (n < B) stats[(int64_t)n * n_ctiles + ct] = lse_merge(red[0][tid], red[1][tid]);
+    if (n < B) stats[(int64_t)n * n_ctiles + ct] = lse_merge2(fRed[0][tid], fRed[1][tid]);
   }
 }
 
@@ -193,16 +257,16 @@ __global__ void __launch_bounds__(256) k_lse16(const float2* __restrict__ stats,
   if (n >= B) return;
   const int64_t nct = ceil_div((int64_t)*n_active_p, (int64_t)kFwdBM);
   float2 acc = make_float2(-INFINITY, 0.0f);
-  for (int64_t c = lane; c < nct; c += 64) acc = lse_merge(acc, stats[(int64_t)n * n_ctiles + c]);
+  for (int64_t c = lane; c < nct; c += 64) acc = lse_merge2(acc, stats[(int64_t)n * n_ctiles + c]);
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) {
     float2 o;
     o.x = __shfl_xor(acc.x, off, 64);
     o.y = __shfl_xor(acc.y, off, 64);
-    acc = lse_merge(acc, o);
+    acc = lse_merge2(acc, o);
   }
   if (lane == 0) {
-    const float lse = acc.x + __logf(acc.y);
+    const float lse = (acc.x + log2f(acc.y)) * 0.6931471805599453f;
     row_lse[n] = lse;
     loss_part[n] = yhat[n] >= 0 ? lse - tgt[n] : 0.0f;
   }
@@ -277,6 +341,26 @@ __global__ void __launch_bounds__(1024) k_loss(const float* __restrict__ loss_pa
   }
 }
 
+template <typename Tag, int NK>
+void launch_fwd16_nk(unsigned grid, hipStream_t stream, const StepArgs& a, const StepWs& w, int B,
+                     int n_rt, int64_t n_tiles, int64_t per_xcd, const Margin& mg) {
+  hipLaunchKernelGGL((k_fwd16<Tag, NK>), dim3(grid), dim3(kFwdThreads), 0, stream,
+                     (const uint16_t*)a.X, (const uint16_t*)a.W, a.active, a.n_active,
+                     a.labels_mapped, w.inv_x, w.inv_w, B, w.ld_cos, w.n_ctiles, n_rt, n_tiles,
+                     per_xcd, mg, (int16_t*)w.cosq, w.stats, w.tgt);
+}
+
+template <typename Tag>
+void launch_fwd16(int d, unsigned grid, hipStream_t stream, const StepArgs& a, const StepWs& w,
+                  int B, int n_rt, int64_t n_tiles, int64_t per_xcd, const Margin& mg) {
+  switch (d) {
+    case 128: launch_fwd16_nk<Tag, 4>(grid, stream, a, w, B, n_rt, n_tiles, per_xcd, mg); break;
+    case 256: launch_fwd16_nk<Tag, 8>(grid, stream, a, w, B, n_rt, n_tiles, per_xcd, mg); break;
+    case 384: launch_fwd16_nk<Tag, 12>(grid, stream, a, w, B, n_rt, n_tiles, per_xcd, mg); break;
+    default: launch_fwd16_nk<Tag, 16>(grid, stream, a, w, B, n_rt, n_tiles, per_xcd, mg); break;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_forward(const StepArgs& a, const StepWs& w, hipStream_t stream) {
@@ -302,15 +386,9 @@ hipError_t launch_forward(const StepArgs& a, const StepWs& w, hipStream_t stream
     const unsigned grid = (unsigned)(8 * per_xcd);
     timing_start(2, stream);
     if (a.dtype == 1)
-      hipLaunchKernelGGL(k_fwd16<Bf16Tag>, dim3(grid), dim3(256), 0, stream,
-                         (const uint16_t*)a.X, (const uint16_t*)a.W, a.active, a.n_active,
-                         a.labels_mapped, w.inv_x, w.inv_w, B, d, w.ld_cos, w.n_ctiles, n_rt,
-                         n_tiles, per_xcd, mg, (int16_t*)w.cosq, w.stats, w.tgt);
+      launch_fwd16<Bf16Tag>(d, grid, stream, a, w, B, n_rt, n_tiles, per_xcd, mg);
     else
-      hipLaunchKernelGGL(k_fwd16<F16Tag>, dim3(grid), dim3(256), 0, stream,
-                         (const uint16_t*)a.X, (const uint16_t*)a.W, a.active, a.n_active,
-                         a.labels_mapped, w.inv_x, w.inv_w, B, d, w.ld_cos, w.n_ctiles, n_rt,
-                         n_tiles, per_xcd, mg, (int16_t*)w.cosq, w.stats, w.tgt);
+      launch_fwd16<F16Tag>(d, grid, stream, a, w, B, n_rt, n_tiles, per_xcd, mg);
     timing_stop(2, stream);
     timing_start(3, stream);
     hipLaunchKernelGGL(k_lse16, dim3((unsigned)ceil_div(B, 4)), dim3(256), 0, stream, w.stats,

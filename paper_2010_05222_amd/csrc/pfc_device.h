@@ -74,12 +74,8 @@ __device__ __forceinline__ f32x16_t mfma_32x32x16(const uint4& a, const uint4& b
   return __builtin_amdgcn_mfma_f32_32x32x16_f16(av, bv, c, 0, 0, 0);
 }
 
-// 16-bit fixed-point store of a cosine (|cos| <= 1): step 2^-15.
-__device__ __forceinline__ int16_t quantise_cos(float c) {
-  float q = rintf(c * kCosQuant);
-  q = fminf(fmaxf(q, -32767.0f), 32767.0f);
-  return (int16_t)q;
-}
+// 16-bit fixed-point cosine: q = round-to-nearest-even(clamp(c, -1, 1) * 32767)
+// (v_cvt_pknorm_i16_f32 in the forward), c ~ q / 32767.
 __device__ __forceinline__ float dequantise_cos(int16_t q) { return (float)q * kCosDequant; }
 
 // Target logit and its slope d f / d cos (divided by s).  CosFace:
@@ -123,6 +119,13 @@ __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
   return v;
+}
+
+// Merge two (max, sum 2^(. - max)) pairs (base-2 log-sum-exp).
+__device__ __forceinline__ float2 lse_merge2(float2 a, float2 b) {
+  const float mx = fmaxf(a.x, b.x);
+  if (mx == -INFINITY) return make_float2(-INFINITY, 0.0f);
+  return make_float2(mx, a.y * exp2f(a.x - mx) + b.y * exp2f(b.x - mx));
 }
 
 // Merge two (max, sum exp(. - max)) pairs.

@@ -42,24 +42,27 @@ struct SampleWs {
 
 // ----------------------------------------------------------------- step
 
-// Quantised cosine store of the 16-bit paths: q = round(cos * 2^15),
-// clamped to [-32767, 32767]; cos = q * 2^-15.
-constexpr float kCosQuant = 32768.0f;
-constexpr float kCosDequant = 1.0f / 32768.0f;
+// Quantised cosine store of the 16-bit paths: q = round(clamp(cos, -1, 1) * 32767),
+// cos ~ q / 32767 (absolute error <= 1.6e-5).
+constexpr float kCosQuant = 32767.0f;
+constexpr float kCosDequant = 1.0f / 32767.0f;
+// Class tile of the forward contraction (one softmax-statistics pair per row and tile).
+constexpr int kFwdClassTile = 256;
 
 struct StepWs {
   float* inv_x;          // [B]      1/max(||x_n||, eps)
-  void* xT;              // [d x ldb] X transposed in bf16, zero for n >= B (16-bit paths)
-  int64_t ldb;           // row stride of xT: B rounded up to 32
+  void* xb;              // [B x d] X in bf16 (operand of the class-gradient contraction)
+  float* inv_w_max;      // [1] max_j 1/||W[S_j]|| (scale of the fp16 feature-gradient operand)
   float* inv_w;          // [ld_cos] 1/max(||W[S_j]||, eps)
   void* cosq;            // [B x ld_cos] quantised cosines (int16) or fp32 cosines
   int64_t ld_cos;        // row stride of cosq: cap rounded up to 256
-  float2* stats;         // [B x n_ctiles] per class tile: (max, sum exp(f - max))
+  float2* stats;         // [B x n_ctiles] per class tile: (max, sum 2^(f log2 e - max)), base 2
   int64_t n_ctiles;      // class tiles of the forward contraction
   float* tgt;            // [B] margined target logit
   float* dx_part;        // [n_split x B x d] split-K partial sums of dX_hat
   int n_split;
   float* loss_part;      // [B] per-row loss terms
+  float4* row_rec;       // [B] (lse log2 e, 1/||x||, label, 0) for the class-gradient kernel
 };
 
 // Layout of the whole workspace (offsets in bytes from its base).
@@ -68,8 +71,9 @@ struct WsLayout {
   size_t sample_bytes;   // prefix used by the sampler
   size_t off_bitmap, off_hist, off_state, off_keys, off_cand;
   size_t off_grp_sure, off_grp_tie, off_grp_out, off_grp_tie_off;
-  size_t off_inv_x, off_xT, off_inv_w, off_cos, off_stats, off_tgt, off_dx, off_loss;
-  int64_t ldb, ld_cos, n_ctiles, n_groups;
+  size_t off_inv_x, off_xb, off_wmax, off_inv_w, off_cos, off_stats, off_tgt, off_dx, off_loss,
+      off_rec;
+  int64_t ld_cos, n_ctiles, n_groups;
   int n_split;
   int top_bits;
 };

@@ -25,47 +25,63 @@ __device__ __forceinline__ float sumsq8(const uint4& v) {
   return acc;
 }
 
-// inv_x[n] and the transposed bf16 copy xT[i * ldb + n] (zero for n >= B),
-// the K-contiguous operand of the class-gradient contraction.
+// inv_x[n] and the bf16 copy xb[n][i] of the batch (the MFMA operand of the
+// class-gradient contraction); also clears the running max of 1/||w_j||.
 template <typename Tag>
 __global__ void __launch_bounds__(256) k_prep_x16(const uint16_t* __restrict__ X, int B, int d,
-                                                  int ldb, float* __restrict__ inv_x,
-                                                  uint16_t* __restrict__ xT) {
+                                                  float* __restrict__ inv_x,
+                                                  uint16_t* __restrict__ xb,
+                                                  float* __restrict__ inv_w_max) {
   const int lane = threadIdx.x & 63;
   const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (n >= ldb) return;
-  if (n >= B) {
-    for (int i = lane; i < d; i += 64) xT[(int64_t)i * ldb + n] = 0;
-    return;
-  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) *inv_w_max = 0.0f;
+  if (n >= B) return;
   const uint16_t* row = X + (int64_t)n * d;
   float ss = 0.0f;
   for (int c = lane; c < d / 8; c += 64) {
     const uint4 v = *reinterpret_cast<const uint4*>(row + 8 * c);
     ss += sumsq8<Tag>(v);
     const uint16_t* h = reinterpret_cast<const uint16_t*>(&v);
+    uint16_t o[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e)
-      xT[(int64_t)(8 * c + e) * ldb + n] = float_to_bf16(to_float<Tag>(h[e]));
+    for (int e = 0; e < 8; ++e) o[e] = float_to_bf16(to_float<Tag>(h[e]));
+    uint4 ov;
+    __builtin_memcpy(&ov, o, 16);
+    *reinterpret_cast<uint4*>(xb + (int64_t)n * d + 8 * c) = ov;
   }
   ss = wave_sum(ss);
   if (lane == 0) inv_x[n] = 1.0f / fmaxf(sqrtf(ss), kEpsNorm);
 }
 
+// 1/||W[S_j]|| of the active rows: one wavefront per row (grid-stride), and
+// the running maximum over all rows (one atomic per workgroup).
 template <typename Tag>
 __global__ void __launch_bounds__(256) k_norm_w16(const uint16_t* __restrict__ W, int d,
                                                   const int32_t* __restrict__ active,
                                                   const int32_t* __restrict__ n_active,
-                                                  int64_t cap, float* __restrict__ inv_w) {
+                                                  int64_t cap, float* __restrict__ inv_w,
+                                                  float* __restrict__ inv_w_max) {
+  __shared__ float wmax[4];
   const int lane = threadIdx.x & 63;
-  const int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (j >= cap || j >= *n_active) return;
-  const uint16_t* row = W + (int64_t)active[j] * d;
-  float ss = 0.0f;
-  for (int c = lane; c < d / 8; c += 64)
-    ss += sumsq8<Tag>(*reinterpret_cast<const uint4*>(row + 8 * c));
-  ss = wave_sum(ss);
-  if (lane == 0) inv_w[j] = 1.0f / fmaxf(sqrtf(ss), kEpsNorm);
+  const int64_t K = *n_active < cap ? *n_active : cap;
+  float mx = 0.0f;
+  for (int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); j < K; j += (int64_t)gridDim.x * 4) {
+    const uint16_t* row = W + (int64_t)active[j] * d;
+    float ss = 0.0f;
+    for (int c = lane; c < d / 8; c += 64)
+      ss += sumsq8<Tag>(*reinterpret_cast<const uint4*>(row + 8 * c));
+    ss = wave_sum(ss);
+    const float inv = 1.0f / fmaxf(sqrtf(ss), kEpsNorm);
+    if (lane == 0) inv_w[j] = inv;
+    mx = fmaxf(mx, inv);
+  }
+  if (lane == 0) wmax[threadIdx.x >> 6] = mx;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const float m = fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]));
+    // Positive floats order like their bit patterns.
+    atomicMax(reinterpret_cast<int*>(inv_w_max), __float_as_int(m));
+  }
 }
 
 __global__ void __launch_bounds__(256) k_prep_x32(const float* __restrict__ X, int B, int d,
@@ -103,6 +119,7 @@ __global__ void __launch_bounds__(256) k_norm_w32(const float* __restrict__ W, i
 hipError_t launch_prep(const StepArgs& a, const StepWs& w, hipStream_t stream) {
   const int B = (int)a.B, d = (int)a.d;
   const unsigned wblocks = (unsigned)ceil_div(a.cap, 4);
+  const unsigned wblocks16 = (unsigned)(ceil_div(a.cap, 4) < 4096 ? ceil_div(a.cap, 4) : 4096);
   timing_start(1, stream);
   if (a.dtype == 0) {
     hipLaunchKernelGGL(k_prep_x32, dim3((unsigned)ceil_div(B, 4)), dim3(256), 0, stream,
@@ -110,15 +127,17 @@ hipError_t launch_prep(const StepArgs& a, const StepWs& w, hipStream_t stream) {
     hipLaunchKernelGGL(k_norm_w32, dim3(wblocks), dim3(256), 0, stream, (const float*)a.W, d,
                        a.active, a.n_active, a.cap, w.inv_w);
   } else if (a.dtype == 1) {
-    hipLaunchKernelGGL(k_prep_x16<Bf16Tag>, dim3((unsigned)ceil_div(w.ldb, 4)), dim3(256), 0,
-                       stream, (const uint16_t*)a.X, B, d, w.ldb, w.inv_x, (uint16_t*)w.xT);
-    hipLaunchKernelGGL(k_norm_w16<Bf16Tag>, dim3(wblocks), dim3(256), 0, stream,
-                       (const uint16_t*)a.W, d, a.active, a.n_active, a.cap, w.inv_w);
+    hipLaunchKernelGGL(k_prep_x16<Bf16Tag>, dim3((unsigned)ceil_div(B, 4)), dim3(256), 0,
+                       stream, (const uint16_t*)a.X, B, d, w.inv_x, (uint16_t*)w.xb, w.inv_w_max);
+    hipLaunchKernelGGL(k_norm_w16<Bf16Tag>, dim3(wblocks16), dim3(256), 0, stream,
+                       (const uint16_t*)a.W, d, a.active, a.n_active, a.cap, w.inv_w,
+                       w.inv_w_max);
   } else {
-    hipLaunchKernelGGL(k_prep_x16<F16Tag>, dim3((unsigned)ceil_div(w.ldb, 4)), dim3(256), 0,
-                       stream, (const uint16_t*)a.X, B, d, w.ldb, w.inv_x, (uint16_t*)w.xT);
-    hipLaunchKernelGGL(k_norm_w16<F16Tag>, dim3(wblocks), dim3(256), 0, stream,
-                       (const uint16_t*)a.W, d, a.active, a.n_active, a.cap, w.inv_w);
+    hipLaunchKernelGGL(k_prep_x16<F16Tag>, dim3((unsigned)ceil_div(B, 4)), dim3(256), 0,
+                       stream, (const uint16_t*)a.X, B, d, w.inv_x, (uint16_t*)w.xb, w.inv_w_max);
+    hipLaunchKernelGGL(k_norm_w16<F16Tag>, dim3(wblocks16), dim3(256), 0, stream,
+                       (const uint16_t*)a.W, d, a.active, a.n_active, a.cap, w.inv_w,
+                       w.inv_w_max);
   }
   timing_stop(1, stream);
   return hipGetLastError();
