@@ -33,6 +33,7 @@ constexpr int kRowStage = kBwKC * kRowLd;
 constexpr int kDxRows = 128;       // batch rows of a dX workgroup
 constexpr int kDwCls = 128;        // classes of a dW workgroup
 constexpr int kGLd = kDwCls + 16;  // LDS row stride of the dW coefficient tile (288 B)
+constexpr int kTLd = 260;         // LDS row stride (floats) of the update's staged gradient rows
 
 // Every operand reaches LDS through direct-to-LDS loads into three-stage
 // rings (one array per stage, so the compiler can keep later stages in
@@ -55,7 +56,6 @@ __shared__ __attribute__((aligned(1024))) int16_t wR0[kBwKC * kDwCls], wR1[kBwKC
 __shared__ __attribute__((aligned(16))) float4 wQ0[kBwKC], wQ1[kBwKC], wQ2[kBwKC];
 __shared__ __attribute__((aligned(1024))) uint16_t wG0[kBwKC * kGLd], wG1[kBwKC * kGLd],
     wG2[kBwKC * kGLd];
-__shared__ float wDot[4][kDwCls];
 
 #define PFC_STAGE3(name, T, a0, a1, a2)          \
   template <int S>                               \
@@ -585,76 +585,122 @@ __global__ void __launch_bounds__(128 * WI) k_dw16(
     }
   }
 
-  int64_t arow[2];
-  float iwj[2];
-  bool jvalid[2];
+  // ---- update: the tile goes through LDS in four passes of 32 classes so
+  // that each wave then owns whole rows: W, momentum and master rows are read
+  // and written in full contiguous segments.  Pass p = (pwj, pnb) holds the
+  // classes 64 pwj + 32 pnb + r (r < 32); entry d of row r sits in stage
+  // array d / 256 at r * kTLd + d % 256.  Lane l owns d = 256 h + 4 l .. + 3.
+  constexpr int NH = D > 256 ? 2 : 1;         // 256-entry halves of a row
+  constexpr int LPH = (D > 256 ? 256 : D) / 4;  // lanes that own entries
+  constexpr int RPW = 32 / NW;                // rows of a pass per wave
+  constexpr int RB = RPW < 4 ? RPW : 4;       // rows per load batch
+  float* const tlo = reinterpret_cast<float*>(wX0);
+  float* const thi = reinterpret_cast<float*>(wX1);
+  const bool lane_on = lane < LPH;
+  wait_lgkm0();
+  stage_barrier();  // every wave's fragment reads of the stage arrays are done
 #pragma unroll
-  for (int nb = 0; nb < 2; ++nb) {
-    const int64_t j = jw + 32 * nb + l32;
-    jvalid[nb] = j < K;
-    arow[nb] = jvalid[nb] ? (int64_t)active[j] : 0;
-    iwj[nb] = jvalid[nb] ? inv_w[j] : 0.0f;
-    float dot = 0.0f;
-    if (jvalid[nb]) {
-      const uint16_t* wrow = W + arow[nb] * D;
+  for (int p = 0; p < 4; ++p) {
+    const int pwj = p & 1, pnb = p >> 1;
+    float4 wv[RB][NH], mv[RB][NH], pv[RB][NH];
+    int64_t rowa[RB];
+    float iwr[RB];
+    bool rv[RB];
+    // Global loads of a batch of this wave's rows (issued before they are needed).
+    auto load_batch = [&](int b) {
+#pragma unroll
+      for (int q = 0; q < RB; ++q) {
+        const int r = wave * RPW + b * RB + q;
+        const int64_t j = j0 + 64 * pwj + 32 * pnb + r;
+        rv[q] = j < K && lane_on;
+        rowa[q] = j < K ? (int64_t)active[j] : 0;
+        iwr[q] = j < K ? inv_w[j] : 0.0f;
+#pragma unroll
+        for (int h = 0; h < NH; ++h) {
+          const int64_t off = rowa[q] * D + 256 * h + 4 * lane;
+          wv[q][h] = mv[q][h] = pv[q][h] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+          if (rv[q]) {
+            const uint2 w4 = *reinterpret_cast<const uint2*>(W + off);
+            wv[q][h] = make_float4(to_float<Tag>((uint16_t)(w4.x & 0xFFFF)),
+                                   to_float<Tag>((uint16_t)(w4.x >> 16)),
+                                   to_float<Tag>((uint16_t)(w4.y & 0xFFFF)),
+                                   to_float<Tag>((uint16_t)(w4.y >> 16)));
+            mv[q][h] = *reinterpret_cast<const float4*>(M + off);
+            if (W_master) pv[q][h] = *reinterpret_cast<const float4*>(W_master + off);
+          }
+        }
+      }
+    };
+    load_batch(0);
+    // The owning waves park this pass's accumulators in LDS.
+    if (wj == pwj) {
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const int i = 128 * wi + 32 * mb + 8 * g + 4 * half;
-          const uint2 w4 = *reinterpret_cast<const uint2*>(wrow + i);
-          const uint16_t* wh = reinterpret_cast<const uint16_t*>(&w4);
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            dot = fmaf(to_float<Tag>(wh[e]) * iwj[nb], sB * acc[mb][nb][4 * g + e], dot);
+          const int d0 = 128 * wi + 32 * mb + 8 * g + 4 * half;
+          *reinterpret_cast<float4*>((d0 >= 256 ? thi : tlo) + l32 * kTLd + (d0 & 255)) =
+              make_float4(acc[mb][pnb][4 * g], acc[mb][pnb][4 * g + 1], acc[mb][pnb][4 * g + 2],
+                          acc[mb][pnb][4 * g + 3]);
         }
     }
-    dot += __shfl_xor(dot, 32, 64);
-    if (half == 0) wDot[wi][64 * wj + 32 * nb + l32] = dot;
-  }
-  __syncthreads();
+    wait_lgkm0();
+    stage_barrier();
 #pragma unroll
-  for (int nb = 0; nb < 2; ++nb) {
-    if (!jvalid[nb]) continue;
-    const int jl = 64 * wj + 32 * nb + l32;
-    float dot = 0.0f;
+    for (int b = 0; b < RPW / RB; ++b) {
+      if (b > 0) load_batch(b);
 #pragma unroll
-    for (int w = 0; w < WI; ++w) dot += wDot[w][jl];
-    uint16_t* wrow = W + arow[nb] * D;
-    float* mrow = M + arow[nb] * D;
-    float* prow_m = W_master ? W_master + arow[nb] * D : nullptr;
+      for (int q = 0; q < RB; ++q) {
+        const int r = wave * RPW + b * RB + q;
+        float4 gv[NH];
+        float dot = 0.0f;
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int i = 128 * wi + 32 * mb + 8 * g + 4 * half;
-        const uint2 w4 = *reinterpret_cast<const uint2*>(wrow + i);
-        const uint16_t* wh = reinterpret_cast<const uint16_t*>(&w4);
-        float4 m4 = *reinterpret_cast<const float4*>(mrow + i);
-        float* mv = reinterpret_cast<float*>(&m4);
-        float wnew[4];
-        float4 p4;
-        float* pv = reinterpret_cast<float*>(&p4);
-        if (prow_m) p4 = *reinterpret_cast<const float4*>(prow_m + i);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float w = to_float<Tag>(wh[e]);
-          const float gr = iwj[nb] * (sB * acc[mb][nb][4 * g + e] - w * iwj[nb] * dot);
-          mv[e] = mu * mv[e] + gr;
-          if (prow_m) {
-            pv[e] = pv[e] - lr * mv[e];
-            wnew[e] = pv[e];
-          } else {
-            wnew[e] = w - lr * mv[e];
+        for (int h = 0; h < NH; ++h) {
+          gv[h] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+          if (rv[q]) {
+            const float4 a4 = *reinterpret_cast<const float4*>((h ? thi : tlo) + r * kTLd + 4 * lane);
+            gv[h] = make_float4(sB * a4.x, sB * a4.y, sB * a4.z, sB * a4.w);
+            dot = fmaf(wv[q][h].x * iwr[q], gv[h].x, dot);
+            dot = fmaf(wv[q][h].y * iwr[q], gv[h].y, dot);
+            dot = fmaf(wv[q][h].z * iwr[q], gv[h].z, dot);
+            dot = fmaf(wv[q][h].w * iwr[q], gv[h].w, dot);
           }
         }
-        *reinterpret_cast<float4*>(mrow + i) = m4;
-        if (prow_m) *reinterpret_cast<float4*>(prow_m + i) = p4;
-        uint2 o;
-        o.x = pack2<Tag>(wnew[0], wnew[1]);
-        o.y = pack2<Tag>(wnew[2], wnew[3]);
-        *reinterpret_cast<uint2*>(wrow + i) = o;
+        dot = wave_sum(dot);
+        if (!rv[q]) continue;
+#pragma unroll
+        for (int h = 0; h < NH; ++h) {
+          const int64_t off = rowa[q] * D + 256 * h + 4 * lane;
+          const float wo[4] = {wv[q][h].x, wv[q][h].y, wv[q][h].z, wv[q][h].w};
+          const float go[4] = {gv[h].x, gv[h].y, gv[h].z, gv[h].w};
+          float mo[4] = {mv[q][h].x, mv[q][h].y, mv[q][h].z, mv[q][h].w};
+          float po[4] = {pv[q][h].x, pv[q][h].y, pv[q][h].z, pv[q][h].w};
+          float wn[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float gr = iwr[q] * (go[e] - wo[e] * iwr[q] * dot);
+            mo[e] = mu * mo[e] + gr;
+            if (W_master) {
+              po[e] = po[e] - lr * mo[e];
+              wn[e] = po[e];
+            } else {
+              wn[e] = wo[e] - lr * mo[e];
+            }
+          }
+          *reinterpret_cast<float4*>(M + off) = make_float4(mo[0], mo[1], mo[2], mo[3]);
+          if (W_master)
+            *reinterpret_cast<float4*>(W_master + off) = make_float4(po[0], po[1], po[2], po[3]);
+          uint2 o;
+          o.x = pack2<Tag>(wn[0], wn[1]);
+          o.y = pack2<Tag>(wn[2], wn[3]);
+          *reinterpret_cast<uint2*>(W + off) = o;
+        }
       }
+    }
+    if (p < 3) {
+      wait_lgkm0();
+      stage_barrier();  // the stage arrays are rewritten by the next pass
+    }
   }
 }
 
