@@ -217,13 +217,19 @@ def main():
         ", ".join(f"{k}={v:.4f}" for k, v in stage_ms.items()) + f"; dominant {dominant}")
 
     # Timed region: exactly `steps` steps; the dominant kernel bracketed by HIP events.
+    # Per-step HIP events on the step's stream give the median / p99 step time.
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in batches]
     abi.pfc_timing_begin(dom_id, args.steps)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for b in batches:
+    for b, (e0, e1) in zip(batches, ev):
+        e0.record()
         run(b)
+        e1.record()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    step_ms = np.array([e0.elapsed_time(e1) for e0, e1 in ev])
     dom_total, dom_n = abi.pfc_timing_end()
     dom_avg = dom_total / max(dom_n, 1)
     loss = float(shard.loss.item())
@@ -266,6 +272,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_per_step,
+        "step_ms_median": float(np.median(step_ms)),
+        "step_ms_p99": float(np.percentile(step_ms, 99)),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

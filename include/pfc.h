@@ -65,8 +65,13 @@ typedef enum {
  * `active_cap` every other call must be given.  Also reports the workspace
  * size needed by a step with these sizes and compute dtype.
  *
- * B, d, C > 0; 0 < r <= 1; d a multiple of 8 (16-byte rows in 16-bit types);
- * compute one of pfc_dtype.  bytes, active_cap are host pointers.
+ * 1 <= B <= PFC_MAX_BATCH; 1 <= C <= PFC_MAX_CLASSES; 0 < r <= 1;
+ * 8 <= d <= 1024 with d a multiple of 8 (else PFC_ERR_INVALID_ARG); compute
+ * one of pfc_dtype.  Implemented sizes (else PFC_ERR_UNSUPPORTED): the
+ * bf16 / fp16 MFMA path takes d in {128, 256, 512}; the fp32 path, meant for
+ * parity-scale problems, takes B <= 4096.  The same limits apply to every
+ * entry point that takes d and a compute dtype.  bytes, active_cap are host
+ * pointers.
  */
 int pfc_workspace_bytes(int64_t B, int64_t d, int64_t C, double r,
                         int compute_dtype, size_t* bytes /*host*/,

@@ -3,14 +3,16 @@
 // target margin and the row-wise log-sum-exp cross-entropy over S
 // (Sec. 3.1, Eq. sampled_probability; max / sum decomposition of Sec. 3.2.1).
 //
-// 16-bit path: one MFMA GEMM kernel, tile 128 classes (MFMA M) x 128 batch
-// rows (MFMA N) x 64 of d, double-buffered LDS.  Classes sit on the MFMA M
-// axis so that each lane holds one batch row and 32 of its classes: the row
-// max / sum-exp of the epilogue is mostly in-register.  The epilogue scales
-// by 1/||x_n|| and 1/||w_j||, stores the unmargined cosine once as 16-bit
-// fixed point (the logits' only write), applies the margin at the target,
-// and emits one (max, sum exp) pair per (row, class tile).  A small kernel
-// merges the pairs into lse_n and the loss.
+// 16-bit path: one MFMA GEMM kernel per 256 active classes (MFMA M) x 256
+// batch rows (MFMA N), d streamed in 32-wide chunks through a four-stage
+// direct-to-LDS ring.  Classes sit on the MFMA M axis so that each lane holds
+// one batch row and 64 of its classes: the row max / sum-exp of the
+// epilogue is mostly in-register.  The epilogue scales by 1/||x_n|| and
+// 1/||w_j||, quantises the unmargined cosine to 16-bit fixed point (the
+// logits' only write: the tile is assembled in the idle LDS ring and stored
+// as whole rows), applies the margin at the target, and emits one
+// (max, sum exp) pair per (row, class tile).  A small kernel merges the pairs
+// into lse_n and the loss.
 #include "pfc_gemm.h"
 
 namespace pfc {
@@ -33,6 +35,7 @@ __shared__ __attribute__((aligned(1024))) uint16_t fA0[kFwdStage], fA1[kFwdStage
 __shared__ __attribute__((aligned(1024))) uint16_t fB0[kFwdStage], fB1[kFwdStage],
     fB2[kFwdStage], fB3[kFwdStage];
 __shared__ float2 fRed[2][kFwdBN];
+__shared__ __attribute__((aligned(16))) float fIw[kFwdBM];
 
 template <int S>
 __device__ __forceinline__ uint16_t* fwd_a() {
@@ -47,6 +50,20 @@ __device__ __forceinline__ uint16_t* fwd_b() {
   else if constexpr (S == 1) return fB1;
   else if constexpr (S == 2) return fB2;
   else return fB3;
+}
+
+// Rows 32 a .. 32 a + 31 of the epilogue's cosine tile (a wave-uniform).
+__device__ __forceinline__ uint16_t* fwd_tile_rows(int a) {
+  switch (a) {
+    case 0: return fA0;
+    case 1: return fA1;
+    case 2: return fA2;
+    case 3: return fA3;
+    case 4: return fB0;
+    case 5: return fB1;
+    case 6: return fB2;
+    default: return fB3;
+  }
 }
 
 // Each wave loads rows 16*(2*wave + u) + lane/4, u = 0, 1, of both operands:
@@ -84,19 +101,19 @@ __device__ __forceinline__ void fwd_compute(f32x16_t (&acc)[4][2], int wm, int w
   }
 }
 
-__device__ __forceinline__ const float* iw_base(const float* inv_w, int64_t j) { return inv_w + j; }
-
 // Epilogue of one lane for one 32-row block (nb): the lane's row n and its
 // 64 classes j = jb + 32 mb + 8 g + e (jb = first class of the lane's
-// pattern, e < 4).  Stores the quantised cosines, leaves the base-2 logits
+// pattern, e < 4).  Writes the quantised cosines to the LDS tile row trow
+// (16-byte block b of the row at position b ^ bsw), leaves the base-2 logits
 // in acc, and returns the lane pair's (max, sum 2^(f - max)) over the
 // wave's 128 classes.  CHECK_J masks classes past |S|; CHECK_T handles a
 // target column in the lane's pattern (tpos = y - jb).
 template <bool CHECK_J, bool CHECK_T>
 __device__ __forceinline__ void fwd_epilogue_rows(f32x16_t (&acc)[4][2], int nb, float ix,
                                                   const float* iwp, int K, int64_t jb, int tpos,
-                                                  const Margin& mg, bool nvalid, int16_t* qrow,
-                                                  float* mx_out, float* sm_out, float* tgt_out) {
+                                                  const Margin& mg, uint16_t* trow, int bbase,
+                                                  int bsw, int half, float* mx_out, float* sm_out,
+                                                  float* tgt_out) {
   const float s2 = mg.s * kLog2e;
   float mx = -INFINITY;
   float ct = 0.0f;
@@ -122,13 +139,13 @@ __device__ __forceinline__ void fwd_epilogue_rows(f32x16_t (&acc)[4][2], int nb,
         acc[mb][nb][4 * g + e] = f2;
         mx = fmaxf(mx, f2);
       }
-      if (nvalid) {
+      {
         const auto q01 = __builtin_amdgcn_cvt_pknorm_i16(cv[0], cv[1]);
         const auto q23 = __builtin_amdgcn_cvt_pknorm_i16(cv[2], cv[3]);
         uint2 packed;
         __builtin_memcpy(&packed.x, &q01, 4);
         __builtin_memcpy(&packed.y, &q23, 4);
-        *reinterpret_cast<uint2*>(qrow + o) = packed;
+        *reinterpret_cast<uint2*>(trow + 8 * ((bbase + o / 8) ^ bsw) + 4 * half) = packed;
       }
     }
   }
@@ -204,6 +221,19 @@ __global__ void __launch_bounds__(kFwdThreads) k_fwd16(
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.0f;
 
+  // Epilogue inputs, requested before the main loop: 1/||w|| of the tile's
+  // classes (one direct-to-LDS load by wave 0; it is the oldest load of that
+  // wave, so the loop's first wait covers it) and each lane's row data.
+  if (wave == 0) dma16(inv_w + j0 + 4 * lane, fIw);
+  float ixr[2];
+  int yhr[2];
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb) {
+    const int n = n0 + 64 * wn + 32 * nb + l32;
+    ixr[nb] = n < B ? inv_x[n] : 0.0f;
+    yhr[nb] = n < B ? yhat[n] : -1;
+  }
+
   fwd_issue<0>(ap, bp, 0, wave);
   if constexpr (NK > 1) fwd_issue<1>(ap, bp, kFwdKC, wave);
   if constexpr (NK > 2) fwd_issue<2>(ap, bp, 2 * kFwdKC, wave);
@@ -216,29 +246,46 @@ __global__ void __launch_bounds__(kFwdThreads) k_fwd16(
     fwd_compute<c & 3, Tag>(acc, wm, wn, lane);
   });
 
-  // ---- epilogue
+  // ---- epilogue.  The quantised 256 x 256 cosine tile is assembled in the
+  // (now idle) LDS ring, row n0 + r in array r / 32 (rows of 512 B, 16-byte
+  // block b of row r at position b ^ (r & 15): conflict-free writes from the
+  // MFMA layout and reads along rows), then written out in whole rows.
+  wait_lgkm0();
+  stage_barrier();  // all fragment reads of the ring are done
   const int64_t jlo = j0 + 128 * wm;
   const bool full = jlo + 128 <= (int64_t)K;   // wave-uniform: no class past |S|
+  const float* iwp = fIw + 128 * wm + 4 * half;
 #pragma unroll
   for (int nb = 0; nb < 2; ++nb) {
     const int nl = 64 * wn + 32 * nb + l32;
     const int n = n0 + nl;
-    const bool nvalid = n < B;
-    const float ix = nvalid ? inv_x[n] : 0.0f;
-    const int yh = nvalid ? yhat[n] : -1;
+    const int yh = yhr[nb];
     const int tpos = yh - (int)(jlo + 4 * half);   // target's offset in this lane's class pattern
     const bool has_t = yh >= jlo && yh < jlo + 128 && ((tpos & 4) == 0);
-    int16_t* qrow = cosq + (int64_t)(nvalid ? n : 0) * ld_cos + jlo + 4 * half;
+    uint16_t* trow = fwd_tile_rows(2 * wn + nb) + l32 * kFwdBM;
     float mx, sm;
     if (full && !__any(has_t))
-      fwd_epilogue_rows<false, false>(acc, nb, ix, iw_base(inv_w, jlo + 4 * half), K, jlo + 4 * half,
-                                      tpos, mg, nvalid, qrow, &mx, &sm, nullptr);
+      fwd_epilogue_rows<false, false>(acc, nb, ixr[nb], iwp, K, jlo + 4 * half, tpos, mg, trow,
+                                      16 * wm, l32 & 15, half, &mx, &sm, nullptr);
     else
-      fwd_epilogue_rows<true, true>(acc, nb, ix, iw_base(inv_w, jlo + 4 * half), K, jlo + 4 * half,
-                                    tpos, mg, nvalid, qrow, &mx, &sm, has_t ? tgt + n : nullptr);
+      fwd_epilogue_rows<true, true>(acc, nb, ixr[nb], iwp, K, jlo + 4 * half, tpos, mg, trow,
+                                    16 * wm, l32 & 15, half, &mx, &sm, has_t ? tgt + n : nullptr);
     if (half == 0) fRed[wm][nl] = make_float2(mx, sm);
   }
-  __syncthreads();
+  wait_lgkm0();
+  stage_barrier();
+  // Wave w writes rows 32 w .. 32 w + 31, two rows (2 x 512 B) per store.
+  {
+    const uint16_t* src = fwd_tile_rows(wave);
+    const int b = lane & 31;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int r = 2 * i + (lane >> 5);
+      const int n = n0 + 32 * wave + r;
+      const uint4 v = *reinterpret_cast<const uint4*>(src + r * kFwdBM + 8 * (b ^ (r & 15)));
+      if (n < B) *reinterpret_cast<uint4*>(cosq + (int64_t)n * ld_cos + j0 + 8 * b) = v;
+    }
+  }
   if (tid < kFwdBN) {
     const int n = n0 + tid;
     if (n < B) stats[(int64_t)n * n_ctiles + ct] = lse_merge2(fRed[0][tid], fRed[1][tid]);
