@@ -49,7 +49,8 @@ __shared__ __attribute__((aligned(16))) float xI0[kBwKC], xI1[kBwKC], xI2[kBwKC]
 __shared__ __attribute__((aligned(1024))) uint16_t xG0[kDxRows * kBwKC], xG1[kDxRows * kBwKC],
     xG2[kDxRows * kBwKC];
 // dW: X rows (bf16), raw cosines [32 rows x 128 classes], per-row records
-// (lse log2 e, 1/||x||, label, -), and the coefficient tile (MN-major).
+// (lse log2 e - log2(1/||x||), 1/||x||, label, -), and the coefficient tile
+// (MN-major).
 __shared__ __attribute__((aligned(1024))) uint16_t wX0[kRowStage], wX1[kRowStage], wX2[kRowStage];
 __shared__ __attribute__((aligned(1024))) int16_t wR0[kBwKC * kDwCls], wR1[kBwKC * kDwCls],
     wR2[kBwKC * kDwCls];
@@ -103,9 +104,21 @@ __device__ __forceinline__ float dx_operand_scale(F16Tag, float inv_w_max) {
 }
 __device__ __forceinline__ float dx_operand_scale(Bf16Tag, float) { return 1.0f; }
 
+// Two floats to a packed pair of 16-bit values, round to nearest even
+// (v_cvt_pk_bf16_f32 / v_cvt_f16_f32 on gfx950).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
 template <typename Tag>
-__device__ __forceinline__ uint32_t pack2(float a, float b) {
-  return (uint32_t)from_float<Tag>(a) | ((uint32_t)from_float<Tag>(b) << 16);
+__device__ __forceinline__ uint32_t pack2(float a, float b);
+template <>
+__device__ __forceinline__ uint32_t pack2<Bf16Tag>(float a, float b) {
+  const bf16x2_t v = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(uint32_t, v);
+}
+template <>
+__device__ __forceinline__ uint32_t pack2<F16Tag>(float a, float b) {
+  const f16x2_t v = {(_Float16)a, (_Float16)b};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 template <typename Tag>
@@ -177,8 +190,11 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
   const float scale = dx_operand_scale(Tag{}, *inv_w_max);
 
   // Coefficient-producer rows of this thread (fixed for the whole kernel).
+  // p * scale = 2^(q s log2(e) / 32767 - (lse log2(e) - log2(scale))); rows past
+  // the batch get an infinite offset (p = 0).
   int prow[GROUPS], pchunk[GROUPS], pyh[GROUPS];
-  float plse2[GROUPS], pkeep[GROUPS];
+  float plse2[GROUPS];
+  const float log2_scale = log2f(scale);
 #pragma unroll
   for (int u = 0; u < GROUPS; ++u) {
     const int q = tid + NT * u;
@@ -187,8 +203,7 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
     const int n = n0 + prow[u];
     const bool ok = n < B;
     pyh[u] = ok ? yhat[n] : -1;
-    plse2[u] = ok ? row_lse[n] * kLog2e : 0.0f;
-    pkeep[u] = ok ? scale : 0.0f;
+    plse2[u] = ok ? row_lse[n] * kLog2e - log2_scale : INFINITY;
   }
   // Raw-cosine DMA of this lane: block b holds rows 16 b .. 16 b + 15.
   int64_t rsrc[RDMA];
@@ -231,21 +246,41 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
     constexpr int S = decltype(st)::value;
     const int64_t jb = c * kBwKC;
     const bool cvalid = c < c_end;
+    const bool chunk_full = cvalid && jb + kBwKC <= K;   // wave-uniform
+    u32x4_t qv[GROUPS], i0v[GROUPS], i1v[GROUPS];
 #pragma unroll
     for (int u = 0; u < GROUPS; ++u) {
+      ds_read_128<0>(qv[u], lds_addr(dx_r<S>()) + (prow[u] * kBwKC + 8 * pchunk[u]) * 2);
+      ds_read_128<0>(i0v[u], lds_addr(dx_i<S>()) + 32 * pchunk[u]);
+      ds_read_128<16>(i1v[u], lds_addr(dx_i<S>()) + 32 * pchunk[u]);
+    }
+    lgkm_wait<0>();
+#pragma unroll
+    for (int u = 0; u < GROUPS; ++u) {
+      pin_reg(qv[u]);
+      pin_reg(i0v[u]);
+      pin_reg(i1v[u]);
       const int64_t jg = jb + 8 * pchunk[u];
       const int tpos = pyh[u] - (int)jg;  // the row's target, if it is one of these 8 classes
-      const uint4 q = *reinterpret_cast<const uint4*>(dx_r<S>() + prow[u] * kBwKC + 8 * pchunk[u]);
-      const float4 i0 = *reinterpret_cast<const float4*>(dx_i<S>() + 8 * pchunk[u]);
-      const float4 i1 = *reinterpret_cast<const float4*>(dx_i<S>() + 8 * pchunk[u] + 4);
-      const float iw[8] = {i0.x, i0.y, i0.z, i0.w, i1.x, i1.y, i1.z, i1.w};
+      const uint4 q = as_uint4(qv[u]);
+      const float iw[8] = {__uint_as_float(i0v[u].x), __uint_as_float(i0v[u].y),
+                           __uint_as_float(i0v[u].z), __uint_as_float(i0v[u].w),
+                           __uint_as_float(i1v[u].x), __uint_as_float(i1v[u].y),
+                           __uint_as_float(i1v[u].z), __uint_as_float(i1v[u].w)};
       float v[8];
+      if (chunk_full && !__any((unsigned)tpos < 8u)) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const bool keep = cvalid && tpos != e && jg + e < K;
-        v[e] = p_of((int16_t)u16_at(q, e), s2q, plse2[u]) * (keep ? iw[e] * pkeep[u] : 0.0f);
+        for (int e = 0; e < 8; ++e) v[e] = p_of((int16_t)u16_at(q, e), s2q, plse2[u]) * iw[e];
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const bool keep = cvalid && tpos != e && jg + e < K;
+          v[e] = keep ? p_of((int16_t)u16_at(q, e), s2q, plse2[u]) * iw[e] : 0.0f;
+        }
       }
-      *reinterpret_cast<uint4*>(dx_g<S>() + k_major32_offset(prow[u], pchunk[u])) = pack8<Tag>(v);
+      const uint4 o = pack8<Tag>(v);
+      ds_write_128<0>(lds_addr(dx_g<S>()) + k_major32_offset(prow[u], pchunk[u]) * 2,
+                      u32x4_t{o.x, o.y, o.z, o.w});
     }
   };
 
@@ -304,19 +339,21 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
         });
         ds_read_128<0>(bq[1][0], gb1);
         ds_read_128<32 * 64>(bq[1][1], gb1);
-        // ... then later chunks' loads and the next coefficients, while they land.
+        // ... then later chunks' loads; the next coefficients are produced
+        // while the first k-step's MFMAs run.
         dma_raw(std::integral_constant<int, u>{}, cu + 3);
         dma_w(std::integral_constant<int, (u + 2) % 3>{});
         load_rows(cu + 3);
-        produce(std::integral_constant<int, (u + 1) % 3>{}, cu + 1);
         static_for<0, 2>([&](auto kq) {
           constexpr int kk = decltype(kq)::value;
-          if constexpr (kk == 0)
+          if constexpr (kk == 0) {
             lgkm_wait<10>(alo[0][0], alo[0][1], alo[0][2], alo[0][3], ahi[0][0], ahi[0][1],
                           ahi[0][2], ahi[0][3], bq[0][0], bq[0][1]);
-          else
+          } else {
+            produce(std::integral_constant<int, (u + 1) % 3>{}, cu + 1);
             lgkm_wait<0>(alo[1][0], alo[1][1], alo[1][2], alo[1][3], ahi[1][0], ahi[1][1],
                          ahi[1][2], ahi[1][3], bq[1][0], bq[1][1]);
+          }
 #pragma unroll
           for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
@@ -351,7 +388,8 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
 // Sum the split partials of a row in split order, add the row's target term
 // g_t * W[S_t] / ||w_t||, and apply the normalisation backward:
 // dx = (dX_hat - x_hat (x_hat . dX_hat)) / ||x||, dX_hat = (s/B) * sum.
-// Also writes the row record (lse log2 e, 1/||x||, label) the dW kernel reads.
+// Also writes the row record (lse log2 e - log2(1/||x||), 1/||x||, label) the
+// dW kernel reads: its coefficient p / ||x|| is then a single power of two.
 template <typename Tag>
 __global__ void __launch_bounds__(256) k_dx_final(
     const float* __restrict__ dx_part, int n_split, const void* __restrict__ X,
@@ -367,7 +405,7 @@ __global__ void __launch_bounds__(256) k_dx_final(
   const float ix = inv_x[n];
   const int yt = yhat[n];
   const float lse = row_lse[n];
-  if (lane == 0) row_rec[n] = make_float4(lse * kLog2e, ix, (float)yt, 0.0f);
+  if (lane == 0) row_rec[n] = make_float4(lse * kLog2e - log2f(ix), ix, (float)yt, 0.0f);
   float gt = 0.0f;
   int64_t wbase = 0;
   if (yt >= 0) {
@@ -467,20 +505,38 @@ __global__ void __launch_bounds__(128 * WI) k_dw16(
   };
   auto produce = [&](auto st, int c) {
     constexpr int S = decltype(st)::value;
+    // Wave-uniform: every row of the chunk in the batch, every class of the tile in S.
+    const bool chunk_full = (c + 1) * kBwKC <= B && j0 + kDwCls <= (int64_t)K;
+    u32x4_t recv[GROUPS], qv[GROUPS];
 #pragma unroll
     for (int u = 0; u < GROUPS; ++u) {
-      const int64_t jg = j0 + pcol[u];
-      const float4 rec = dw_q<S>()[prow[u]];
-      const bool rok = c * kBwKC + prow[u] < B;
-      const int tpos = (int)rec.z - (int)jg;
-      const uint4 q = *reinterpret_cast<const uint4*>(dw_r<S>() + prow[u] * kDwCls + pcol[u]);
-      float v[8];
+      ds_read_128<0>(recv[u], lds_addr(dw_q<S>()) + 16 * prow[u]);
+      ds_read_128<0>(qv[u], lds_addr(dw_r<S>()) + (prow[u] * kDwCls + pcol[u]) * 2);
+    }
+    lgkm_wait<0>();
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const bool keep = rok && tpos != e && jg + e < K;
-        v[e] = p_of((int16_t)u16_at(q, e), s2q, rec.x) * (keep ? rec.y : 0.0f);
+    for (int u = 0; u < GROUPS; ++u) {
+      pin_reg(recv[u]);
+      pin_reg(qv[u]);
+      const int64_t jg = j0 + pcol[u];
+      const float rec_off = __uint_as_float(recv[u].x);   // lse log2 e - log2(1/||x||)
+      const bool rok = c * kBwKC + prow[u] < B;
+      const int tpos = (int)__uint_as_float(recv[u].z) - (int)jg;
+      const uint4 q = as_uint4(qv[u]);
+      float v[8];
+      if (chunk_full && !__any((unsigned)tpos < 8u)) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = p_of((int16_t)u16_at(q, e), s2q, rec_off);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const bool keep = rok && tpos != e && jg + e < K;
+          v[e] = keep ? p_of((int16_t)u16_at(q, e), s2q, rec_off) : 0.0f;
+        }
       }
-      *reinterpret_cast<uint4*>(dw_g<S>() + prow[u] * kGLd + pcol[u]) = pack8<Bf16Tag>(v);
+      const uint4 o = pack8<Bf16Tag>(v);
+      ds_write_128<0>(lds_addr(dw_g<S>()) + (prow[u] * kGLd + pcol[u]) * 2,
+                      u32x4_t{o.x, o.y, o.z, o.w});
     }
   };
 
@@ -532,15 +588,17 @@ __global__ void __launch_bounds__(128 * WI) k_dw16(
       });
       dma_raw(std::integral_constant<int, u>{}, cu + 3);
       dma_x(std::integral_constant<int, (u + 2) % 3>{}, cu + 2);
-      produce(std::integral_constant<int, (u + 1) % 3>{}, cu + 1);
       static_for<0, 2>([&](auto kq) {
         constexpr int kk = decltype(kq)::value;
-        if constexpr (kk == 0)
+        if constexpr (kk == 0) {
           lgkm_wait<12>(alo[0][0], alo[0][1], alo[0][2], alo[0][3], ahi[0][0], ahi[0][1],
                         ahi[0][2], ahi[0][3], blo[0][0], blo[0][1], bhi[0][0], bhi[0][1]);
-        else
+        } else {
+          // the next coefficients are produced while the first k-step's MFMAs run
+          produce(std::integral_constant<int, (u + 1) % 3>{}, cu + 1);
           lgkm_wait<0>(alo[1][0], alo[1][1], alo[1][2], alo[1][3], ahi[1][0], ahi[1][1],
                        ahi[1][2], ahi[1][3], blo[1][0], blo[1][1], bhi[1][0], bhi[1][1]);
+        }
         if (cu < n_chunks) {
 #pragma unroll
           for (int mb = 0; mb < 4; ++mb)

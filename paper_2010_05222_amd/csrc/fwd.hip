@@ -3,9 +3,9 @@
 // target margin and the row-wise log-sum-exp cross-entropy over S
 // (Sec. 3.1, Eq. sampled_probability; max / sum decomposition of Sec. 3.2.1).
 //
-// 16-bit path: one MFMA GEMM kernel per 256 active classes (MFMA M) x 256
-// batch rows (MFMA N), d streamed in 32-wide chunks through a four-stage
-// direct-to-LDS ring.  Classes sit on the MFMA M axis so that each lane holds
+// 16-bit path: one MFMA GEMM workgroup per 256 active classes (MFMA M) x 128
+// batch rows (MFMA N), d streamed in 32-wide chunks through a three-stage
+// direct-to-LDS ring; two workgroups share a CU.  Classes sit on the MFMA M axis so that each lane holds
 // one batch row and 64 of its classes: the row max / sum-exp of the
 // epilogue is mostly in-register.  The epilogue scales by 1/||x_n|| and
 // 1/||w_j||, quantises the unmargined cosine to 16-bit fixed point (the
@@ -19,21 +19,24 @@ namespace pfc {
 namespace {
 
 constexpr int kFwdBM = 256;       // classes per tile (MFMA M)
-constexpr int kFwdBN = 256;       // batch rows per tile (MFMA N)
+constexpr int kFwdBN = 128;       // batch rows per tile (MFMA N)
 constexpr int kFwdKC = 32;        // slice of d per pipeline stage
-constexpr int kFwdThreads = 512;  // 8 waves: 2 (classes) x 4 (rows), 128 x 64 each
-constexpr int kFwdStage = kFwdBM * kFwdKC;  // uint16 elements per operand per stage
+constexpr int kFwdThreads = 256;  // 4 waves: 2 (classes) x 2 (rows), 128 x 64 each
+constexpr int kFwdStageA = kFwdBM * kFwdKC;  // uint16 elements per stage, class operand
+constexpr int kFwdStageB = kFwdBN * kFwdKC;  // uint16 elements per stage, batch operand
 constexpr float kLog2e = 1.4426950408889634f;
 
-// Four-stage LDS ring per operand, one array per stage so the compiler can
-// keep the direct-to-LDS loads of later stages in flight while a stage is
-// read.  Row r of a stage holds 32 elements (64 B) as four 16-byte chunks;
-// chunk c is stored at position c ^ ((r >> 1) & 3), so the eight lanes of a
-// 16-byte LDS read that address eight consecutive rows hit distinct banks.
-__shared__ __attribute__((aligned(1024))) uint16_t fA0[kFwdStage], fA1[kFwdStage],
-    fA2[kFwdStage], fA3[kFwdStage];
-__shared__ __attribute__((aligned(1024))) uint16_t fB0[kFwdStage], fB1[kFwdStage],
-    fB2[kFwdStage], fB3[kFwdStage];
+// Three-stage LDS ring per operand (24 KB per stage; 75 KB in all, so two
+// workgroups share a CU and one's epilogue overlaps the other's MFMA loop).
+// One array per stage, so the compiler can keep the direct-to-LDS loads of
+// later stages in flight while a stage is read.  Row r of a stage holds 32
+// elements (64 B) as four 16-byte chunks; chunk c is stored at position
+// c ^ ((r >> 1) & 3), so the eight lanes of a 16-byte LDS read that address
+// eight consecutive rows hit distinct banks.
+__shared__ __attribute__((aligned(1024))) uint16_t fA0[kFwdStageA], fA1[kFwdStageA],
+    fA2[kFwdStageA];
+__shared__ __attribute__((aligned(1024))) uint16_t fB0[kFwdStageB], fB1[kFwdStageB],
+    fB2[kFwdStageB];
 __shared__ float2 fRed[2][kFwdBN];
 __shared__ __attribute__((aligned(16))) float fIw[kFwdBM];
 
@@ -41,64 +44,75 @@ template <int S>
 __device__ __forceinline__ uint16_t* fwd_a() {
   if constexpr (S == 0) return fA0;
   else if constexpr (S == 1) return fA1;
-  else if constexpr (S == 2) return fA2;
-  else return fA3;
+  else return fA2;
 }
 template <int S>
 __device__ __forceinline__ uint16_t* fwd_b() {
   if constexpr (S == 0) return fB0;
   else if constexpr (S == 1) return fB1;
-  else if constexpr (S == 2) return fB2;
-  else return fB3;
+  else return fB2;
 }
 
-// Rows 32 a .. 32 a + 31 of the epilogue's cosine tile (a wave-uniform).
-__device__ __forceinline__ uint16_t* fwd_tile_rows(int a) {
-  switch (a) {
-    case 0: return fA0;
-    case 1: return fA1;
-    case 2: return fA2;
-    case 3: return fA3;
-    case 4: return fB0;
-    case 5: return fB1;
-    case 6: return fB2;
-    default: return fB3;
-  }
+// Row r (0..127) of the epilogue's cosine tile, rows of 256 elements: rows
+// 0..95 in the class-operand stages (32 each), 96..127 in two batch-operand
+// stages (16 each).
+__device__ __forceinline__ uint16_t* fwd_tile_row(int r) {
+  uint16_t* base;
+  if (r < 32) base = fA0 + r * kFwdBM;
+  else if (r < 64) base = fA1 + (r - 32) * kFwdBM;
+  else if (r < 96) base = fA2 + (r - 64) * kFwdBM;
+  else if (r < 112) base = fB0 + (r - 96) * kFwdBM;
+  else base = fB1 + (r - 112) * kFwdBM;
+  return base;
 }
 
-// Each wave loads rows 16*(2*wave + u) + lane/4, u = 0, 1, of both operands:
-// four 16-byte loads per thread per stage.
+// DMA of one stage: class operand rows 16 (4 wave + u) + lane / 4 (u < 4),
+// batch operand rows 16 (2 wave + u) + lane / 4 (u < 2).
 template <int S>
-__device__ __forceinline__ void fwd_issue(const uint16_t* const ap[2], const uint16_t* const bp[2],
+__device__ __forceinline__ void fwd_issue(const uint16_t* const ap[4], const uint16_t* const bp[2],
                                           int k0, int wave) {
 #pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    dma16(ap[u] + k0, fwd_a<S>() + (2 * wave + u) * 16 * kFwdKC);
-    dma16(bp[u] + k0, fwd_b<S>() + (2 * wave + u) * 16 * kFwdKC);
-  }
+  for (int u = 0; u < 4; ++u) dma16(ap[u] + k0, fwd_a<S>() + (4 * wave + u) * 16 * kFwdKC);
+#pragma unroll
+  for (int u = 0; u < 2; ++u) dma16(bp[u] + k0, fwd_b<S>() + (2 * wave + u) * 16 * kFwdKC);
 }
 
+// Fragments of both 16-wide k-steps of a stage are requested first, then
+// consumed: lane l reads row 32 q + l % 32 of its operand block, chunk
+// 2 kk + l / 32 (stored at chunk ^ ((row >> 1) & 3)).
 template <int S, typename Tag>
 __device__ __forceinline__ void fwd_compute(f32x16_t (&acc)[4][2], int wm, int wn, int lane) {
-  const uint16_t* A = fwd_a<S>();
-  const uint16_t* Bm = fwd_b<S>();
   const int r32 = lane & 31;
   const int sw = (lane >> 1) & 3;
-#pragma unroll
-  for (int kk = 0; kk < kFwdKC / 16; ++kk) {
-    const int pos = ((2 * kk + (lane >> 5)) ^ sw) * 8;
-    uint4 af[4], bf[2];
+  const uint32_t arow = lds_addr(fwd_a<S>()) + (128 * wm + r32) * kFwdKC * 2;
+  const uint32_t brow = lds_addr(fwd_b<S>()) + (64 * wn + r32) * kFwdKC * 2;
+  u32x4_t af[2][4], bf[2][2];
+  static_for<0, 2>([&](auto kq) {
+    constexpr int kk = decltype(kq)::value;
+    const uint32_t chunk = (uint32_t)(((2 * kk + (lane >> 5)) ^ sw) * 16);
+    static_for<0, 4>([&](auto mm) {
+      constexpr int mb = decltype(mm)::value;
+      ds_read_128<32 * mb * kFwdKC * 2>(af[kk][mb], arow + chunk);
+    });
+    static_for<0, 2>([&](auto nn) {
+      constexpr int nb = decltype(nn)::value;
+      ds_read_128<32 * nb * kFwdKC * 2>(bf[kk][nb], brow + chunk);
+    });
+  });
+  static_for<0, 2>([&](auto kq) {
+    constexpr int kk = decltype(kq)::value;
+    if constexpr (kk == 0)
+      lgkm_wait<6>(af[0][0], af[0][1], af[0][2], af[0][3], bf[0][0], bf[0][1]);
+    else
+      lgkm_wait<0>(af[1][0], af[1][1], af[1][2], af[1][3], bf[1][0], bf[1][1]);
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
-      af[mb] = *reinterpret_cast<const uint4*>(A + (128 * wm + 32 * mb + r32) * kFwdKC + pos);
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
-      bf[nb] = *reinterpret_cast<const uint4*>(Bm + (64 * wn + 32 * nb + r32) * kFwdKC + pos);
-#pragma unroll
-    for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb) acc[mb][nb] = mfma_32x32x16(af[mb], bf[nb], acc[mb][nb], Tag{});
-  }
+      for (int nb = 0; nb < 2; ++nb)
+        acc[mb][nb] = mfma_32x32x16(make_uint4(af[kk][mb].x, af[kk][mb].y, af[kk][mb].z, af[kk][mb].w),
+                                    make_uint4(bf[kk][nb].x, bf[kk][nb].y, bf[kk][nb].z, bf[kk][nb].w),
+                                    acc[mb][nb], Tag{});
+  });
 }
 
 // Epilogue of one lane for one 32-row block (nb): the lane's row n and its
@@ -170,13 +184,13 @@ __device__ __forceinline__ void fwd_epilogue_rows(f32x16_t (&acc)[4][2], int nb,
   *sm_out = sm;
 }
 
-// Tile: 256 active classes x 256 batch rows, the whole of d (= 32 * NK).
+// Tile: 256 active classes x 128 batch rows, the whole of d (= 32 * NK).
 // Epilogue, per (row, class): c = acc / (||x|| ||w||); the 16-bit fixed-point
 // cosine round(c * 32767) is stored once; the row's (max, sum) over the tile
 // is accumulated in base 2 from the fp32 logit s*c (the margined logit at
 // the target), and the target logit itself goes to tgt[n].
 template <typename Tag, int NK>
-__global__ void __launch_bounds__(kFwdThreads) k_fwd16(
+__global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
     const int32_t* __restrict__ active, const int32_t* __restrict__ n_active_p,
     const int32_t* __restrict__ yhat, const float* __restrict__ inv_x,
@@ -196,19 +210,23 @@ __global__ void __launch_bounds__(kFwdThreads) k_fwd16(
   const int n0 = rt * kFwdBN;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 2, wn = wave & 3;
+  const int wm = wave >> 1, wn = wave & 1;
   const int half = lane >> 5, l32 = lane & 31;
 
-  // Per-lane source rows of the two DMA segments; rows past the end are
-  // clamped to a valid row (their results are masked in the epilogue).
+  // Per-lane source rows of the DMA segments; rows past the end are clamped
+  // to a valid row (their results are masked in the epilogue).
   const int cidx = (lane & 3) ^ ((lane >> 3) & 3);
-  const uint16_t* ap[2];
+  const uint16_t* ap[4];
   const uint16_t* bp[2];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int row = 16 * (4 * wave + u) + (lane >> 2);
+    const int64_t jr = j0 + row < K ? j0 + row : K - 1;
+    ap[u] = W + (int64_t)active[jr] * D + 8 * cidx;
+  }
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
     const int row = 16 * (2 * wave + u) + (lane >> 2);
-    const int64_t jr = j0 + row < K ? j0 + row : K - 1;
-    ap[u] = W + (int64_t)active[jr] * D + 8 * cidx;
     const int nr = n0 + row < B ? n0 + row : B - 1;
     bp[u] = X + (int64_t)nr * D + 8 * cidx;
   }
@@ -234,22 +252,24 @@ __global__ void __launch_bounds__(kFwdThreads) k_fwd16(
     yhr[nb] = n < B ? yhat[n] : -1;
   }
 
+  constexpr int kPerStage = 6;  // DMAs per thread per stage
   fwd_issue<0>(ap, bp, 0, wave);
   if constexpr (NK > 1) fwd_issue<1>(ap, bp, kFwdKC, wave);
-  if constexpr (NK > 2) fwd_issue<2>(ap, bp, 2 * kFwdKC, wave);
   static_for<0, NK>([&](auto cc) {
     constexpr int c = decltype(cc)::value;
-    constexpr int ahead = (NK - 1 - c) < 2 ? (NK - 1 - c) : 2;
-    wait_vmcnt<4 * ahead>();
+    constexpr int ahead = (NK - 1 - c) < 1 ? (NK - 1 - c) : 1;
+    // This wave's loads of chunk c have landed; after the barrier everyone's
+    // have, and every wave is done with chunk c - 1, whose stage is refilled.
+    wait_vmcnt<kPerStage * ahead>();
     stage_barrier();
-    if constexpr (c + 3 < NK) fwd_issue<(c + 3) & 3>(ap, bp, (c + 3) * kFwdKC, wave);
-    fwd_compute<c & 3, Tag>(acc, wm, wn, lane);
+    if constexpr (c + 2 < NK) fwd_issue<(c + 2) % 3>(ap, bp, (c + 2) * kFwdKC, wave);
+    fwd_compute<c % 3, Tag>(acc, wm, wn, lane);
   });
 
-  // ---- epilogue.  The quantised 256 x 256 cosine tile is assembled in the
-  // (now idle) LDS ring, row n0 + r in array r / 32 (rows of 512 B, 16-byte
-  // block b of row r at position b ^ (r & 15): conflict-free writes from the
-  // MFMA layout and reads along rows), then written out in whole rows.
+  // ---- epilogue.  The quantised 256-class x 128-row cosine tile is
+  // assembled in the (now idle) LDS ring (rows of 512 B, 16-byte block b of
+  // row r at position b ^ (r & 15): conflict-free writes from the MFMA layout
+  // and reads along rows), then written out in whole rows.
   wait_lgkm0();
   stage_barrier();  // all fragment reads of the ring are done
   const int64_t jlo = j0 + 128 * wm;
@@ -262,27 +282,26 @@ __global__ void __launch_bounds__(kFwdThreads) k_fwd16(
     const int yh = yhr[nb];
     const int tpos = yh - (int)(jlo + 4 * half);   // target's offset in this lane's class pattern
     const bool has_t = yh >= jlo && yh < jlo + 128 && ((tpos & 4) == 0);
-    uint16_t* trow = fwd_tile_rows(2 * wn + nb) + l32 * kFwdBM;
+    uint16_t* trow = fwd_tile_row(nl);
     float mx, sm;
     if (full && !__any(has_t))
       fwd_epilogue_rows<false, false>(acc, nb, ixr[nb], iwp, K, jlo + 4 * half, tpos, mg, trow,
-                                      16 * wm, l32 & 15, half, &mx, &sm, nullptr);
+                                      16 * wm, nl & 15, half, &mx, &sm, nullptr);
     else
       fwd_epilogue_rows<true, true>(acc, nb, ixr[nb], iwp, K, jlo + 4 * half, tpos, mg, trow,
-                                    16 * wm, l32 & 15, half, &mx, &sm, has_t ? tgt + n : nullptr);
+                                    16 * wm, nl & 15, half, &mx, &sm, has_t ? tgt + n : nullptr);
     if (half == 0) fRed[wm][nl] = make_float2(mx, sm);
   }
   wait_lgkm0();
   stage_barrier();
   // Wave w writes rows 32 w .. 32 w + 31, two rows (2 x 512 B) per store.
   {
-    const uint16_t* src = fwd_tile_rows(wave);
     const int b = lane & 31;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      const int r = 2 * i + (lane >> 5);
-      const int n = n0 + 32 * wave + r;
-      const uint4 v = *reinterpret_cast<const uint4*>(src + r * kFwdBM + 8 * (b ^ (r & 15)));
+      const int r = 32 * wave + 2 * i + (lane >> 5);
+      const int n = n0 + r;
+      const uint4 v = *reinterpret_cast<const uint4*>(fwd_tile_row(r) + 8 * (b ^ (r & 15)));
       if (n < B) *reinterpret_cast<uint4*>(cosq + (int64_t)n * ld_cos + j0 + 8 * b) = v;
     }
   }
@@ -403,7 +422,6 @@ void launch_fwd16(int d, unsigned grid, hipStream_t stream, const StepArgs& a, c
   switch (d) {
     case 128: launch_fwd16_nk<Tag, 4>(grid, stream, a, w, B, n_rt, n_tiles, per_xcd, mg); break;
     case 256: launch_fwd16_nk<Tag, 8>(grid, stream, a, w, B, n_rt, n_tiles, per_xcd, mg); break;
-    case 384: launch_fwd16_nk<Tag, 12>(grid, stream, a, w, B, n_rt, n_tiles, per_xcd, mg); break;
     default: launch_fwd16_nk<Tag, 16>(grid, stream, a, w, B, n_rt, n_tiles, per_xcd, mg); break;
   }
 }

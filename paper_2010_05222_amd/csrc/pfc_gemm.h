@@ -57,10 +57,13 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
 
-// LDS reads issued as inline assembly.  The compiler neither orders them
-// against pending direct-to-LDS loads (the pipeline's own waits do) nor
-// waits for their results: lgkm_wait() below must separate them from the
-// first use of their destinations.
+// LDS accesses issued as inline assembly.  Inside the pipelined loops every
+// LDS access goes through these: the compiler would otherwise hoist plain
+// LDS loads above the stage barrier, and make each plain LDS access wait for
+// every pending direct-to-LDS load (it cannot tell the stages apart).  It
+// neither orders these against pending direct-to-LDS loads (the pipeline's
+// own waits do) nor waits for their results: lgkm_wait() below must separate
+// a read from the first use of its destination.
 template <int OFF>
 __device__ __forceinline__ void ds_read_tr_b64(u32x2_t& dst, uint32_t addr) {
   asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(dst) : "v"(addr), "i"(OFF));
@@ -68,6 +71,11 @@ __device__ __forceinline__ void ds_read_tr_b64(u32x2_t& dst, uint32_t addr) {
 template <int OFF>
 __device__ __forceinline__ void ds_read_128(u32x4_t& dst, uint32_t addr) {
   asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(dst) : "v"(addr), "i"(OFF));
+}
+
+template <int OFF>
+__device__ __forceinline__ void ds_write_128(uint32_t addr, const u32x4_t& v) {
+  asm volatile("ds_write_b128 %0, %1 offset:%2" ::"v"(addr), "v"(v), "i"(OFF) : "memory");
 }
 
 template <typename T>
