@@ -84,6 +84,7 @@ WsLayout ws_layout(int64_t B, int64_t d, int64_t C, int64_t cap, int compute) {
 
   L.ld_cos = round_up(cap, 256);
   L.n_ctiles = ceil_div(cap, kFwdClassTile);
+  L.ld_xt = round_up(B, 32);
   if (compute == PFC_F32) {
     L.n_split = 1;
   } else {
@@ -97,7 +98,7 @@ WsLayout ws_layout(int64_t B, int64_t d, int64_t C, int64_t cap, int compute) {
   }
   const size_t cos_elt = compute == PFC_F32 ? 4 : 2;
   L.off_inv_x = take((size_t)B * 4);
-  L.off_xb = take(compute == PFC_F32 ? 0 : (size_t)B * d * 2);
+  L.off_xb = take(compute == PFC_F32 ? 0 : (size_t)L.ld_xt * d * 2);
   L.off_wmax = take(4);
   L.off_inv_w = take((size_t)L.ld_cos * 4);
   L.off_cos = take((size_t)B * L.ld_cos * cos_elt);
@@ -105,7 +106,7 @@ WsLayout ws_layout(int64_t B, int64_t d, int64_t C, int64_t cap, int compute) {
   L.off_tgt = take((size_t)B * 4);
   L.off_dx = take((size_t)L.n_split * B * d * 4);
   L.off_loss = take((size_t)B * 4);
-  L.off_rec = take((size_t)B * 16);
+  L.off_rec = take((size_t)L.ld_xt * 8);
   L.bytes = off;
   return L;
 }
@@ -129,7 +130,8 @@ StepWs step_ws(void* ws, const WsLayout& L) {
   char* b = (char*)ws;
   StepWs w;
   w.inv_x = (float*)(b + L.off_inv_x);
-  w.xb = b + L.off_xb;
+  w.xbT = b + L.off_xb;
+  w.ld_xt = L.ld_xt;
   w.inv_w_max = (float*)(b + L.off_wmax);
   w.inv_w = (float*)(b + L.off_inv_w);
   w.cosq = b + L.off_cos;
@@ -140,7 +142,7 @@ StepWs step_ws(void* ws, const WsLayout& L) {
   w.dx_part = (float*)(b + L.off_dx);
   w.n_split = L.n_split;
   w.loss_part = (float*)(b + L.off_loss);
-  w.row_rec = (float4*)(b + L.off_rec);
+  w.row_rec = (float2*)(b + L.off_rec);
   return w;
 }
 

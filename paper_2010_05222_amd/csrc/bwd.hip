@@ -32,7 +32,6 @@ constexpr int kRowLd = 528;        // LDS row stride of a DMA'd row of up to 512
 constexpr int kRowStage = kBwKC * kRowLd;
 constexpr int kDxRows = 128;       // batch rows of a dX workgroup
 constexpr int kDwCls = 128;        // classes of a dW workgroup
-constexpr int kGLd = kDwCls + 16;  // LDS row stride of the dW coefficient tile (288 B)
 constexpr int kTLd = 260;         // LDS row stride (floats) of the update's staged gradient rows
 
 // Every operand reaches LDS through direct-to-LDS loads into three-stage
@@ -48,15 +47,17 @@ __shared__ __attribute__((aligned(1024))) int16_t xR0[kDxRows * kBwKC], xR1[kDxR
 __shared__ __attribute__((aligned(16))) float xI0[kBwKC], xI1[kBwKC], xI2[kBwKC];
 __shared__ __attribute__((aligned(1024))) uint16_t xG0[kDxRows * kBwKC], xG1[kDxRows * kBwKC],
     xG2[kDxRows * kBwKC];
-// dW: X rows (bf16), raw cosines [32 rows x 128 classes], per-row records
-// (lse log2 e - log2(1/||x||), 1/||x||, label, -), and the coefficient tile
-// (MN-major).
+// dW: X^T rows (K-major: d rows of 32 batch rows, bf16), raw cosines
+// [32 rows x 128 classes] (16-byte pieces swizzled per row), per-row records
+// (lse log2 e - log2(1/||x||), label), and the coefficient tile G^T (K-major:
+// 128 class rows of 32 batch rows).  The X^T stages (33 KB) also hold the
+// update's staged gradient rows after the loop.
 __shared__ __attribute__((aligned(1024))) uint16_t wX0[kRowStage], wX1[kRowStage], wX2[kRowStage];
 __shared__ __attribute__((aligned(1024))) int16_t wR0[kBwKC * kDwCls], wR1[kBwKC * kDwCls],
     wR2[kBwKC * kDwCls];
-__shared__ __attribute__((aligned(16))) float4 wQ0[kBwKC], wQ1[kBwKC], wQ2[kBwKC];
-__shared__ __attribute__((aligned(1024))) uint16_t wG0[kBwKC * kGLd], wG1[kBwKC * kGLd],
-    wG2[kBwKC * kGLd];
+__shared__ __attribute__((aligned(16))) float2 wQ0[kBwKC], wQ1[kBwKC], wQ2[kBwKC];
+__shared__ __attribute__((aligned(1024))) uint16_t wG0[kDwCls * kBwKC], wG1[kDwCls * kBwKC],
+    wG2[kDwCls * kBwKC];
 
 #define PFC_STAGE3(name, T, a0, a1, a2)          \
   template <int S>                               \
@@ -71,7 +72,7 @@ PFC_STAGE3(dx_i, float, xI0, xI1, xI2)
 PFC_STAGE3(dx_g, uint16_t, xG0, xG1, xG2)
 PFC_STAGE3(dw_x, uint16_t, wX0, wX1, wX2)
 PFC_STAGE3(dw_r, int16_t, wR0, wR1, wR2)
-PFC_STAGE3(dw_q, float4, wQ0, wQ1, wQ2)
+PFC_STAGE3(dw_q, float2, wQ0, wQ1, wQ2)
 PFC_STAGE3(dw_g, uint16_t, wG0, wG1, wG2)
 #undef PFC_STAGE3
 
@@ -242,31 +243,38 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
       if (lane < D / 8) dma16(W + (int64_t)rows_pf[v] * D + 8 * lane, dx_w<S>() + r * kRowLd);
     }
   };
-  auto produce = [&](auto st, int64_t c) {
+  // Coefficients of chunk c (K-major, rows of 32 classes): the LDS reads are
+  // issued first (produce_load) and consumed later (produce_store), after an
+  // lgkm wait that covers them.
+  struct ProdIn {
+    u32x4_t qv[GROUPS], i0v[GROUPS], i1v[GROUPS];
+  };
+  auto produce_load = [&](auto st, ProdIn& in) {
+    constexpr int S = decltype(st)::value;
+#pragma unroll
+    for (int u = 0; u < GROUPS; ++u) {
+      ds_read_128<0>(in.qv[u], lds_addr(dx_r<S>()) + (prow[u] * kBwKC + 8 * pchunk[u]) * 2);
+      ds_read_128<0>(in.i0v[u], lds_addr(dx_i<S>()) + 32 * pchunk[u]);
+      ds_read_128<16>(in.i1v[u], lds_addr(dx_i<S>()) + 32 * pchunk[u]);
+    }
+  };
+  auto produce_store = [&](auto st, int64_t c, ProdIn& in) {
     constexpr int S = decltype(st)::value;
     const int64_t jb = c * kBwKC;
     const bool cvalid = c < c_end;
     const bool chunk_full = cvalid && jb + kBwKC <= K;   // wave-uniform
-    u32x4_t qv[GROUPS], i0v[GROUPS], i1v[GROUPS];
 #pragma unroll
     for (int u = 0; u < GROUPS; ++u) {
-      ds_read_128<0>(qv[u], lds_addr(dx_r<S>()) + (prow[u] * kBwKC + 8 * pchunk[u]) * 2);
-      ds_read_128<0>(i0v[u], lds_addr(dx_i<S>()) + 32 * pchunk[u]);
-      ds_read_128<16>(i1v[u], lds_addr(dx_i<S>()) + 32 * pchunk[u]);
-    }
-    lgkm_wait<0>();
-#pragma unroll
-    for (int u = 0; u < GROUPS; ++u) {
-      pin_reg(qv[u]);
-      pin_reg(i0v[u]);
-      pin_reg(i1v[u]);
+      pin_reg(in.qv[u]);
+      pin_reg(in.i0v[u]);
+      pin_reg(in.i1v[u]);
       const int64_t jg = jb + 8 * pchunk[u];
       const int tpos = pyh[u] - (int)jg;  // the row's target, if it is one of these 8 classes
-      const uint4 q = as_uint4(qv[u]);
-      const float iw[8] = {__uint_as_float(i0v[u].x), __uint_as_float(i0v[u].y),
-                           __uint_as_float(i0v[u].z), __uint_as_float(i0v[u].w),
-                           __uint_as_float(i1v[u].x), __uint_as_float(i1v[u].y),
-                           __uint_as_float(i1v[u].z), __uint_as_float(i1v[u].w)};
+      const uint4 q = as_uint4(in.qv[u]);
+      const float iw[8] = {__uint_as_float(in.i0v[u].x), __uint_as_float(in.i0v[u].y),
+                           __uint_as_float(in.i0v[u].z), __uint_as_float(in.i0v[u].w),
+                           __uint_as_float(in.i1v[u].x), __uint_as_float(in.i1v[u].y),
+                           __uint_as_float(in.i1v[u].z), __uint_as_float(in.i1v[u].w)};
       float v[8];
       if (chunk_full && !__any((unsigned)tpos < 8u)) {
 #pragma unroll
@@ -275,7 +283,8 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           const bool keep = cvalid && tpos != e && jg + e < K;
-          v[e] = keep ? p_of((int16_t)u16_at(q, e), s2q, plse2[u]) * iw[e] : 0.0f;
+          const float pe = p_of((int16_t)u16_at(q, e), s2q, plse2[u]) * iw[e];
+          v[e] = keep ? pe : 0.0f;
         }
       }
       const uint4 o = pack8<Tag>(v);
@@ -310,7 +319,10 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
     dma_raw(S2{}, c_begin + 2);
     wait_vmcnt_lgkm0<2 * (RDMA + 1) + WROWS>();
     stage_barrier();
-    produce(S0{}, c_begin);
+    ProdIn in0;
+    produce_load(S0{}, in0);
+    lgkm_wait<0>();
+    produce_store(S0{}, c_begin, in0);
     for (int64_t c = c_begin; c < c_stop; c += 3) {
       static_for<0, 3>([&](auto uu) {
         constexpr int u = decltype(uu)::value;
@@ -319,7 +331,10 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
         // coefficient writes of the previous iteration are complete.
         wait_vmcnt_lgkm0<PER_ITER>();
         stage_barrier();
-        // Fragments of chunk cu (both 16-class k-steps) are requested first...
+        // The producer's reads of chunk cu + 1 go first (consumed while the
+        // first k-step's MFMAs run), then the fragments of chunk cu...
+        ProdIn pin;
+        produce_load(std::integral_constant<int, (u + 1) % 3>{}, pin);
         const uint32_t wb = lds_addr(dx_w<u>()) + a_lane;
         const uint32_t gb0 = lds_addr(dx_g<u>()) + b_lane0;
         const uint32_t gb1 = lds_addr(dx_g<u>()) + b_lane1;
@@ -350,7 +365,7 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
             lgkm_wait<10>(alo[0][0], alo[0][1], alo[0][2], alo[0][3], ahi[0][0], ahi[0][1],
                           ahi[0][2], ahi[0][3], bq[0][0], bq[0][1]);
           } else {
-            produce(std::integral_constant<int, (u + 1) % 3>{}, cu + 1);
+            produce_store(std::integral_constant<int, (u + 1) % 3>{}, cu + 1, pin);
             lgkm_wait<0>(alo[1][0], alo[1][1], alo[1][2], alo[1][3], ahi[1][0], ahi[1][1],
                          ahi[1][2], ahi[1][3], bq[1][0], bq[1][1]);
           }
@@ -388,8 +403,8 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
 // Sum the split partials of a row in split order, add the row's target term
 // g_t * W[S_t] / ||w_t||, and apply the normalisation backward:
 // dx = (dX_hat - x_hat (x_hat . dX_hat)) / ||x||, dX_hat = (s/B) * sum.
-// Also writes the row record (lse log2 e - log2(1/||x||), 1/||x||, label) the
-// dW kernel reads: its coefficient p / ||x|| is then a single power of two.
+// Also writes the row record (lse log2 e - log2(1/||x||), label) the dW kernel
+// reads: its coefficient p / ||x|| is then a single power of two.
 template <typename Tag>
 __global__ void __launch_bounds__(256) k_dx_final(
     const float* __restrict__ dx_part, int n_split, const void* __restrict__ X,
@@ -397,7 +412,7 @@ __global__ void __launch_bounds__(256) k_dx_final(
     const int32_t* __restrict__ yhat, const float* __restrict__ row_lse,
     const float* __restrict__ inv_x, const float* __restrict__ inv_w,
     const int16_t* __restrict__ cosq, int64_t ld_cos, int B, int d, Margin mg, float sB,
-    float* __restrict__ dX, float4* __restrict__ row_rec) {
+    float* __restrict__ dX, float2* __restrict__ row_rec) {
   constexpr int kMaxPer = 8;  // d <= 512
   const int lane = threadIdx.x & 63;
   const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -405,7 +420,7 @@ __global__ void __launch_bounds__(256) k_dx_final(
   const float ix = inv_x[n];
   const int yt = yhat[n];
   const float lse = row_lse[n];
-  if (lane == 0) row_rec[n] = make_float4(lse * kLog2e - log2f(ix), ix, (float)yt, 0.0f);
+  if (lane == 0) row_rec[n] = make_float2(lse * kLog2e - log2f(ix), __int_as_float(yt));
   float gt = 0.0f;
   int64_t wbase = 0;
   if (yt >= 0) {
@@ -439,25 +454,30 @@ __global__ void __launch_bounds__(256) k_dx_final(
 // ------------------------------------------------------------------ dW
 
 // D = 128 * WI; 2 * WI waves: wave (wi, wj) owns d entries [128 wi, +128) and
-// classes [64 wj, +64) of the workgroup's 128.  Pipeline per chunk c (32
-// batch rows): raw cosines and row records of chunk c + 3 and X rows of chunk
-// c + 2 requested, coefficients of chunk c + 1 produced, chunk c contracted.
+// classes [64 wj, +64) of the workgroup's 128.  Both MFMA operands are
+// K-major in LDS, so every fragment is one 16-byte read: X^T from the
+// transposed bf16 copy of the batch, and G^T written by the producer.
+// Pipeline per chunk c (32 batch rows): raw cosines and row records of chunk
+// c + 3 and X^T of chunk c + 2 requested, coefficients of chunk c + 1
+// produced (after the first k-step's MFMAs are issued), chunk c contracted.
 template <typename Tag, int WI>
 __global__ void __launch_bounds__(128 * WI) k_dw16(
-    const uint16_t* __restrict__ xb, const void* __restrict__ X, uint16_t* __restrict__ W,
-    float* __restrict__ W_master, float* __restrict__ M, const int32_t* __restrict__ active,
-    const int32_t* __restrict__ n_active_p, const int32_t* __restrict__ yhat,
-    const float* __restrict__ row_lse, const float* __restrict__ inv_x,
-    const float* __restrict__ inv_w, const float4* __restrict__ row_rec,
-    const int16_t* __restrict__ cosq, int64_t ld_cos, int B, Margin mg, float sB, float lr,
-    float mu) {
+    const uint16_t* __restrict__ xbT, int64_t ld_xt, const void* __restrict__ X,
+    uint16_t* __restrict__ W, float* __restrict__ W_master, float* __restrict__ M,
+    const int32_t* __restrict__ active, const int32_t* __restrict__ n_active_p,
+    const int32_t* __restrict__ yhat, const float* __restrict__ row_lse,
+    const float* __restrict__ inv_x, const float* __restrict__ inv_w,
+    const float2* __restrict__ row_rec, const int16_t* __restrict__ cosq, int64_t ld_cos, int B,
+    Margin mg, float sB, float lr, float mu) {
   constexpr int D = 128 * WI;
   constexpr int NT = 128 * WI;
   constexpr int NW = 2 * WI;
-  constexpr int XROWS = kBwKC / NW;     // X rows DMA'd by each wave per chunk
-  constexpr int RDMA = 8 / NW;          // 1-KB raw-cosine blocks (4 rows) per wave
-  constexpr int GROUPS = 512 / NT;
-  constexpr int PER_ITER = XROWS + RDMA + 1;
+  constexpr int XDMA = D / 16 / NW;     // X^T loads (16 d rows each) per wave per chunk
+  constexpr int RDMA = 8 / NW;          // raw-cosine loads (4 rows each) per wave
+  constexpr int QL = 16 / NW;           // record pieces (2 rows each) per wave
+  constexpr int GROUPS = 512 / NT;      // producer slots per thread
+  constexpr int PER_ITER = XDMA + RDMA + 1;
+  static_assert(XDMA == 4, "X^T loads per wave");
   const int K = *n_active_p;
   const int64_t j0 = (int64_t)blockIdx.x * kDwCls;
   if (j0 >= K) return;
@@ -469,82 +489,132 @@ __global__ void __launch_bounds__(128 * WI) k_dw16(
   const float s2q = mg.s * kLog2e * kCosDequant;
   const int n_chunks = (int)ceil_div(B, kBwKC);
   const int c_stop = (int)ceil_div(n_chunks, 3) * 3;
+  const bool tile_full = j0 + kDwCls <= (int64_t)K;   // every class of the tile in S
 
-  int prow[GROUPS], pcol[GROUPS];
+  // Producer slots: a 16-lane group owns 16 classes x 8 batch rows of a chunk;
+  // lane gi of the group owns class 16 cb + gi.
+  const int grp = lane >> 4, gi = lane & 15;
+  int pcls[GROUPS], prg[GROUPS];
+  uint32_t ptr_off[GROUPS];   // byte offset of the lane's transposing raw read
 #pragma unroll
   for (int u = 0; u < GROUPS; ++u) {
-    const int q = tid + NT * u;
-    prow[u] = q >> 4;        // batch row within the chunk
-    pcol[u] = (q & 15) * 8;  // first of 8 classes
+    const int s = 4 * wave + grp + (NT / 16) * u;
+    const int cb = s >> 2;
+    pcls[u] = 16 * cb + gi;
+    prg[u] = s & 3;
+    // Lane 4 e + q of the group points at row 8 rg + e, classes 16 cb + 4 q .. + 3
+    // (16-byte piece 2 cb + q / 2, stored at piece ^ 2 (row & 3)), half q & 1.
+    const int e = gi >> 2, q = gi & 3;
+    const int r = 8 * prg[u] + e;
+    ptr_off[u] = (uint32_t)(r * kDwCls * 2 + 16 * ((2 * cb + (q >> 1)) ^ (2 * (r & 3))) + 8 * (q & 1));
   }
 
+  // Raw cosines: load v of this wave covers rows 4 b .. 4 b + 3 (b = wave RDMA + v);
+  // lane l fills piece l % 16 of row 4 b + l / 16 with source piece
+  // (l % 16) ^ 2 (row & 3).
   auto dma_raw = [&](auto st, int c) {
     constexpr int S = decltype(st)::value;
     const int cc = c < n_chunks ? c : n_chunks - 1;
 #pragma unroll
     for (int v = 0; v < RDMA; ++v) {
-      const int r = 4 * (wave * RDMA + v) + (lane >> 4);
+      const int blk = wave * RDMA + v;
+      const int r = 4 * blk + (lane >> 4);
       int n = cc * kBwKC + r;
       n = n < B ? n : B - 1;
-      dma16(cosq + (int64_t)n * ld_cos + j0 + 8 * (lane & 15), dw_r<S>() + 512 * (wave * RDMA + v));
+      const int piece = (lane & 15) ^ (2 * (r & 3));
+      dma16(cosq + (int64_t)n * ld_cos + j0 + 8 * piece, dw_r<S>() + 512 * blk);
     }
-    const int rr = (kBwKC / NW) * wave + lane;  // row records: kBwKC / NW rows per wave
-    int nr = cc * kBwKC + rr;
-    nr = nr < B ? nr : B - 1;
-    if (lane < kBwKC / NW) dma16(row_rec + nr, dw_q<S>() + (kBwKC / NW) * wave);
+    // Row records: QL 16-byte pieces (2 rows each) per wave; rows < ld_xt always.
+    if (lane < QL) dma16(row_rec + cc * kBwKC + 2 * (QL * wave + lane), dw_q<S>() + 2 * QL * wave);
   };
+  // X^T: block cc of the transposed batch ([d][32], contiguous); load v of this
+  // wave covers d rows 16 m .. 16 m + 15 (m = wave XDMA + v), 4 pieces each;
+  // lane l fills piece l & 3 of row 16 m + l / 4 with source piece
+  // (l & 3) ^ ((row >> 1) & 3).
   auto dma_x = [&](auto st, int c) {
     constexpr int S = decltype(st)::value;
+    const int cc = c < n_chunks ? c : n_chunks - 1;
 #pragma unroll
-    for (int v = 0; v < XROWS; ++v) {
-      const int r = wave * XROWS + v;
-      int n = c * kBwKC + r;
-      n = n < B ? n : B - 1;
-      if (lane < D / 8) dma16(xb + (int64_t)n * D + 8 * lane, dw_x<S>() + r * kRowLd);
+    for (int v = 0; v < XDMA; ++v) {
+      const int m = wave * XDMA + v;
+      const int i = 16 * m + (lane >> 2);
+      const int piece = (lane & 3) ^ ((i >> 1) & 3);
+      dma16(xbT + ((int64_t)cc * D + i) * kBwKC + 8 * piece, dw_x<S>() + 512 * m);
     }
   };
-  auto produce = [&](auto st, int c) {
+  // Coefficients of chunk c: G^T[class][row] = p / ||x_row|| for the non-target
+  // entries (zero at targets, classes past |S| and rows past the batch).  The
+  // LDS reads are issued first (produce_load) and consumed later
+  // (produce_store), after an lgkm wait that covers them.
+  struct ProdIn {
+    u32x2_t qlo[GROUPS], qhi[GROUPS];
+    u32x4_t rq[GROUPS][4];
+  };
+  auto produce_load = [&](auto st, ProdIn& in) {
     constexpr int S = decltype(st)::value;
-    // Wave-uniform: every row of the chunk in the batch, every class of the tile in S.
-    const bool chunk_full = (c + 1) * kBwKC <= B && j0 + kDwCls <= (int64_t)K;
-    u32x4_t recv[GROUPS], qv[GROUPS];
 #pragma unroll
     for (int u = 0; u < GROUPS; ++u) {
-      ds_read_128<0>(recv[u], lds_addr(dw_q<S>()) + 16 * prow[u]);
-      ds_read_128<0>(qv[u], lds_addr(dw_r<S>()) + (prow[u] * kDwCls + pcol[u]) * 2);
+      const uint32_t ra = lds_addr(dw_r<S>()) + ptr_off[u];
+      ds_read_tr_b64<0>(in.qlo[u], ra);
+      ds_read_tr_b64<4 * kDwCls * 2>(in.qhi[u], ra);
+      const uint32_t qa = lds_addr(dw_q<S>()) + 64 * prg[u];
+      ds_read_128<0>(in.rq[u][0], qa);
+      ds_read_128<16>(in.rq[u][1], qa);
+      ds_read_128<32>(in.rq[u][2], qa);
+      ds_read_128<48>(in.rq[u][3], qa);
     }
-    lgkm_wait<0>();
+  };
+  constexpr int kProdReads = 6 * GROUPS;   // LDS reads of produce_load
+  auto produce_store = [&](auto st, ProdIn& in) {
+    constexpr int S = decltype(st)::value;
 #pragma unroll
     for (int u = 0; u < GROUPS; ++u) {
-      pin_reg(recv[u]);
-      pin_reg(qv[u]);
-      const int64_t jg = j0 + pcol[u];
-      const float rec_off = __uint_as_float(recv[u].x);   // lse log2 e - log2(1/||x||)
-      const bool rok = c * kBwKC + prow[u] < B;
-      const int tpos = (int)__uint_as_float(recv[u].z) - (int)jg;
-      const uint4 q = as_uint4(qv[u]);
-      float v[8];
-      if (chunk_full && !__any((unsigned)tpos < 8u)) {
+      pin_reg(in.qlo[u]);
+      pin_reg(in.qhi[u]);
+      pin_reg(in.rq[u][0]);
+      pin_reg(in.rq[u][1]);
+      pin_reg(in.rq[u][2]);
+      pin_reg(in.rq[u][3]);
+      const int jc = (int)j0 + pcls[u];   // the class's position in S
+      const uint32_t qw[4] = {in.qlo[u].x, in.qlo[u].y, in.qhi[u].x, in.qhi[u].y};
+      float off[8];
+      int lab[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = p_of((int16_t)u16_at(q, e), s2q, rec_off);
+      for (int e2 = 0; e2 < 4; ++e2) {
+        off[2 * e2] = __uint_as_float(in.rq[u][e2].x);
+        lab[2 * e2] = (int)in.rq[u][e2].y;
+        off[2 * e2 + 1] = __uint_as_float(in.rq[u][e2].z);
+        lab[2 * e2 + 1] = (int)in.rq[u][e2].w;
+      }
+      bool has_t = false;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) has_t |= lab[e] == jc;
+      float v[8];
+      if (tile_full && !__any(has_t)) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          v[e] = p_of((int16_t)(qw[e >> 1] >> (16 * (e & 1))), s2q, off[e]);
       } else {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const bool keep = rok && tpos != e && jg + e < K;
-          v[e] = keep ? p_of((int16_t)u16_at(q, e), s2q, rec_off) : 0.0f;
+          const float pe = p_of((int16_t)(qw[e >> 1] >> (16 * (e & 1))), s2q, off[e]);
+          v[e] = (lab[e] != jc && jc < K) ? pe : 0.0f;
         }
       }
       const uint4 o = pack8<Bf16Tag>(v);
-      ds_write_128<0>(lds_addr(dw_g<S>()) + (prow[u] * kGLd + pcol[u]) * 2,
+      const int cl = pcls[u];
+      ds_write_128<0>(lds_addr(dw_g<S>()) + cl * kBwKC * 2 + 16 * (prg[u] ^ ((cl >> 1) & 3)),
                       u32x4_t{o.x, o.y, o.z, o.w});
     }
   };
 
-  const int fg = lane >> 4, fsrc = lane & 15;
-  const uint32_t a_lane =
-      ((8 * (fg >> 1) + (fsrc >> 2)) * kRowLd + 16 * (fg & 1) + 4 * (fsrc & 3) + 128 * wi) * 2;
-  const uint32_t b_lane =
-      ((8 * (fg >> 1) + (fsrc >> 2)) * kGLd + 16 * (fg & 1) + 4 * (fsrc & 3) + 64 * wj) * 2;
+  // Fragment byte offsets: operand row (d entry or class) 32 q + l32 of the
+  // wave's block, chunk 2 kk + half stored at chunk ^ ((row >> 1) & 3).
+  const int sw = (l32 >> 1) & 3;
+  const uint32_t a_lane0 = (uint32_t)((128 * wi + l32) * kBwKC * 2 + 16 * ((0 + half) ^ sw));
+  const uint32_t a_lane1 = (uint32_t)((128 * wi + l32) * kBwKC * 2 + 16 * ((2 + half) ^ sw));
+  const uint32_t b_lane0 = (uint32_t)((64 * wj + l32) * kBwKC * 2 + 16 * ((0 + half) ^ sw));
+  const uint32_t b_lane1 = (uint32_t)((64 * wj + l32) * kBwKC * 2 + 16 * ((2 + half) ^ sw));
 
   f32x16_t acc[4][2];
   zero_acc(acc);
@@ -558,55 +628,63 @@ __global__ void __launch_bounds__(128 * WI) k_dw16(
     dma_raw(S1{}, 1);
     dma_x(S1{}, 1);
     dma_raw(S2{}, 2);
-    wait_vmcnt_lgkm0<2 * (RDMA + 1) + XROWS>();
+    wait_vmcnt_lgkm0<2 * (RDMA + 1) + XDMA>();
     stage_barrier();
-    produce(S0{}, 0);
+    ProdIn in0;
+    produce_load(S0{}, in0);
+    lgkm_wait<0>();
+    produce_store(S0{}, in0);
   }
   for (int c = 0; c < c_stop; c += 3) {
     static_for<0, 3>([&](auto uu) {
       constexpr int u = decltype(uu)::value;
       const int cu = c + u;
-      // Landed: X rows of chunk cu, raw data of chunk cu + 1; this wave's
+      // Landed: X^T of chunk cu, raw data of chunk cu + 1; this wave's
       // coefficient writes of the previous iteration are complete.
       wait_vmcnt_lgkm0<PER_ITER>();
       stage_barrier();
-      const uint32_t xbs = lds_addr(dw_x<u>()) + a_lane;
-      const uint32_t gbs = lds_addr(dw_g<u>()) + b_lane;
-      u32x2_t alo[2][4], ahi[2][4], blo[2][2], bhi[2][2];
-      static_for<0, 2>([&](auto kq) {
-        constexpr int kk = decltype(kq)::value;
-        static_for<0, 4>([&](auto mm) {
-          constexpr int mb = decltype(mm)::value;
-          ds_read_tr_b64<((16 * kk) * kRowLd + 32 * mb) * 2>(alo[kk][mb], xbs);
-          ds_read_tr_b64<((16 * kk + 4) * kRowLd + 32 * mb) * 2>(ahi[kk][mb], xbs);
-        });
-        static_for<0, 2>([&](auto nn) {
-          constexpr int nb = decltype(nn)::value;
-          ds_read_tr_b64<((16 * kk) * kGLd + 32 * nb) * 2>(blo[kk][nb], gbs);
-          ds_read_tr_b64<((16 * kk + 4) * kGLd + 32 * nb) * 2>(bhi[kk][nb], gbs);
-        });
+      const uint32_t xs = lds_addr(dw_x<u>());
+      const uint32_t gs = lds_addr(dw_g<u>());
+      // The producer's reads go first: they are consumed while the first
+      // k-step's MFMAs run.
+      ProdIn pin;
+      produce_load(std::integral_constant<int, (u + 1) % 3>{}, pin);
+      u32x4_t af[2][4], bf[2][2];
+      static_for<0, 4>([&](auto mm) {
+        constexpr int mb = decltype(mm)::value;
+        ds_read_128<32 * mb * kBwKC * 2>(af[0][mb], xs + a_lane0);
+      });
+      static_for<0, 2>([&](auto nn) {
+        constexpr int nb = decltype(nn)::value;
+        ds_read_128<32 * nb * kBwKC * 2>(bf[0][nb], gs + b_lane0);
+      });
+      static_for<0, 4>([&](auto mm) {
+        constexpr int mb = decltype(mm)::value;
+        ds_read_128<32 * mb * kBwKC * 2>(af[1][mb], xs + a_lane1);
+      });
+      static_for<0, 2>([&](auto nn) {
+        constexpr int nb = decltype(nn)::value;
+        ds_read_128<32 * nb * kBwKC * 2>(bf[1][nb], gs + b_lane1);
       });
       dma_raw(std::integral_constant<int, u>{}, cu + 3);
       dma_x(std::integral_constant<int, (u + 2) % 3>{}, cu + 2);
       static_for<0, 2>([&](auto kq) {
         constexpr int kk = decltype(kq)::value;
         if constexpr (kk == 0) {
-          lgkm_wait<12>(alo[0][0], alo[0][1], alo[0][2], alo[0][3], ahi[0][0], ahi[0][1],
-                        ahi[0][2], ahi[0][3], blo[0][0], blo[0][1], bhi[0][0], bhi[0][1]);
+          // producer reads and the first k-step's fragments have landed
+          lgkm_wait<6>(af[0][0], af[0][1], af[0][2], af[0][3], bf[0][0], bf[0][1]);
         } else {
           // the next coefficients are produced while the first k-step's MFMAs run
-          produce(std::integral_constant<int, (u + 1) % 3>{}, cu + 1);
-          lgkm_wait<0>(alo[1][0], alo[1][1], alo[1][2], alo[1][3], ahi[1][0], ahi[1][1],
-                       ahi[1][2], ahi[1][3], blo[1][0], blo[1][1], bhi[1][0], bhi[1][1]);
+          produce_store(std::integral_constant<int, (u + 1) % 3>{}, pin);
+          lgkm_wait<0>(af[1][0], af[1][1], af[1][2], af[1][3], bf[1][0], bf[1][1]);
         }
         if (cu < n_chunks) {
 #pragma unroll
           for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
             for (int nb = 0; nb < 2; ++nb)
-              acc[mb][nb] = mfma_32x32x16(frag_of(alo[kk][mb], ahi[kk][mb]),
-                                          frag_of(blo[kk][nb], bhi[kk][nb]), acc[mb][nb],
-                                          Bf16Tag{});
+              acc[mb][nb] = mfma_32x32x16(as_uint4(af[kk][mb]), as_uint4(bf[kk][nb]),
+                                          acc[mb][nb], Bf16Tag{});
         }
       });
     });
@@ -895,7 +973,7 @@ void launch_bwd16(const StepArgs& a, const StepWs& w, const Margin& mg, float sB
   timing_stop(5, stream);
   timing_start(6, stream);
   hipLaunchKernelGGL((k_dw16<Tag, WI>), dim3((unsigned)ceil_div(a.cap, kDwCls)), dim3(128 * WI),
-                     0, stream, (const uint16_t*)w.xb, a.X, (uint16_t*)a.W, a.W_master, a.M,
+                     0, stream, (const uint16_t*)w.xbT, w.ld_xt, a.X, (uint16_t*)a.W, a.W_master, a.M,
                      a.active, a.n_active, a.labels_mapped, a.row_lse, w.inv_x, w.inv_w,
                      w.row_rec, (const int16_t*)w.cosq, w.ld_cos, B, mg, sB, a.lr, a.mu);
   timing_stop(6, stream);

@@ -51,7 +51,9 @@ constexpr int kFwdClassTile = 256;
 
 struct StepWs {
   float* inv_x;          // [B]      1/max(||x_n||, eps)
-  void* xb;              // [B x d] X in bf16 (operand of the class-gradient contraction)
+  void* xbT;             // [ld_xt / 32][d][32] X transposed in blocks of 32 rows, bf16, zero
+                         // past B (the class-gradient operand)
+  int64_t ld_xt;         // B rounded up to 32
   float* inv_w_max;      // [1] max_j 1/||W[S_j]|| (scale of the fp16 feature-gradient operand)
   float* inv_w;          // [ld_cos] 1/max(||W[S_j]||, eps)
   void* cosq;            // [B x ld_cos] quantised cosines (int16) or fp32 cosines
@@ -62,7 +64,8 @@ struct StepWs {
   float* dx_part;        // [n_split x B x d] split-K partial sums of dX_hat
   int n_split;
   float* loss_part;      // [B] per-row loss terms
-  float4* row_rec;       // [B] (lse log2 e, 1/||x||, label, 0) for the class-gradient kernel
+  float2* row_rec;       // [ld_xt] (lse log2 e - log2(1/||x||), label bits) for the class-gradient
+                         // kernel; rows past B hold (+inf, -1)
 };
 
 // Layout of the whole workspace (offsets in bytes from its base).
@@ -73,7 +76,7 @@ struct WsLayout {
   size_t off_grp_sure, off_grp_tie, off_grp_out, off_grp_tie_off;
   size_t off_inv_x, off_xb, off_wmax, off_inv_w, off_cos, off_stats, off_tgt, off_dx, off_loss,
       off_rec;
-  int64_t ld_cos, n_ctiles, n_groups;
+  int64_t ld_cos, n_ctiles, n_groups, ld_xt;
   int n_split;
   int top_bits;
 };

@@ -25,32 +25,58 @@ __device__ __forceinline__ float sumsq8(const uint4& v) {
   return acc;
 }
 
-// inv_x[n] and the bf16 copy xb[n][i] of the batch (the MFMA operand of the
-// class-gradient contraction); also clears the running max of 1/||w_j||.
+// inv_x[n] and a transposed bf16 copy of the batch in blocks of 32 rows
+// (block c = [d][32]: entry (i, r) = X[32 c + r][i]), the K-major operand of
+// the class-gradient contraction; a workgroup transposes one block through
+// LDS.  Rows n in [B, ld_xt) are zero and their row records (+inf, -1), so
+// the padded rows drop out of that contraction.  Also clears the running
+// max of 1/||w_j||.
+constexpr int kPrepRows = 32;
 template <typename Tag>
 __global__ void __launch_bounds__(256) k_prep_x16(const uint16_t* __restrict__ X, int B, int d,
-                                                  float* __restrict__ inv_x,
-                                                  uint16_t* __restrict__ xb,
+                                                  int64_t ld_xt, float* __restrict__ inv_x,
+                                                  uint16_t* __restrict__ xbT,
+                                                  float2* __restrict__ row_rec,
                                                   float* __restrict__ inv_w_max) {
-  const int lane = threadIdx.x & 63;
-  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
+  __shared__ uint16_t tile[kPrepRows][512 + 8];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n0 = blockIdx.x * kPrepRows;
   if (blockIdx.x == 0 && threadIdx.x == 0) *inv_w_max = 0.0f;
-  if (n >= B) return;
-  const uint16_t* row = X + (int64_t)n * d;
-  float ss = 0.0f;
-  for (int c = lane; c < d / 8; c += 64) {
-    const uint4 v = *reinterpret_cast<const uint4*>(row + 8 * c);
-    ss += sumsq8<Tag>(v);
-    const uint16_t* h = reinterpret_cast<const uint16_t*>(&v);
+  for (int r = wave; r < kPrepRows; r += 4) {
+    const int n = n0 + r;
+    float ss = 0.0f;
+    for (int c = lane; c < d / 8; c += 64) {
+      uint4 ov = make_uint4(0, 0, 0, 0);
+      if (n < B) {
+        const uint4 v = *reinterpret_cast<const uint4*>(X + (int64_t)n * d + 8 * c);
+        ss += sumsq8<Tag>(v);
+        const uint16_t* h = reinterpret_cast<const uint16_t*>(&v);
+        uint16_t o[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = float_to_bf16(to_float<Tag>(h[e]));
+        __builtin_memcpy(&ov, o, 16);
+      }
+      *reinterpret_cast<uint4*>(&tile[r][8 * c]) = ov;
+    }
+    ss = wave_sum(ss);
+    if (lane == 0) {
+      if (n < B) inv_x[n] = 1.0f / fmaxf(sqrtf(ss), kEpsNorm);
+      else if (n < ld_xt) row_rec[n] = make_float2(INFINITY, __int_as_float(-1));
+    }
+  }
+  __syncthreads();
+  // Column i of the tile (32 rows) -> block blockIdx.x of xbT, row i: four
+  // 16-byte pieces (the block is contiguous: [d][32]).
+  uint16_t* blk = xbT + (int64_t)blockIdx.x * d * kPrepRows;
+  for (int q = threadIdx.x; q < d * 4; q += 256) {
+    const int i = q >> 2, r0 = (q & 3) * 8;
     uint16_t o[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) o[e] = float_to_bf16(to_float<Tag>(h[e]));
+    for (int e = 0; e < 8; ++e) o[e] = tile[r0 + e][i];
     uint4 ov;
     __builtin_memcpy(&ov, o, 16);
-    *reinterpret_cast<uint4*>(xb + (int64_t)n * d + 8 * c) = ov;
+    *reinterpret_cast<uint4*>(blk + i * kPrepRows + r0) = ov;
   }
-  ss = wave_sum(ss);
-  if (lane == 0) inv_x[n] = 1.0f / fmaxf(sqrtf(ss), kEpsNorm);
 }
 
 // 1/||W[S_j]|| of the active rows: one wavefront per row (grid-stride), and
@@ -127,14 +153,16 @@ hipError_t launch_prep(const StepArgs& a, const StepWs& w, hipStream_t stream) {
     hipLaunchKernelGGL(k_norm_w32, dim3(wblocks), dim3(256), 0, stream, (const float*)a.W, d,
                        a.active, a.n_active, a.cap, w.inv_w);
   } else if (a.dtype == 1) {
-    hipLaunchKernelGGL(k_prep_x16<Bf16Tag>, dim3((unsigned)ceil_div(B, 4)), dim3(256), 0,
-                       stream, (const uint16_t*)a.X, B, d, w.inv_x, (uint16_t*)w.xb, w.inv_w_max);
+    hipLaunchKernelGGL(k_prep_x16<Bf16Tag>, dim3((unsigned)(w.ld_xt / kPrepRows)), dim3(256), 0,
+                       stream, (const uint16_t*)a.X, B, d, w.ld_xt, w.inv_x, (uint16_t*)w.xbT,
+                       w.row_rec, w.inv_w_max);
     hipLaunchKernelGGL(k_norm_w16<Bf16Tag>, dim3(wblocks16), dim3(256), 0, stream,
                        (const uint16_t*)a.W, d, a.active, a.n_active, a.cap, w.inv_w,
                        w.inv_w_max);
   } else {
-    hipLaunchKernelGGL(k_prep_x16<F16Tag>, dim3((unsigned)ceil_div(B, 4)), dim3(256), 0,
-                       stream, (const uint16_t*)a.X, B, d, w.inv_x, (uint16_t*)w.xb, w.inv_w_max);
+    hipLaunchKernelGGL(k_prep_x16<F16Tag>, dim3((unsigned)(w.ld_xt / kPrepRows)), dim3(256), 0,
+                       stream, (const uint16_t*)a.X, B, d, w.ld_xt, w.inv_x, (uint16_t*)w.xbT,
+                       w.row_rec, w.inv_w_max);
     hipLaunchKernelGGL(k_norm_w16<F16Tag>, dim3(wblocks16), dim3(256), 0, stream,
                        (const uint16_t*)a.W, d, a.active, a.n_active, a.cap, w.inv_w,
                        w.inv_w_max);
