@@ -53,7 +53,9 @@ def algorithmic_work(name, cfg, K):
     if name == "dw_update":
         return cm.contraction_flops(B, d, K), cm.update_bytes(K, d, dt, cfg["master"])
     if name == "prep":
-        return 0, cm.gather_bytes(K, d, dt) + B * d * xb
+        # the batch side only: X read, its transposed bf16 copy written (the
+        # class-row norms come out of the forward contraction kernel)
+        return 0, B * d * (xb + 2)
     return 0, 0
 
 

@@ -25,6 +25,7 @@ constexpr int kFwdThreads = 256;  // 4 waves: 2 (classes) x 2 (rows), 128 x 64 e
 constexpr int kFwdStageA = kFwdBM * kFwdKC;  // uint16 elements per stage, class operand
 constexpr int kFwdStageB = kFwdBN * kFwdKC;  // uint16 elements per stage, batch operand
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kEpsNormW = 1e-12f;  // ||w|| floor of the normalisation
 
 // Three-stage LDS ring per operand (24 KB per stage; 75 KB in all, so two
 // workgroups share a CU and one's epilogue overlaps the other's MFMA loop).
@@ -39,6 +40,7 @@ __shared__ __attribute__((aligned(1024))) uint16_t fB0[kFwdStageB], fB1[kFwdStag
     fB2[kFwdStageB];
 __shared__ float2 fRed[2][kFwdBN];
 __shared__ __attribute__((aligned(16))) float fIw[kFwdBM];
+__shared__ float fNrm[2][kFwdBM];
 
 template <int S>
 __device__ __forceinline__ uint16_t* fwd_a() {
@@ -77,11 +79,27 @@ __device__ __forceinline__ void fwd_issue(const uint16_t* const ap[4], const uin
   for (int u = 0; u < 2; ++u) dma16(bp[u] + k0, fwd_b<S>() + (2 * wave + u) * 16 * kFwdKC);
 }
 
+// a0^2 + a1^2 + acc for a packed pair of 16-bit values (v_dot2_f32_*).
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ float sumsq2(uint32_t v, float acc, F16Tag) {
+  const f16x2_t h = __builtin_bit_cast(f16x2_t, v);
+  return __builtin_amdgcn_fdot2(h, h, acc, false);
+}
+__device__ __forceinline__ float sumsq2(uint32_t v, float acc, Bf16Tag) {
+  const bf16x2_t h = __builtin_bit_cast(bf16x2_t, v);
+  return __builtin_amdgcn_fdot2_f32_bf16(h, h, acc, false);
+}
+
 // Fragments of both 16-wide k-steps of a stage are requested first, then
 // consumed: lane l reads row 32 q + l % 32 of its operand block, chunk
-// 2 kk + l / 32 (stored at chunk ^ ((row >> 1) & 3)).
+// 2 kk + l / 32 (stored at chunk ^ ((row >> 1) & 3)).  The class-operand
+// fragments also feed the class-row norms: the wave with wn == kk adds the
+// squares of its k-step's fragments to wss[mb] (class row 128 wm + 32 mb +
+// l % 32, elements 8 (l / 32) .. + 7 of the k-step).
 template <int S, typename Tag>
-__device__ __forceinline__ void fwd_compute(f32x16_t (&acc)[4][2], int wm, int wn, int lane) {
+__device__ __forceinline__ void fwd_compute(f32x16_t (&acc)[4][2], int wm, int wn, int lane,
+                                            float (&wss)[4]) {
   const int r32 = lane & 31;
   const int sw = (lane >> 1) & 3;
   const uint32_t arow = lds_addr(fwd_a<S>()) + (128 * wm + r32) * kFwdKC * 2;
@@ -105,6 +123,15 @@ __device__ __forceinline__ void fwd_compute(f32x16_t (&acc)[4][2], int wm, int w
       lgkm_wait<6>(af[0][0], af[0][1], af[0][2], af[0][3], bf[0][0], bf[0][1]);
     else
       lgkm_wait<0>(af[1][0], af[1][1], af[1][2], af[1][3], bf[1][0], bf[1][1]);
+    if (wn == kk) {
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb) {
+        wss[mb] = sumsq2(af[kk][mb].x, wss[mb], Tag{});
+        wss[mb] = sumsq2(af[kk][mb].y, wss[mb], Tag{});
+        wss[mb] = sumsq2(af[kk][mb].z, wss[mb], Tag{});
+        wss[mb] = sumsq2(af[kk][mb].w, wss[mb], Tag{});
+      }
+    }
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
@@ -194,9 +221,9 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
     const int32_t* __restrict__ active, const int32_t* __restrict__ n_active_p,
     const int32_t* __restrict__ yhat, const float* __restrict__ inv_x,
-    const float* __restrict__ inv_w, int B, int64_t ld_cos, int64_t n_ctiles, int n_rt,
-    int64_t n_tiles, int64_t per_xcd, Margin mg, int16_t* __restrict__ cosq,
-    float2* __restrict__ stats, float* __restrict__ tgt) {
+    float* __restrict__ inv_w, float* __restrict__ inv_w_max, int B, int64_t ld_cos,
+    int64_t n_ctiles, int n_rt, int64_t n_tiles, int64_t per_xcd, Margin mg,
+    int16_t* __restrict__ cosq, float2* __restrict__ stats, float* __restrict__ tgt) {
   constexpr int D = NK * kFwdKC;
   // All batch-row tiles of a class tile run on one XCD: the gathered W rows
   // come from HBM once and are re-read from that XCD's L2.
@@ -239,10 +266,7 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.0f;
 
-  // Epilogue inputs, requested before the main loop: 1/||w|| of the tile's
-  // classes (one direct-to-LDS load by wave 0; it is the oldest load of that
-  // wave, so the loop's first wait covers it) and each lane's row data.
-  if (wave == 0) dma16(inv_w + j0 + 4 * lane, fIw);
+  // Epilogue inputs, requested before the main loop: each lane's row data.
   float ixr[2];
   int yhr[2];
 #pragma unroll
@@ -252,6 +276,7 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
     yhr[nb] = n < B ? yhat[n] : -1;
   }
 
+  float wss[4] = {0.0f, 0.0f, 0.0f, 0.0f};  // partial ||w||^2 of the lane's class rows
   constexpr int kPerStage = 6;  // DMAs per thread per stage
   fwd_issue<0>(ap, bp, 0, wave);
   if constexpr (NK > 1) fwd_issue<1>(ap, bp, kFwdKC, wave);
@@ -263,8 +288,31 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
     wait_vmcnt<kPerStage * ahead>();
     stage_barrier();
     if constexpr (c + 2 < NK) fwd_issue<(c + 2) % 3>(ap, bp, (c + 2) * kFwdKC, wave);
-    fwd_compute<c % 3, Tag>(acc, wm, wn, lane);
+    fwd_compute<c % 3, Tag>(acc, wm, wn, lane, wss);
   });
+
+  // Inverse norms of the tile's class rows (stage 3 of the step, computed from
+  // the rows this kernel streams anyway): the four partial sums of a row
+  // (lane halves, and the two waves wn = 0, 1) meet in LDS; the norms stay in
+  // LDS for the epilogue, and the first batch-row tile of each class tile
+  // also publishes them, and their running maximum, for the backward kernels.
+  {
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) {
+      const float s = wss[mb] + __shfl_xor(wss[mb], 32, 64);
+      if (half == 0) fNrm[wn][128 * wm + 32 * mb + l32] = s;
+    }
+    wait_lgkm0();
+    stage_barrier();
+    const float inv = 1.0f / fmaxf(sqrtf(fNrm[0][tid] + fNrm[1][tid]), kEpsNormW);
+    fIw[tid] = inv;
+    if (rt == 0) {
+      const bool jok = j0 + tid < (int64_t)K;
+      if (jok) inv_w[j0 + tid] = inv;
+      const float m = wave_max(jok ? inv : 0.0f);
+      if (lane == 0) atomicMax(reinterpret_cast<int*>(inv_w_max), __float_as_int(m));
+    }
+  }
 
   // ---- epilogue.  The quantised 256-class x 128-row cosine tile is
   // assembled in the (now idle) LDS ring (rows of 512 B, 16-byte block b of
@@ -412,8 +460,8 @@ void launch_fwd16_nk(unsigned grid, hipStream_t stream, const StepArgs& a, const
                      int n_rt, int64_t n_tiles, int64_t per_xcd, const Margin& mg) {
   hipLaunchKernelGGL((k_fwd16<Tag, NK>), dim3(grid), dim3(kFwdThreads), 0, stream,
                      (const uint16_t*)a.X, (const uint16_t*)a.W, a.active, a.n_active,
-                     a.labels_mapped, w.inv_x, w.inv_w, B, w.ld_cos, w.n_ctiles, n_rt, n_tiles,
-                     per_xcd, mg, (int16_t*)w.cosq, w.stats, w.tgt);
+                     a.labels_mapped, w.inv_x, w.inv_w, w.inv_w_max, B, w.ld_cos, w.n_ctiles,
+                     n_rt, n_tiles, per_xcd, mg, (int16_t*)w.cosq, w.stats, w.tgt);
 }
 
 template <typename Tag>

@@ -4,8 +4,10 @@
 //
 // The normalised rows are never materialised: the contractions use the raw
 // 16-bit rows (exact products in fp32) and apply 1/||x_n|| and 1/||w_j|| as
-// row / column scales.  These kernels read each row once with 16-byte
-// loads, one wavefront per row (a 512-wide 16-bit row is exactly 64 x 16 B).
+// row / column scales.  On the 16-bit paths the class-row norms come out of
+// the forward contraction kernel, which streams every active row through
+// LDS anyway; this file holds the batch side (norms, the transposed bf16
+// copy used by the class-gradient contraction) and the fp32 path.
 #include "pfc_device.h"
 
 namespace pfc {
@@ -79,37 +81,6 @@ __global__ void __launch_bounds__(256) k_prep_x16(const uint16_t* __restrict__ X
   }
 }
 
-// 1/||W[S_j]|| of the active rows: one wavefront per row (grid-stride), and
-// the running maximum over all rows (one atomic per workgroup).
-template <typename Tag>
-__global__ void __launch_bounds__(256) k_norm_w16(const uint16_t* __restrict__ W, int d,
-                                                  const int32_t* __restrict__ active,
-                                                  const int32_t* __restrict__ n_active,
-                                                  int64_t cap, float* __restrict__ inv_w,
-                                                  float* __restrict__ inv_w_max) {
-  __shared__ float wmax[4];
-  const int lane = threadIdx.x & 63;
-  const int64_t K = *n_active < cap ? *n_active : cap;
-  float mx = 0.0f;
-  for (int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); j < K; j += (int64_t)gridDim.x * 4) {
-    const uint16_t* row = W + (int64_t)active[j] * d;
-    float ss = 0.0f;
-    for (int c = lane; c < d / 8; c += 64)
-      ss += sumsq8<Tag>(*reinterpret_cast<const uint4*>(row + 8 * c));
-    ss = wave_sum(ss);
-    const float inv = 1.0f / fmaxf(sqrtf(ss), kEpsNorm);
-    if (lane == 0) inv_w[j] = inv;
-    mx = fmaxf(mx, inv);
-  }
-  if (lane == 0) wmax[threadIdx.x >> 6] = mx;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const float m = fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]));
-    // Positive floats order like their bit patterns.
-    atomicMax(reinterpret_cast<int*>(inv_w_max), __float_as_int(m));
-  }
-}
-
 __global__ void __launch_bounds__(256) k_prep_x32(const float* __restrict__ X, int B, int d,
                                                   float* __restrict__ inv_x) {
   const int lane = threadIdx.x & 63;
@@ -145,7 +116,6 @@ __global__ void __launch_bounds__(256) k_norm_w32(const float* __restrict__ W, i
 hipError_t launch_prep(const StepArgs& a, const StepWs& w, hipStream_t stream) {
   const int B = (int)a.B, d = (int)a.d;
   const unsigned wblocks = (unsigned)ceil_div(a.cap, 4);
-  const unsigned wblocks16 = (unsigned)(ceil_div(a.cap, 4) < 4096 ? ceil_div(a.cap, 4) : 4096);
   timing_start(1, stream);
   if (a.dtype == 0) {
     hipLaunchKernelGGL(k_prep_x32, dim3((unsigned)ceil_div(B, 4)), dim3(256), 0, stream,
@@ -156,16 +126,10 @@ hipError_t launch_prep(const StepArgs& a, const StepWs& w, hipStream_t stream) {
     hipLaunchKernelGGL(k_prep_x16<Bf16Tag>, dim3((unsigned)(w.ld_xt / kPrepRows)), dim3(256), 0,
                        stream, (const uint16_t*)a.X, B, d, w.ld_xt, w.inv_x, (uint16_t*)w.xbT,
                        w.row_rec, w.inv_w_max);
-    hipLaunchKernelGGL(k_norm_w16<Bf16Tag>, dim3(wblocks16), dim3(256), 0, stream,
-                       (const uint16_t*)a.W, d, a.active, a.n_active, a.cap, w.inv_w,
-                       w.inv_w_max);
   } else {
     hipLaunchKernelGGL(k_prep_x16<F16Tag>, dim3((unsigned)(w.ld_xt / kPrepRows)), dim3(256), 0,
                        stream, (const uint16_t*)a.X, B, d, w.ld_xt, w.inv_x, (uint16_t*)w.xbT,
                        w.row_rec, w.inv_w_max);
-    hipLaunchKernelGGL(k_norm_w16<F16Tag>, dim3(wblocks16), dim3(256), 0, stream,
-                       (const uint16_t*)a.W, d, a.active, a.n_active, a.cap, w.inv_w,
-                       w.inv_w_max);
   }
   timing_stop(1, stream);
   return hipGetLastError();

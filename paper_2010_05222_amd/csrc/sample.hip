@@ -205,10 +205,12 @@ __global__ void __launch_bounds__(256) k_keys_hist(uint64_t seed, int64_t a, int
   const int nbins = 1 << top_bits;
   for (int i = threadIdx.x; i < nbins; i += blockDim.x) lhist[i] = 0u;
   __syncthreads();
+  // Grid-stride over the Philox blocks of the shard: each workgroup builds
+  // one histogram of its share and flushes it once.
   const int64_t q_lo = a >> 2;
   const int64_t q_hi = (a + C - 1) >> 2;
-  const int64_t q = q_lo + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (q <= q_hi) {
+  for (int64_t q = q_lo + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q <= q_hi;
+       q += (int64_t)gridDim.x * blockDim.x) {
     const U64x4 w = philox4x64_10((uint64_t)q, seed);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -219,9 +221,13 @@ __global__ void __launch_bounds__(256) k_keys_hist(uint64_t seed, int64_t a, int
     }
   }
   __syncthreads();
+  // Flush starting at a per-workgroup offset so that workgroups finishing
+  // together hit different bins.
+  const int rot = (int)((blockIdx.x * 97u) & (uint32_t)(nbins - 1));
   for (int i = threadIdx.x; i < nbins; i += blockDim.x) {
-    const uint32_t h = lhist[i];
-    if (h) atomicAdd(&hist[i], h);
+    const int b = (i + rot) & (nbins - 1);
+    const uint32_t h = lhist[b];
+    if (h) atomicAdd(&hist[b], h);
   }
 }
 
@@ -472,7 +478,8 @@ hipError_t launch_sample(const int64_t* labels, int64_t B, int64_t C, int64_t a,
                      labels, B, C, a, w.bitmap, w.state);
   hipLaunchKernelGGL(k_sample_plan, dim3(1), dim3(64), 0, stream, w.state, budget, C);
   const int64_t n_blocks_philox = ((a + C - 1) >> 2) - (a >> 2) + 1;
-  hipLaunchKernelGGL(k_keys_hist, dim3((unsigned)ceil_div(n_blocks_philox, 256)), dim3(256), 0,
+  const int64_t hist_wgs = ceil_div(n_blocks_philox, 256);
+  hipLaunchKernelGGL(k_keys_hist, dim3((unsigned)(hist_wgs < 512 ? hist_wgs : 512)), dim3(256), 0,
                      stream, seed, a, C, top_bits, w.bitmap, w.keys, w.hist, w.state);
   hipLaunchKernelGGL(k_select_top, dim3(1), dim3(1024), 0, stream, w.hist, top_bits, w.state);
   hipLaunchKernelGGL(k_collect, dim3((unsigned)ceil_div(C, 1024)), dim3(256), 0, stream, w.keys,
