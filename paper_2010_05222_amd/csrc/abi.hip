@@ -85,6 +85,8 @@ WsLayout ws_layout(int64_t B, int64_t d, int64_t C, int64_t cap, int compute) {
   L.ld_cos = round_up(cap, 256);
   L.n_ctiles = ceil_div(cap, kFwdClassTile);
   L.ld_xt = round_up(B, 32);
+  L.ld_g = round_up(B, 128);
+  L.n_lgroups = L.ld_cos / kLogitGroup;
   if (compute == PFC_F32) {
     L.n_split = 1;
   } else {
@@ -106,7 +108,9 @@ WsLayout ws_layout(int64_t B, int64_t d, int64_t C, int64_t cap, int compute) {
   L.off_tgt = take((size_t)B * 4);
   L.off_dx = take((size_t)L.n_split * B * d * 4);
   L.off_loss = take((size_t)B * 4);
-  L.off_rec = take((size_t)L.ld_xt * 8);
+  L.off_tgtc = take((size_t)B * 4);
+  L.off_gmax = take(compute == PFC_F32 ? 0 : (size_t)L.n_lgroups * L.ld_g * 4);
+  L.off_gscale = take(compute == PFC_F32 ? 0 : (size_t)L.n_lgroups * L.ld_g * 4);
   L.bytes = off;
   return L;
 }
@@ -134,7 +138,7 @@ StepWs step_ws(void* ws, const WsLayout& L) {
   w.ld_xt = L.ld_xt;
   w.inv_w_max = (float*)(b + L.off_wmax);
   w.inv_w = (float*)(b + L.off_inv_w);
-  w.cosq = b + L.off_cos;
+  w.lbuf = b + L.off_cos;
   w.ld_cos = L.ld_cos;
   w.stats = (float2*)(b + L.off_stats);
   w.n_ctiles = L.n_ctiles;
@@ -142,7 +146,11 @@ StepWs step_ws(void* ws, const WsLayout& L) {
   w.dx_part = (float*)(b + L.off_dx);
   w.n_split = L.n_split;
   w.loss_part = (float*)(b + L.off_loss);
-  w.row_rec = (float2*)(b + L.off_rec);
+  w.tgtc = (float*)(b + L.off_tgtc);
+  w.gmax = (float*)(b + L.off_gmax);
+  w.gscale = (float*)(b + L.off_gscale);
+  w.ld_g = L.ld_g;
+  w.n_groups = L.n_lgroups;
   return w;
 }
 

@@ -45,6 +45,7 @@ __shared__ __attribute__((aligned(1024))) uint16_t xW0[kRowStage], xW1[kRowStage
 __shared__ __attribute__((aligned(1024))) int16_t xR0[kDxRows * kBwKC], xR1[kDxRows * kBwKC],
     xR2[kDxRows * kBwKC];
 __shared__ __attribute__((aligned(16))) float xI0[kBwKC], xI1[kBwKC], xI2[kBwKC];
+__shared__ __attribute__((aligned(16))) float xS0[kDxRows], xS1[kDxRows], xS2[kDxRows];
 __shared__ __attribute__((aligned(1024))) uint16_t xG0[kDxRows * kBwKC], xG1[kDxRows * kBwKC],
     xG2[kDxRows * kBwKC];
 // dW: X^T rows (K-major: d rows of 32 batch rows, bf16), raw cosines
@@ -55,7 +56,7 @@ __shared__ __attribute__((aligned(1024))) uint16_t xG0[kDxRows * kBwKC], xG1[kDx
 __shared__ __attribute__((aligned(1024))) uint16_t wX0[kRowStage], wX1[kRowStage], wX2[kRowStage];
 __shared__ __attribute__((aligned(1024))) int16_t wR0[kBwKC * kDwCls], wR1[kBwKC * kDwCls],
     wR2[kBwKC * kDwCls];
-__shared__ __attribute__((aligned(16))) float2 wQ0[kBwKC], wQ1[kBwKC], wQ2[kBwKC];
+__shared__ __attribute__((aligned(16))) float wQ0[kBwKC], wQ1[kBwKC], wQ2[kBwKC];
 __shared__ __attribute__((aligned(1024))) uint16_t wG0[kDwCls * kBwKC], wG1[kDwCls * kBwKC],
     wG2[kDwCls * kBwKC];
 
@@ -69,10 +70,11 @@ __shared__ __attribute__((aligned(1024))) uint16_t wG0[kDwCls * kBwKC], wG1[kDwC
 PFC_STAGE3(dx_w, uint16_t, xW0, xW1, xW2)
 PFC_STAGE3(dx_r, int16_t, xR0, xR1, xR2)
 PFC_STAGE3(dx_i, float, xI0, xI1, xI2)
+PFC_STAGE3(dx_s, float, xS0, xS1, xS2)
 PFC_STAGE3(dx_g, uint16_t, xG0, xG1, xG2)
 PFC_STAGE3(dw_x, uint16_t, wX0, wX1, wX2)
 PFC_STAGE3(dw_r, int16_t, wR0, wR1, wR2)
-PFC_STAGE3(dw_q, float2, wQ0, wQ1, wQ2)
+PFC_STAGE3(dw_q, float, wQ0, wQ1, wQ2)
 PFC_STAGE3(dw_g, uint16_t, wG0, wG1, wG2)
 #undef PFC_STAGE3
 
@@ -81,19 +83,8 @@ __device__ __forceinline__ float load16(const void* p, int64_t idx) {
   return to_float<Tag>(((const uint16_t*)p)[idx]);
 }
 
-__device__ __forceinline__ uint16_t u16_at(const uint4& v, int e) {
-  return reinterpret_cast<const uint16_t*>(&v)[e];
-}
-
-// Non-target softmax probability from a quantised cosine, in base 2:
-// p = 2^(q * s log2(e) / 32767 - lse log2(e)).
-__device__ __forceinline__ float p_of(int16_t q, float s2q, float lse2) {
-  return __builtin_amdgcn_exp2f(fmaf((float)q, s2q, -lse2));
-}
-
-// Target term of a row, (p_t - 1) * slope_t, from the quantised target cosine.
-__device__ __forceinline__ float target_coef(const Margin& mg, int16_t q, float lse) {
-  const float c = dequantise_cos(q);
+// Target term of a row, (p_t - 1) * slope_t, from its unmargined target cosine.
+__device__ __forceinline__ float target_coef(const Margin& mg, float c, float lse) {
   const float p = __expf(target_logit(mg, c) - lse);
   return (p - 1.0f) * target_slope(mg, c);
 }
@@ -158,18 +149,17 @@ __device__ __forceinline__ void zero_acc(T (&acc)[4][2]) {
 template <typename Tag, int WI>
 __global__ void __launch_bounds__(128 * WI) k_dx16(
     const uint16_t* __restrict__ W, const int32_t* __restrict__ active,
-    const int32_t* __restrict__ n_active_p, const int32_t* __restrict__ yhat,
-    const float* __restrict__ row_lse, const float* __restrict__ inv_w,
-    const float* __restrict__ inv_w_max, const int16_t* __restrict__ cosq, int64_t ld_cos, int B,
-    int n_rt, int n_split, int64_t n_tiles, int64_t per_xcd, float s,
-    float* __restrict__ dx_part) {
+    const int32_t* __restrict__ n_active_p, const float* __restrict__ inv_w,
+    const float* __restrict__ inv_w_max, const uint16_t* __restrict__ lbuf, int64_t ld_cos,
+    const float* __restrict__ gscale, int64_t ld_g, int B, int n_rt, int n_split,
+    int64_t n_tiles, int64_t per_xcd, float* __restrict__ dx_part) {
   constexpr int D = 128 * WI;
   constexpr int NT = 128 * WI;              // threads
   constexpr int NW = 2 * WI;                // waves
   constexpr int WROWS = kBwKC / NW;         // W rows DMA'd by each wave per chunk
-  constexpr int RDMA = 8 / NW;              // 1-KB raw-cosine blocks DMA'd by each wave
+  constexpr int RDMA = 8 / NW;              // 1-KB logit-store blocks DMA'd by each wave
   constexpr int GROUPS = 512 / NT;          // 8-coefficient groups per thread per chunk
-  constexpr int PER_ITER = WROWS + RDMA + 1;  // DMAs a wave issues per chunk
+  constexpr int PER_ITER = WROWS + RDMA + 2;  // DMAs a wave issues per chunk
   const int64_t t = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
   if (t >= n_tiles) return;
   // The batch-row tiles of one split share its class range: they run on one
@@ -187,26 +177,18 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wi = wave >> 1, wn = wave & 1;
-  const float s2q = s * kLog2e * kCosDequant;
   const float scale = dx_operand_scale(Tag{}, *inv_w_max);
 
-  // Coefficient-producer rows of this thread (fixed for the whole kernel).
-  // p * scale = 2^(q s log2(e) / 32767 - (lse log2(e) - log2(scale))); rows past
-  // the batch get an infinite offset (p = 0).
-  int prow[GROUPS], pchunk[GROUPS], pyh[GROUPS];
-  float plse2[GROUPS];
-  const float log2_scale = log2f(scale);
+  // Coefficient-producer slots of this thread (fixed for the whole kernel):
+  // row prow, classes 8 pchunk .. + 7 of each chunk.
+  int prow[GROUPS], pchunk[GROUPS];
 #pragma unroll
   for (int u = 0; u < GROUPS; ++u) {
     const int q = tid + NT * u;
     prow[u] = q >> 2;
     pchunk[u] = q & 3;
-    const int n = n0 + prow[u];
-    const bool ok = n < B;
-    pyh[u] = ok ? yhat[n] : -1;
-    plse2[u] = ok ? row_lse[n] * kLog2e - log2_scale : INFINITY;
   }
-  // Raw-cosine DMA of this lane: block b holds rows 16 b .. 16 b + 15.
+  // Logit-store DMA of this lane: block b holds rows 16 b .. 16 b + 15.
   int64_t rsrc[RDMA];
 #pragma unroll
   for (int v = 0; v < RDMA; ++v) {
@@ -220,9 +202,12 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
     const int64_t jb = (c < n_chunks ? c : n_chunks - 1) * kBwKC;
 #pragma unroll
     for (int v = 0; v < RDMA; ++v)
-      dma16(cosq + rsrc[v] + jb, dx_r<S>() + 512 * (wave * RDMA + v));
+      dma16(lbuf + rsrc[v] + jb, dx_r<S>() + 512 * (wave * RDMA + v));
     // 1/||w|| of the chunk's 32 classes: 8 / NW 16-byte pieces per wave.
     if (lane < 8 / NW) dma16(inv_w + jb + 4 * (wave * (8 / NW) + lane), dx_i<S>() + 4 * wave * (8 / NW));
+    // Row scales of the chunk's 128-class group for the 128 rows: 32 / NW pieces per wave.
+    const float* gs = gscale + (jb / kLogitGroup) * ld_g + n0;
+    if (lane < 32 / NW) dma16(gs + 4 * (wave * (32 / NW) + lane), dx_s<S>() + 4 * wave * (32 / NW));
   };
   // Active-set indices of the W rows this wave DMAs for a chunk, loaded one
   // chunk ahead of their DMA (wave-uniform: scalar loads).
@@ -246,8 +231,12 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
   // Coefficients of chunk c (K-major, rows of 32 classes): the LDS reads are
   // issued first (produce_load) and consumed later (produce_store), after an
   // lgkm wait that covers them.
+  // Coefficient of (row, class): p / ||w_j|| * scale = E * gscale_row * scale * (1/||w_j||);
+  // E is 0 at the row's target and past |S|, gscale 0 past the batch, so only
+  // chunks past the split's end need masking.
   struct ProdIn {
     u32x4_t qv[GROUPS], i0v[GROUPS], i1v[GROUPS];
+    uint32_t sv[GROUPS];
   };
   auto produce_load = [&](auto st, ProdIn& in) {
     constexpr int S = decltype(st)::value;
@@ -256,36 +245,30 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
       ds_read_128<0>(in.qv[u], lds_addr(dx_r<S>()) + (prow[u] * kBwKC + 8 * pchunk[u]) * 2);
       ds_read_128<0>(in.i0v[u], lds_addr(dx_i<S>()) + 32 * pchunk[u]);
       ds_read_128<16>(in.i1v[u], lds_addr(dx_i<S>()) + 32 * pchunk[u]);
+      ds_read_32<0>(in.sv[u], lds_addr(dx_s<S>()) + 4 * prow[u]);
     }
   };
   auto produce_store = [&](auto st, int64_t c, ProdIn& in) {
     constexpr int S = decltype(st)::value;
-    const int64_t jb = c * kBwKC;
-    const bool cvalid = c < c_end;
-    const bool chunk_full = cvalid && jb + kBwKC <= K;   // wave-uniform
+    const bool cvalid = c < c_end;   // wave-uniform
 #pragma unroll
     for (int u = 0; u < GROUPS; ++u) {
       pin_reg(in.qv[u]);
       pin_reg(in.i0v[u]);
       pin_reg(in.i1v[u]);
-      const int64_t jg = jb + 8 * pchunk[u];
-      const int tpos = pyh[u] - (int)jg;  // the row's target, if it is one of these 8 classes
+      pin_reg(in.sv[u]);
       const uint4 q = as_uint4(in.qv[u]);
+      const uint32_t qw[4] = {q.x, q.y, q.z, q.w};
       const float iw[8] = {__uint_as_float(in.i0v[u].x), __uint_as_float(in.i0v[u].y),
                            __uint_as_float(in.i0v[u].z), __uint_as_float(in.i0v[u].w),
                            __uint_as_float(in.i1v[u].x), __uint_as_float(in.i1v[u].y),
                            __uint_as_float(in.i1v[u].z), __uint_as_float(in.i1v[u].w)};
+      const float sc = cvalid ? __uint_as_float(in.sv[u]) * scale : 0.0f;
       float v[8];
-      if (chunk_full && !__any((unsigned)tpos < 8u)) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = p_of((int16_t)u16_at(q, e), s2q, plse2[u]) * iw[e];
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const bool keep = cvalid && tpos != e && jg + e < K;
-          const float pe = p_of((int16_t)u16_at(q, e), s2q, plse2[u]) * iw[e];
-          v[e] = keep ? pe : 0.0f;
-        }
+      for (int e = 0; e < 8; ++e) {
+        const float ev = (e & 1) ? f16_hi(qw[e >> 1]) : f16_lo(qw[e >> 1]);
+        v[e] = ev * (sc * iw[e]);
       }
       const uint4 o = pack8<Tag>(v);
       ds_write_128<0>(lds_addr(dx_g<S>()) + k_major32_offset(prow[u], pchunk[u]) * 2,
@@ -400,19 +383,34 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
   }
 }
 
+// Row scales of the logit store: gscale[g][n] = 2^(m_gn - lse_n log2 e), so that
+// E * gscale is the softmax probability (0 for rows past the batch).  Groups
+// past |S| are never read and are skipped.
+__global__ void __launch_bounds__(256) k_scales(const float* __restrict__ gmax,
+                                                const float* __restrict__ row_lse, int B,
+                                                int64_t ld_g, int64_t n_groups,
+                                                const int32_t* __restrict__ n_active_p,
+                                                float* __restrict__ gscale) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_groups * ld_g) return;
+  const int64_t g = i / ld_g;
+  const int n = (int)(i - g * ld_g);
+  if (g * kLogitGroup >= (int64_t)*n_active_p) return;
+  float v = 0.0f;
+  if (n < B) v = __builtin_amdgcn_exp2f(gmax[i] - row_lse[n] * kLog2e);
+  gscale[i] = v;
+}
+
 // Sum the split partials of a row in split order, add the row's target term
 // g_t * W[S_t] / ||w_t||, and apply the normalisation backward:
 // dx = (dX_hat - x_hat (x_hat . dX_hat)) / ||x||, dX_hat = (s/B) * sum.
-// Also writes the row record (lse log2 e - log2(1/||x||), label) the dW kernel
-// reads: its coefficient p / ||x|| is then a single power of two.
 template <typename Tag>
 __global__ void __launch_bounds__(256) k_dx_final(
     const float* __restrict__ dx_part, int n_split, const void* __restrict__ X,
     const void* __restrict__ W, const int32_t* __restrict__ active,
     const int32_t* __restrict__ yhat, const float* __restrict__ row_lse,
     const float* __restrict__ inv_x, const float* __restrict__ inv_w,
-    const int16_t* __restrict__ cosq, int64_t ld_cos, int B, int d, Margin mg, float sB,
-    float* __restrict__ dX, float2* __restrict__ row_rec) {
+    const float* __restrict__ tgtc, int B, int d, Margin mg, float sB, float* __restrict__ dX) {
   constexpr int kMaxPer = 8;  // d <= 512
   const int lane = threadIdx.x & 63;
   const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -420,11 +418,10 @@ __global__ void __launch_bounds__(256) k_dx_final(
   const float ix = inv_x[n];
   const int yt = yhat[n];
   const float lse = row_lse[n];
-  if (lane == 0) row_rec[n] = make_float2(lse * kLog2e - log2f(ix), __int_as_float(yt));
   float gt = 0.0f;
   int64_t wbase = 0;
   if (yt >= 0) {
-    gt = target_coef(mg, cosq[(int64_t)n * ld_cos + yt], lse) * inv_w[yt];
+    gt = target_coef(mg, tgtc[n], lse) * inv_w[yt];
     wbase = (int64_t)active[yt] * d;
   }
   float v[kMaxPer], xh[kMaxPer];
@@ -467,14 +464,15 @@ __global__ void __launch_bounds__(128 * WI) k_dw16(
     const int32_t* __restrict__ active, const int32_t* __restrict__ n_active_p,
     const int32_t* __restrict__ yhat, const float* __restrict__ row_lse,
     const float* __restrict__ inv_x, const float* __restrict__ inv_w,
-    const float2* __restrict__ row_rec, const int16_t* __restrict__ cosq, int64_t ld_cos, int B,
-    Margin mg, float sB, float lr, float mu) {
+    const float* __restrict__ tgtc, const uint16_t* __restrict__ lbuf, int64_t ld_cos,
+    const float* __restrict__ gscale, int64_t ld_g, int B, Margin mg, float sB, float lr,
+    float mu) {
   constexpr int D = 128 * WI;
   constexpr int NT = 128 * WI;
   constexpr int NW = 2 * WI;
   constexpr int XDMA = D / 16 / NW;     // X^T loads (16 d rows each) per wave per chunk
-  constexpr int RDMA = 8 / NW;          // raw-cosine loads (4 rows each) per wave
-  constexpr int QL = 16 / NW;           // record pieces (2 rows each) per wave
+  constexpr int RDMA = 8 / NW;          // logit-store loads (4 rows each) per wave
+  constexpr int QL = 8 / NW;            // row-scale pieces (4 rows each) per wave
   constexpr int GROUPS = 512 / NT;      // producer slots per thread
   constexpr int PER_ITER = XDMA + RDMA + 1;
   static_assert(XDMA == 4, "X^T loads per wave");
@@ -486,10 +484,10 @@ __global__ void __launch_bounds__(128 * WI) k_dw16(
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wi = wave >> 1, wj = wave & 1;
   const int half = lane >> 5, l32 = lane & 31;
-  const float s2q = mg.s * kLog2e * kCosDequant;
   const int n_chunks = (int)ceil_div(B, kBwKC);
   const int c_stop = (int)ceil_div(n_chunks, 3) * 3;
-  const bool tile_full = j0 + kDwCls <= (int64_t)K;   // every class of the tile in S
+  // The tile is one 128-class group of the logit store: its row scales.
+  const float* gsc = gscale + (j0 / kLogitGroup) * ld_g;
 
   // Producer slots: a 16-lane group owns 16 classes x 8 batch rows of a chunk;
   // lane gi of the group owns class 16 cb + gi.
@@ -522,10 +520,10 @@ __global__ void __launch_bounds__(128 * WI) k_dw16(
       int n = cc * kBwKC + r;
       n = n < B ? n : B - 1;
       const int piece = (lane & 15) ^ (2 * (r & 3));
-      dma16(cosq + (int64_t)n * ld_cos + j0 + 8 * piece, dw_r<S>() + 512 * blk);
+      dma16(lbuf + (int64_t)n * ld_cos + j0 + 8 * piece, dw_r<S>() + 512 * blk);
     }
-    // Row records: QL 16-byte pieces (2 rows each) per wave; rows < ld_xt always.
-    if (lane < QL) dma16(row_rec + cc * kBwKC + 2 * (QL * wave + lane), dw_q<S>() + 2 * QL * wave);
+    // Row scales of the chunk: QL 16-byte pieces (4 rows each) per wave; rows < ld_g always.
+    if (lane < QL) dma16(gsc + cc * kBwKC + 4 * (QL * wave + lane), dw_q<S>() + 4 * QL * wave);
   };
   // X^T: block cc of the transposed batch ([d][32], contiguous); load v of this
   // wave covers d rows 16 m .. 16 m + 15 (m = wave XDMA + v), 4 pieces each;
@@ -542,13 +540,13 @@ __global__ void __launch_bounds__(128 * WI) k_dw16(
       dma16(xbT + ((int64_t)cc * D + i) * kBwKC + 8 * piece, dw_x<S>() + 512 * m);
     }
   };
-  // Coefficients of chunk c: G^T[class][row] = p / ||x_row|| for the non-target
-  // entries (zero at targets, classes past |S| and rows past the batch).  The
-  // LDS reads are issued first (produce_load) and consumed later
-  // (produce_store), after an lgkm wait that covers them.
+  // Coefficients of chunk c: G^T[class][row] = p = E * gscale_row (the operand
+  // X^T holds x_hat, so no 1/||x|| here).  E is 0 at targets and past |S|,
+  // gscale 0 past the batch.  The LDS reads are issued first (produce_load)
+  // and consumed later (produce_store), after an lgkm wait that covers them.
   struct ProdIn {
     u32x2_t qlo[GROUPS], qhi[GROUPS];
-    u32x4_t rq[GROUPS][4];
+    u32x4_t sq[GROUPS][2];
   };
   auto produce_load = [&](auto st, ProdIn& in) {
     constexpr int S = decltype(st)::value;
@@ -557,49 +555,29 @@ __global__ void __launch_bounds__(128 * WI) k_dw16(
       const uint32_t ra = lds_addr(dw_r<S>()) + ptr_off[u];
       ds_read_tr_b64<0>(in.qlo[u], ra);
       ds_read_tr_b64<4 * kDwCls * 2>(in.qhi[u], ra);
-      const uint32_t qa = lds_addr(dw_q<S>()) + 64 * prg[u];
-      ds_read_128<0>(in.rq[u][0], qa);
-      ds_read_128<16>(in.rq[u][1], qa);
-      ds_read_128<32>(in.rq[u][2], qa);
-      ds_read_128<48>(in.rq[u][3], qa);
+      const uint32_t qa = lds_addr(dw_q<S>()) + 32 * prg[u];
+      ds_read_128<0>(in.sq[u][0], qa);
+      ds_read_128<16>(in.sq[u][1], qa);
     }
   };
-  constexpr int kProdReads = 6 * GROUPS;   // LDS reads of produce_load
   auto produce_store = [&](auto st, ProdIn& in) {
     constexpr int S = decltype(st)::value;
 #pragma unroll
     for (int u = 0; u < GROUPS; ++u) {
       pin_reg(in.qlo[u]);
       pin_reg(in.qhi[u]);
-      pin_reg(in.rq[u][0]);
-      pin_reg(in.rq[u][1]);
-      pin_reg(in.rq[u][2]);
-      pin_reg(in.rq[u][3]);
-      const int jc = (int)j0 + pcls[u];   // the class's position in S
+      pin_reg(in.sq[u][0]);
+      pin_reg(in.sq[u][1]);
       const uint32_t qw[4] = {in.qlo[u].x, in.qlo[u].y, in.qhi[u].x, in.qhi[u].y};
-      float off[8];
-      int lab[8];
-#pragma unroll
-      for (int e2 = 0; e2 < 4; ++e2) {
-        off[2 * e2] = __uint_as_float(in.rq[u][e2].x);
-        lab[2 * e2] = (int)in.rq[u][e2].y;
-        off[2 * e2 + 1] = __uint_as_float(in.rq[u][e2].z);
-        lab[2 * e2 + 1] = (int)in.rq[u][e2].w;
-      }
-      bool has_t = false;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) has_t |= lab[e] == jc;
+      const float sc[8] = {__uint_as_float(in.sq[u][0].x), __uint_as_float(in.sq[u][0].y),
+                           __uint_as_float(in.sq[u][0].z), __uint_as_float(in.sq[u][0].w),
+                           __uint_as_float(in.sq[u][1].x), __uint_as_float(in.sq[u][1].y),
+                           __uint_as_float(in.sq[u][1].z), __uint_as_float(in.sq[u][1].w)};
       float v[8];
-      if (tile_full && !__any(has_t)) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-          v[e] = p_of((int16_t)(qw[e >> 1] >> (16 * (e & 1))), s2q, off[e]);
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float pe = p_of((int16_t)(qw[e >> 1] >> (16 * (e & 1))), s2q, off[e]);
-          v[e] = (lab[e] != jc && jc < K) ? pe : 0.0f;
-        }
+      for (int e = 0; e < 8; ++e) {
+        const float ev = (e & 1) ? f16_hi(qw[e >> 1]) : f16_lo(qw[e >> 1]);
+        v[e] = ev * sc[e];
       }
       const uint4 o = pack8<Bf16Tag>(v);
       const int cl = pcls[u];
@@ -703,7 +681,7 @@ __global__ void __launch_bounds__(128 * WI) k_dw16(
       mask &= mask - 1;
       const int nn = nbase + bit;
       const int yt = __shfl(yv, bit, 64);
-      const float gt = target_coef(mg, cosq[(int64_t)nn * ld_cos + yt], row_lse[nn]) * inv_x[nn];
+      const float gt = target_coef(mg, tgtc[nn], row_lse[nn]) * inv_x[nn];
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb) {
         if (jw + 32 * nb + l32 != yt) continue;
@@ -960,22 +938,25 @@ void launch_bwd16(const StepArgs& a, const StepWs& w, const Margin& mg, float sB
   const int64_t n_tiles = (int64_t)n_rt * w.n_split;
   const int64_t per_xcd = ceil_div(n_tiles, 8);
   timing_start(4, stream);
+  // Row scales of the logit store from the lse the gradient is normalised with.
+  hipLaunchKernelGGL(k_scales, dim3((unsigned)ceil_div(w.n_groups * w.ld_g, 256)), dim3(256), 0,
+                     stream, w.gmax, a.row_lse, B, w.ld_g, w.n_groups, a.n_active, w.gscale);
   hipLaunchKernelGGL((k_dx16<Tag, WI>), dim3((unsigned)(8 * per_xcd)), dim3(128 * WI), 0, stream,
-                     (const uint16_t*)a.W, a.active, a.n_active, a.labels_mapped, a.row_lse,
-                     w.inv_w, w.inv_w_max, (const int16_t*)w.cosq, w.ld_cos, B, n_rt, w.n_split,
-                     n_tiles, per_xcd, a.s, w.dx_part);
+                     (const uint16_t*)a.W, a.active, a.n_active, w.inv_w, w.inv_w_max,
+                     (const uint16_t*)w.lbuf, w.ld_cos, w.gscale, w.ld_g, B, n_rt, w.n_split,
+                     n_tiles, per_xcd, w.dx_part);
   timing_stop(4, stream);
   timing_start(5, stream);
   hipLaunchKernelGGL(k_dx_final<Tag>, dim3((unsigned)ceil_div(B, 4)), dim3(256), 0, stream,
                      w.dx_part, w.n_split, a.X, a.W, a.active, a.labels_mapped, a.row_lse,
-                     w.inv_x, w.inv_w, (const int16_t*)w.cosq, w.ld_cos, B, (int)a.d, mg, sB,
-                     a.dX, w.row_rec);
+                     w.inv_x, w.inv_w, w.tgtc, B, (int)a.d, mg, sB, a.dX);
   timing_stop(5, stream);
   timing_start(6, stream);
   hipLaunchKernelGGL((k_dw16<Tag, WI>), dim3((unsigned)ceil_div(a.cap, kDwCls)), dim3(128 * WI),
                      0, stream, (const uint16_t*)w.xbT, w.ld_xt, a.X, (uint16_t*)a.W, a.W_master, a.M,
                      a.active, a.n_active, a.labels_mapped, a.row_lse, w.inv_x, w.inv_w,
-                     w.row_rec, (const int16_t*)w.cosq, w.ld_cos, B, mg, sB, a.lr, a.mu);
+                     w.tgtc, (const uint16_t*)w.lbuf, w.ld_cos, w.gscale, w.ld_g, B, mg, sB, a.lr,
+                     a.mu);
   timing_stop(6, stream);
 }
 
@@ -999,7 +980,7 @@ hipError_t launch_backward(const StepArgs& a, const StepWs& w, hipStream_t strea
     timing_start(4, stream);
     hipLaunchKernelGGL(k_dx32, dim3((unsigned)ceil_div(d, 256), (unsigned)B), dim3(256), 0,
                        stream, (const float*)a.W, a.active, a.n_active, a.labels_mapped,
-                       a.row_lse, w.inv_w, (const float*)w.cosq, w.ld_cos, B, d, mg, w.dx_part);
+                       a.row_lse, w.inv_w, (const float*)w.lbuf, w.ld_cos, B, d, mg, w.dx_part);
     timing_stop(4, stream);
     timing_start(5, stream);
     hipLaunchKernelGGL(k_dx_final32, dim3((unsigned)ceil_div(B, 4)), dim3(256), 0, stream,
@@ -1008,7 +989,7 @@ hipError_t launch_backward(const StepArgs& a, const StepWs& w, hipStream_t strea
     timing_start(6, stream);
     hipLaunchKernelGGL(k_dw32, dim3((unsigned)a.cap), dim3(256), 0, stream, (const float*)a.X,
                        (float*)a.W, a.W_master, a.M, a.active, a.n_active, a.labels_mapped,
-                       a.row_lse, w.inv_x, w.inv_w, (const float*)w.cosq, w.ld_cos, B, d, mg, sB,
+                       a.row_lse, w.inv_x, w.inv_w, (const float*)w.lbuf, w.ld_cos, B, d, mg, sB,
                        a.lr, a.mu);
     timing_stop(6, stream);
   } else if (a.dtype == 1) {

@@ -80,7 +80,6 @@ __device__ __forceinline__ void fwd_issue(const uint16_t* const ap[4], const uin
 }
 
 // a0^2 + a1^2 + acc for a packed pair of 16-bit values (v_dot2_f32_*).
-typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ float sumsq2(uint32_t v, float acc, F16Tag) {
   const f16x2_t h = __builtin_bit_cast(f16x2_t, v);
@@ -144,17 +143,18 @@ __device__ __forceinline__ void fwd_compute(f32x16_t (&acc)[4][2], int wm, int w
 
 // Epilogue of one lane for one 32-row block (nb): the lane's row n and its
 // 64 classes j = jb + 32 mb + 8 g + e (jb = first class of the lane's
-// pattern, e < 4).  Writes the quantised cosines to the LDS tile row trow
-// (16-byte block b of the row at position b ^ bsw), leaves the base-2 logits
-// in acc, and returns the lane pair's (max, sum 2^(f - max)) over the
-// wave's 128 classes.  CHECK_J masks classes past |S|; CHECK_T handles a
-// target column in the lane's pattern (tpos = y - jb).
+// pattern, e < 4); with the partner lane (half ^ 1) they are the row's 128
+// classes of one group.  Computes the base-2 logits f2 = s c log2 e (-inf at
+// the target, whose margined logit is merged separately, and past |S|), the
+// group maximum m (the target's margined logit included), and writes
+// E = 2^(f2 - m) as fp16 to the LDS tile row trow (16-byte block b of the row
+// at position b ^ bsw).  Returns the pair's (m, sum of E and the target term).
 template <bool CHECK_J, bool CHECK_T>
 __device__ __forceinline__ void fwd_epilogue_rows(f32x16_t (&acc)[4][2], int nb, float ix,
                                                   const float* iwp, int K, int64_t jb, int tpos,
                                                   const Margin& mg, uint16_t* trow, int bbase,
                                                   int bsw, int half, float* mx_out, float* sm_out,
-                                                  float* tgt_out) {
+                                                  float* tgt_out, float* tgtc_out) {
   const float s2 = mg.s * kLog2e;
   float mx = -INFINITY;
   float ct = 0.0f;
@@ -165,12 +165,9 @@ __device__ __forceinline__ void fwd_epilogue_rows(f32x16_t (&acc)[4][2], int nb,
       const int o = 32 * mb + 8 * g;
       const float4 iw4 = *reinterpret_cast<const float4*>(iwp + o);
       const float iwv[4] = {iw4.x, iw4.y, iw4.z, iw4.w};
-      float cv[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        float c = acc[mb][nb][4 * g + e] * ix * iwv[e];
-        if (CHECK_J && jb + o + e >= K) c = 0.0f;
-        cv[e] = c;
+        const float c = acc[mb][nb][4 * g + e] * ix * iwv[e];
         float f2 = c * s2;
         if (CHECK_J && jb + o + e >= K) f2 = -INFINITY;
         if (CHECK_T && tpos == o + e) {
@@ -180,32 +177,38 @@ __device__ __forceinline__ void fwd_epilogue_rows(f32x16_t (&acc)[4][2], int nb,
         acc[mb][nb][4 * g + e] = f2;
         mx = fmaxf(mx, f2);
       }
-      {
-        const auto q01 = __builtin_amdgcn_cvt_pknorm_i16(cv[0], cv[1]);
-        const auto q23 = __builtin_amdgcn_cvt_pknorm_i16(cv[2], cv[3]);
-        uint2 packed;
-        __builtin_memcpy(&packed.x, &q01, 4);
-        __builtin_memcpy(&packed.y, &q23, 4);
-        *reinterpret_cast<uint2*>(trow + 8 * ((bbase + o / 8) ^ bsw) + 4 * half) = packed;
-      }
     }
   }
   float ft2 = -INFINITY;
   if (CHECK_T && tgt_out) {
     const float ft = target_logit(mg, ct);
     *tgt_out = ft;
+    *tgtc_out = ct;
     ft2 = ft * kLog2e;
     mx = fmaxf(mx, ft2);
   }
   mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  // A group with no live logit keeps reference 0 (all its E are 0).
+  const float mref = mx == -INFINITY ? 0.0f : mx;
   float sm = 0.0f;
-  if (mx != -INFINITY) {
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb)
+  for (int mb = 0; mb < 4; ++mb) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sm += __builtin_amdgcn_exp2f(acc[mb][nb][r] - mx);
-    if (CHECK_T && tgt_out) sm += __builtin_amdgcn_exp2f(ft2 - mx);
+    for (int g = 0; g < 4; ++g) {
+      const int o = 32 * mb + 8 * g;
+      float ev[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        ev[e] = __builtin_amdgcn_exp2f(acc[mb][nb][4 * g + e] - mref);
+        sm += ev[e];
+      }
+      uint2 packed;
+      packed.x = pack_f16x2(ev[0], ev[1]);
+      packed.y = pack_f16x2(ev[2], ev[3]);
+      *reinterpret_cast<uint2*>(trow + 8 * ((bbase + o / 8) ^ bsw) + 4 * half) = packed;
+    }
   }
+  if (CHECK_T && tgt_out) sm += __builtin_amdgcn_exp2f(ft2 - mref);
   sm += __shfl_xor(sm, 32, 64);
   *mx_out = mx;
   *sm_out = sm;
@@ -223,7 +226,8 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
     const int32_t* __restrict__ yhat, const float* __restrict__ inv_x,
     float* __restrict__ inv_w, float* __restrict__ inv_w_max, int B, int64_t ld_cos,
     int64_t n_ctiles, int n_rt, int64_t n_tiles, int64_t per_xcd, Margin mg,
-    int16_t* __restrict__ cosq, float2* __restrict__ stats, float* __restrict__ tgt) {
+    uint16_t* __restrict__ lbuf, float2* __restrict__ stats, float* __restrict__ tgt,
+    float* __restrict__ tgtc, float* __restrict__ gmax, int64_t ld_g) {
   constexpr int D = NK * kFwdKC;
   // All batch-row tiles of a class tile run on one XCD: the gathered W rows
   // come from HBM once and are re-read from that XCD's L2.
@@ -308,7 +312,7 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
     fIw[tid] = inv;
     if (rt == 0) {
       const bool jok = j0 + tid < (int64_t)K;
-      if (jok) inv_w[j0 + tid] = inv;
+      inv_w[j0 + tid] = jok ? inv : 0.0f;
       const float m = wave_max(jok ? inv : 0.0f);
       if (lane == 0) atomicMax(reinterpret_cast<int*>(inv_w_max), __float_as_int(m));
     }
@@ -334,11 +338,16 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
     float mx, sm;
     if (full && !__any(has_t))
       fwd_epilogue_rows<false, false>(acc, nb, ixr[nb], iwp, K, jlo + 4 * half, tpos, mg, trow,
-                                      16 * wm, nl & 15, half, &mx, &sm, nullptr);
+                                      16 * wm, nl & 15, half, &mx, &sm, nullptr, nullptr);
     else
       fwd_epilogue_rows<true, true>(acc, nb, ixr[nb], iwp, K, jlo + 4 * half, tpos, mg, trow,
-                                    16 * wm, nl & 15, half, &mx, &sm, has_t ? tgt + n : nullptr);
-    if (half == 0) fRed[wm][nl] = make_float2(mx, sm);
+                                    16 * wm, nl & 15, half, &mx, &sm, has_t ? tgt + n : nullptr,
+                                    has_t ? tgtc + n : nullptr);
+    if (half == 0) {
+      fRed[wm][nl] = make_float2(mx, sm);
+      // reference of the row's 128-class group 2 ct + wm
+      if (n < B) gmax[(2 * ct + wm) * ld_g + n] = mx == -INFINITY ? 0.0f : mx;
+    }
   }
   wait_lgkm0();
   stage_barrier();
@@ -350,7 +359,7 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
       const int r = 32 * wave + 2 * i + (lane >> 5);
       const int n = n0 + r;
       const uint4 v = *reinterpret_cast<const uint4*>(fwd_tile_row(r) + 8 * (b ^ (r & 15)));
-      if (n < B) *reinterpret_cast<uint4*>(cosq + (int64_t)n * ld_cos + j0 + 8 * b) = v;
+      if (n < B) *reinterpret_cast<uint4*>(lbuf + (int64_t)n * ld_cos + j0 + 8 * b) = v;
     }
   }
   if (tid < kFwdBN) {
@@ -461,7 +470,8 @@ void launch_fwd16_nk(unsigned grid, hipStream_t stream, const StepArgs& a, const
   hipLaunchKernelGGL((k_fwd16<Tag, NK>), dim3(grid), dim3(kFwdThreads), 0, stream,
                      (const uint16_t*)a.X, (const uint16_t*)a.W, a.active, a.n_active,
                      a.labels_mapped, w.inv_x, w.inv_w, w.inv_w_max, B, w.ld_cos, w.n_ctiles,
-                     n_rt, n_tiles, per_xcd, mg, (int16_t*)w.cosq, w.stats, w.tgt);
+                     n_rt, n_tiles, per_xcd, mg, (uint16_t*)w.lbuf, w.stats, w.tgt, w.tgtc,
+                     w.gmax, w.ld_g);
 }
 
 template <typename Tag>
@@ -486,11 +496,11 @@ hipError_t launch_forward(const StepArgs& a, const StepWs& w, hipStream_t stream
     timing_start(2, stream);
     hipLaunchKernelGGL(k_fwd32, grid, dim3(256), 0, stream, (const float*)a.X,
                        (const float*)a.W, a.active, a.n_active, w.inv_x, w.inv_w, B, d, a.cap,
-                       w.ld_cos, (float*)w.cosq);
+                       w.ld_cos, (float*)w.lbuf);
     timing_stop(2, stream);
     timing_start(3, stream);
     hipLaunchKernelGGL(k_lse32, dim3((unsigned)ceil_div(B, 4)), dim3(256), 0, stream,
-                       (const float*)w.cosq, w.ld_cos, a.n_active, a.labels_mapped, B, mg,
+                       (const float*)w.lbuf, w.ld_cos, a.n_active, a.labels_mapped, B, mg,
                        a.row_lse_out, w.loss_part);
   } else {
     const int n_rt = (int)ceil_div(B, kFwdBN);

@@ -1,5 +1,5 @@
-// Device helpers of the step kernels: 16-bit conversions, MFMA wrappers,
-// cosine quantisation and the target-margin formulas.
+// Device helpers of the step kernels: 16-bit conversions, MFMA wrappers and
+// the target-margin formulas.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -56,6 +56,19 @@ __device__ __forceinline__ uint16_t from_float<Bf16Tag>(float f) { return float_
 template <>
 __device__ __forceinline__ uint16_t from_float<F16Tag>(float f) { return float_to_f16(f); }
 
+// Two floats to a packed pair of fp16 values, round to nearest even.
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
+  const f16x2_t v = {(_Float16)a, (_Float16)b};
+  return __builtin_bit_cast(uint32_t, v);
+}
+__device__ __forceinline__ float f16_lo(uint32_t v) {
+  return (float)__builtin_bit_cast(f16x2_t, v).x;
+}
+__device__ __forceinline__ float f16_hi(uint32_t v) {
+  return (float)__builtin_bit_cast(f16x2_t, v).y;
+}
+
 // D(32x32, fp32) += A(32x16) * B(16x32).  Lane l supplies A[l%32][8(l/32)..+7]
 // and B[8(l/32)..+7][l%32]; accumulator register r of lane l is
 // D[8(r/4) + 4(l/32) + r%4][l%32].
@@ -73,10 +86,6 @@ __device__ __forceinline__ f32x16_t mfma_32x32x16(const uint4& a, const uint4& b
   __builtin_memcpy(&bv, &b, 16);
   return __builtin_amdgcn_mfma_f32_32x32x16_f16(av, bv, c, 0, 0, 0);
 }
-
-// 16-bit fixed-point cosine: q = round-to-nearest-even(clamp(c, -1, 1) * 32767)
-// (v_cvt_pknorm_i16_f32 in the forward), c ~ q / 32767.
-__device__ __forceinline__ float dequantise_cos(int16_t q) { return (float)q * kCosDequant; }
 
 // Target logit and its slope d f / d cos (divided by s).  CosFace:
 // s (c - m), slope 1.  ArcFace: s cos(acos(c) + m) = s (c cos m - sin(theta) sin m),

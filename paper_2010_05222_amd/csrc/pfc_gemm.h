@@ -74,6 +74,10 @@ __device__ __forceinline__ void ds_read_128(u32x4_t& dst, uint32_t addr) {
 }
 
 template <int OFF>
+__device__ __forceinline__ void ds_read_32(uint32_t& dst, uint32_t addr) {
+  asm volatile("ds_read_b32 %0, %1 offset:%2" : "=v"(dst) : "v"(addr), "i"(OFF));
+}
+template <int OFF>
 __device__ __forceinline__ void ds_write_128(uint32_t addr, const u32x4_t& v) {
   asm volatile("ds_write_b128 %0, %1 offset:%2" ::"v"(addr), "v"(v), "i"(OFF) : "memory");
 }

@@ -42,30 +42,34 @@ struct SampleWs {
 
 // ----------------------------------------------------------------- step
 
-// Quantised cosine store of the 16-bit paths: q = round(clamp(cos, -1, 1) * 32767),
-// cos ~ q / 32767 (absolute error <= 1.6e-5).
-constexpr float kCosQuant = 32767.0f;
-constexpr float kCosDequant = 1.0f / 32767.0f;
 // Class tile of the forward contraction (one softmax-statistics pair per row and tile).
 constexpr int kFwdClassTile = 256;
+// Class group of the logit store: the forward keeps one base-2 reference per
+// (row, group of 128 active classes).
+constexpr int kLogitGroup = 128;
 
 struct StepWs {
   float* inv_x;          // [B]      1/max(||x_n||, eps)
-  void* xbT;             // [ld_xt / 32][d][32] X transposed in blocks of 32 rows, bf16, zero
-                         // past B (the class-gradient operand)
+  void* xbT;             // [ld_xt / 32][d][32] x_hat (normalised rows) transposed in blocks of
+                         // 32 rows, bf16, zero past B (the class-gradient operand)
   int64_t ld_xt;         // B rounded up to 32
   float* inv_w_max;      // [1] max_j 1/||W[S_j]|| (scale of the fp16 feature-gradient operand)
-  float* inv_w;          // [ld_cos] 1/max(||W[S_j]||, eps)
-  void* cosq;            // [B x ld_cos] quantised cosines (int16) or fp32 cosines
-  int64_t ld_cos;        // row stride of cosq: cap rounded up to 256
+  float* inv_w;          // [ld_cos] 1/max(||W[S_j]||, eps), 0 past |S| within the last tile
+  void* lbuf;            // [B x ld_cos] logit store.  16-bit paths: fp16 E = 2^(f log2 e - m)
+                         // with m the row's reference for the class's 128-class group (E = 0
+                         // at the target and past |S|); fp32 path: fp32 cosines
+  int64_t ld_cos;        // row stride of lbuf: cap rounded up to 256
   float2* stats;         // [B x n_ctiles] per class tile: (max, sum 2^(f log2 e - max)), base 2
   int64_t n_ctiles;      // class tiles of the forward contraction
   float* tgt;            // [B] margined target logit
+  float* tgtc;           // [B] unmargined target cosine
+  float* gmax;           // [n_groups x ld_g] reference m of each (group, row)
+  float* gscale;         // [n_groups x ld_g] 2^(m - lse log2 e), so p = E * gscale (0 past B)
+  int64_t ld_g;          // B rounded up to 128
+  int64_t n_groups;      // ld_cos / 128
   float* dx_part;        // [n_split x B x d] split-K partial sums of dX_hat
   int n_split;
   float* loss_part;      // [B] per-row loss terms
-  float2* row_rec;       // [ld_xt] (lse log2 e - log2(1/||x||), label bits) for the class-gradient
-                         // kernel; rows past B hold (+inf, -1)
 };
 
 // Layout of the whole workspace (offsets in bytes from its base).
@@ -74,9 +78,9 @@ struct WsLayout {
   size_t sample_bytes;   // prefix used by the sampler
   size_t off_bitmap, off_hist, off_state, off_keys, off_cand;
   size_t off_grp_sure, off_grp_tie, off_grp_out, off_grp_tie_off;
-  size_t off_inv_x, off_xb, off_wmax, off_inv_w, off_cos, off_stats, off_tgt, off_dx, off_loss,
-      off_rec;
-  int64_t ld_cos, n_ctiles, n_groups, ld_xt;
+  size_t off_inv_x, off_xb, off_wmax, off_inv_w, off_cos, off_stats, off_tgt, off_tgtc,
+      off_gmax, off_gscale, off_dx, off_loss;
+  int64_t ld_cos, n_ctiles, n_groups, ld_xt, ld_g, n_lgroups;
   int n_split;
   int top_bits;
 };

@@ -27,18 +27,16 @@ __device__ __forceinline__ float sumsq8(const uint4& v) {
   return acc;
 }
 
-// inv_x[n] and a transposed bf16 copy of the batch in blocks of 32 rows
-// (block c = [d][32]: entry (i, r) = X[32 c + r][i]), the K-major operand of
-// the class-gradient contraction; a workgroup transposes one block through
-// LDS.  Rows n in [B, ld_xt) are zero and their row records (+inf, -1), so
-// the padded rows drop out of that contraction.  Also clears the running
-// max of 1/||w_j||.
+// inv_x[n] and a transposed bf16 copy of the normalised batch x_hat in blocks
+// of 32 rows (block c = [d][32]: entry (i, r) = x_hat[32 c + r][i]), the
+// K-major operand of the class-gradient contraction; a workgroup transposes
+// one block through LDS.  Rows n in [B, ld_xt) are zero.  Also clears the
+// running max of 1/||w_j||.
 constexpr int kPrepRows = 32;
 template <typename Tag>
 __global__ void __launch_bounds__(256) k_prep_x16(const uint16_t* __restrict__ X, int B, int d,
                                                   int64_t ld_xt, float* __restrict__ inv_x,
                                                   uint16_t* __restrict__ xbT,
-                                                  float2* __restrict__ row_rec,
                                                   float* __restrict__ inv_w_max) {
   __shared__ uint16_t tile[kPrepRows][512 + 8];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -46,24 +44,20 @@ __global__ void __launch_bounds__(256) k_prep_x16(const uint16_t* __restrict__ X
   if (blockIdx.x == 0 && threadIdx.x == 0) *inv_w_max = 0.0f;
   for (int r = wave; r < kPrepRows; r += 4) {
     const int n = n0 + r;
-    float ss = 0.0f;
-    for (int c = lane; c < d / 8; c += 64) {
-      uint4 ov = make_uint4(0, 0, 0, 0);
-      if (n < B) {
-        const uint4 v = *reinterpret_cast<const uint4*>(X + (int64_t)n * d + 8 * c);
-        ss += sumsq8<Tag>(v);
-        const uint16_t* h = reinterpret_cast<const uint16_t*>(&v);
-        uint16_t o[8];
+    const bool c_ok = lane < d / 8;   // d <= 512: one 16-byte piece per lane
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (n < B && c_ok) v = *reinterpret_cast<const uint4*>(X + (int64_t)n * d + 8 * lane);
+    const float ss = wave_sum(sumsq8<Tag>(v));
+    const float ix = 1.0f / fmaxf(sqrtf(ss), kEpsNorm);
+    if (lane == 0 && n < B) inv_x[n] = ix;
+    if (c_ok) {
+      const uint16_t* h = reinterpret_cast<const uint16_t*>(&v);
+      uint16_t o[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) o[e] = float_to_bf16(to_float<Tag>(h[e]));
-        __builtin_memcpy(&ov, o, 16);
-      }
-      *reinterpret_cast<uint4*>(&tile[r][8 * c]) = ov;
-    }
-    ss = wave_sum(ss);
-    if (lane == 0) {
-      if (n < B) inv_x[n] = 1.0f / fmaxf(sqrtf(ss), kEpsNorm);
-      else if (n < ld_xt) row_rec[n] = make_float2(INFINITY, __int_as_float(-1));
+      for (int e = 0; e < 8; ++e) o[e] = float_to_bf16(to_float<Tag>(h[e]) * ix);
+      uint4 ov;
+      __builtin_memcpy(&ov, o, 16);
+      *reinterpret_cast<uint4*>(&tile[r][8 * lane]) = ov;
     }
   }
   __syncthreads();
@@ -125,11 +119,11 @@ hipError_t launch_prep(const StepArgs& a, const StepWs& w, hipStream_t stream) {
   } else if (a.dtype == 1) {
     hipLaunchKernelGGL(k_prep_x16<Bf16Tag>, dim3((unsigned)(w.ld_xt / kPrepRows)), dim3(256), 0,
                        stream, (const uint16_t*)a.X, B, d, w.ld_xt, w.inv_x, (uint16_t*)w.xbT,
-                       w.row_rec, w.inv_w_max);
+                       w.inv_w_max);
   } else {
     hipLaunchKernelGGL(k_prep_x16<F16Tag>, dim3((unsigned)(w.ld_xt / kPrepRows)), dim3(256), 0,
                        stream, (const uint16_t*)a.X, B, d, w.ld_xt, w.inv_x, (uint16_t*)w.xbT,
-                       w.row_rec, w.inv_w_max);
+                       w.inv_w_max);
   }
   timing_stop(1, stream);
   return hipGetLastError();
