@@ -5,9 +5,11 @@
 //
 // With dcos = (s/B) g and g_{nj} = (p_{nj} - [j = y_n]) * slope_{nj}, the
 // contractions run over the non-target part p_{nj} only (p <= 1, which keeps
-// the 16-bit operands in range), rebuilt on the fly from the forward's
-// quantised cosines and lse_n.  The single target term of each row,
-// (p_t - 1) * slope_t, is added exactly in fp32 outside the MFMA loops.
+// the 16-bit operands in range), rebuilt on the fly from the forward's logit
+// store as p = E * gscale (E = 2^(f - m) per row and 128-class group, zero at
+// targets and past |S|; gscale = 2^(m - lse log2 e) per row and group).  The
+// single target term of each row, (p_t - 1) * slope_t, is added exactly in
+// fp32 outside the MFMA loops.
 //
 // dX (k_dx16): split-K MFMA contraction over classes, dX_hat^T[i][n] =
 //   sum_j W[S_j][i] * p_{nj} / ||w_j||.  A workgroup owns 128 batch rows x all
@@ -16,11 +18,11 @@
 //   operands with transposing LDS reads, so they are never staged in
 //   registers.  k_dx_final sums the split partials in a fixed order, adds the
 //   target terms and applies the normalisation backward of x.
-// dW + update (k_dw16): a workgroup owns 128 active classes x all of d and
-//   reduces over the whole batch, so its epilogue has complete rows: target
-//   terms, tangent projection, momentum, weight step and the scatter into the
-//   persistent W / momentum rows (unique rows, no atomics).  It runs after
-//   the dX kernels, which read the old W.
+// dW + update (k_dw16): a workgroup (four waves, one per SIMD) owns 128
+//   active classes x all of d and reduces over the whole batch, so its
+//   epilogue has complete rows: target terms, tangent projection, momentum,
+//   weight step and the scatter into the persistent W / momentum rows (unique
+//   rows, no atomics).  It runs after the dX kernels, which read the old W.
 #include "pfc_gemm.h"
 
 namespace pfc {
@@ -33,14 +35,15 @@ constexpr int kRowStage = kBwKC * kRowLd;
 constexpr int kDxRows = 128;       // batch rows of a dX workgroup
 constexpr int kDwCls = 128;        // classes of a dW workgroup
 constexpr int kTLd = 260;         // LDS row stride (floats) of the update's staged gradient rows
+constexpr int kHitCap = 512;      // target rows listed per wave of a dW workgroup
 
 // Every operand reaches LDS through direct-to-LDS loads into three-stage
 // rings (one array per stage, so the compiler can keep later stages in
 // flight while a stage is read); the coefficient producer reads the raw
-// quantised cosines from LDS and writes the 16-bit MFMA operand back to LDS.
+// logit-store values from LDS and writes the 16-bit MFMA operand back to LDS.
 //
-// dX: W rows, raw cosines [128 rows x 32 classes], 1/||w|| of the chunk, and
-// the coefficient tile (K-major, 64-byte rows).
+// dX: W rows, raw logit-store values [128 rows x 32 classes], 1/||w|| of the
+// chunk, the rows' scales, and the coefficient tile (K-major, 64-byte rows).
 __shared__ __attribute__((aligned(1024))) uint16_t xW0[kRowStage], xW1[kRowStage], xW2[kRowStage];
 __shared__ __attribute__((aligned(1024))) int16_t xR0[kDxRows * kBwKC], xR1[kDxRows * kBwKC],
     xR2[kDxRows * kBwKC];
@@ -48,11 +51,11 @@ __shared__ __attribute__((aligned(16))) float xI0[kBwKC], xI1[kBwKC], xI2[kBwKC]
 __shared__ __attribute__((aligned(16))) float xS0[kDxRows], xS1[kDxRows], xS2[kDxRows];
 __shared__ __attribute__((aligned(1024))) uint16_t xG0[kDxRows * kBwKC], xG1[kDxRows * kBwKC],
     xG2[kDxRows * kBwKC];
-// dW: X^T rows (K-major: d rows of 32 batch rows, bf16), raw cosines
-// [32 rows x 128 classes] (16-byte pieces swizzled per row), per-row records
-// (lse log2 e - log2(1/||x||), label), and the coefficient tile G^T (K-major:
-// 128 class rows of 32 batch rows).  The X^T stages (33 KB) also hold the
-// update's staged gradient rows after the loop.
+// dW: X^T rows (K-major: d rows of 32 batch rows, bf16), raw logit-store
+// values [32 rows x 128 classes] (16-byte pieces swizzled per row), the rows'
+// scales, and the coefficient tile G^T (K-major: 128 class rows of 32 batch
+// rows).  After the loop the X^T stages (33 KB each) hold the update's staged
+// gradient rows, a coefficient stage the target-row lists.
 __shared__ __attribute__((aligned(1024))) uint16_t wX0[kRowStage], wX1[kRowStage], wX2[kRowStage];
 __shared__ __attribute__((aligned(1024))) int16_t wR0[kBwKC * kDwCls], wR1[kBwKC * kDwCls],
     wR2[kBwKC * kDwCls];
@@ -450,15 +453,18 @@ __global__ void __launch_bounds__(256) k_dx_final(
 
 // ------------------------------------------------------------------ dW
 
-// D = 128 * WI; 2 * WI waves: wave (wi, wj) owns d entries [128 wi, +128) and
-// classes [64 wj, +64) of the workgroup's 128.  Both MFMA operands are
-// K-major in LDS, so every fragment is one 16-byte read: X^T from the
-// transposed bf16 copy of the batch, and G^T written by the producer.
-// Pipeline per chunk c (32 batch rows): raw cosines and row records of chunk
-// c + 3 and X^T of chunk c + 2 requested, coefficients of chunk c + 1
-// produced (after the first k-step's MFMAs are issued), chunk c contracted.
+// D = 128 * WI; four waves, one per SIMD: wave w owns d entries
+// [D/4 w, +D/4) and all 128 classes of the workgroup (MB x 4 accumulator
+// tiles of 32 x 32).  Both MFMA operands are K-major in LDS, so every fragment
+// is one 16-byte read: X^T from the transposed bf16 copy of the batch, and G^T
+// written by the producer.
+// Pipeline per chunk c (32 batch rows): raw logit-store values and row
+// scales of chunk c + 3 and X^T of chunk c + 2 requested, coefficients of
+// chunk c + 1 produced, chunk c contracted.  The second k-step of chunk c is
+// contracted at the start of the next chunk, from fragments read in this
+// one, so that the matrix pipe is busy while the next fragments arrive.
 template <typename Tag, int WI>
-__global__ void __launch_bounds__(128 * WI) k_dw16(
+__global__ void __launch_bounds__(256) k_dw16(
     const uint16_t* __restrict__ xbT, int64_t ld_xt, const void* __restrict__ X,
     uint16_t* __restrict__ W, float* __restrict__ W_master, float* __restrict__ M,
     const int32_t* __restrict__ active, const int32_t* __restrict__ n_active_p,
@@ -468,21 +474,23 @@ __global__ void __launch_bounds__(128 * WI) k_dw16(
     const float* __restrict__ gscale, int64_t ld_g, int B, Margin mg, float sB, float lr,
     float mu) {
   constexpr int D = 128 * WI;
-  constexpr int NT = 128 * WI;
-  constexpr int NW = 2 * WI;
+  constexpr int NW = 4;
+  constexpr int DW = D / NW;            // d entries of a wave
+  constexpr int MB = DW / 32;           // 32-entry d blocks of a wave
+  constexpr int NB = kDwCls / 32;       // 32-class blocks
   constexpr int XDMA = D / 16 / NW;     // X^T loads (16 d rows each) per wave per chunk
   constexpr int RDMA = 8 / NW;          // logit-store loads (4 rows each) per wave
   constexpr int QL = 8 / NW;            // row-scale pieces (4 rows each) per wave
-  constexpr int GROUPS = 512 / NT;      // producer slots per thread
+  constexpr int GROUPS = 2;             // producer slots per thread (512 / 256)
   constexpr int PER_ITER = XDMA + RDMA + 1;
-  static_assert(XDMA == 4, "X^T loads per wave");
+  constexpr int NF = MB + NB;           // fragment reads per k-step
+  static_assert(PER_ITER + 2 * (RDMA + 1) < 64, "vmcnt range");
   const int K = *n_active_p;
   const int64_t j0 = (int64_t)blockIdx.x * kDwCls;
   if (j0 >= K) return;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wi = wave >> 1, wj = wave & 1;
   const int half = lane >> 5, l32 = lane & 31;
   const int n_chunks = (int)ceil_div(B, kBwKC);
   const int c_stop = (int)ceil_div(n_chunks, 3) * 3;
@@ -496,7 +504,7 @@ __global__ void __launch_bounds__(128 * WI) k_dw16(
   uint32_t ptr_off[GROUPS];   // byte offset of the lane's transposing raw read
 #pragma unroll
   for (int u = 0; u < GROUPS; ++u) {
-    const int s = 4 * wave + grp + (NT / 16) * u;
+    const int s = 4 * wave + grp + 16 * u;
     const int cb = s >> 2;
     pcls[u] = 16 * cb + gi;
     prg[u] = s & 3;
@@ -507,38 +515,45 @@ __global__ void __launch_bounds__(128 * WI) k_dw16(
     ptr_off[u] = (uint32_t)(r * kDwCls * 2 + 16 * ((2 * cb + (q >> 1)) ^ (2 * (r & 3))) + 8 * (q & 1));
   }
 
-  // Raw cosines: load v of this wave covers rows 4 b .. 4 b + 3 (b = wave RDMA + v);
-  // lane l fills piece l % 16 of row 4 b + l / 16 with source piece
-  // (l % 16) ^ 2 (row & 3).
-  auto dma_raw = [&](auto st, int c) {
+  // Raw logit-store values: load v of this wave covers rows 4 b .. 4 b + 3
+  // (b = wave RDMA + v); lane l fills piece l % 16 of row 4 b + l / 16 with
+  // source piece (l % 16) ^ 2 (row & 3).
+  auto dma_raw_piece = [&](auto st, int c, int v) __attribute__((always_inline)) {
     constexpr int S = decltype(st)::value;
     const int cc = c < n_chunks ? c : n_chunks - 1;
-#pragma unroll
-    for (int v = 0; v < RDMA; ++v) {
-      const int blk = wave * RDMA + v;
-      const int r = 4 * blk + (lane >> 4);
-      int n = cc * kBwKC + r;
-      n = n < B ? n : B - 1;
-      const int piece = (lane & 15) ^ (2 * (r & 3));
-      dma16(lbuf + (int64_t)n * ld_cos + j0 + 8 * piece, dw_r<S>() + 512 * blk);
-    }
-    // Row scales of the chunk: QL 16-byte pieces (4 rows each) per wave; rows < ld_g always.
+    const int blk = wave * RDMA + v;
+    const int r = 4 * blk + (lane >> 4);
+    int n = cc * kBwKC + r;
+    n = n < B ? n : B - 1;
+    const int piece = (lane & 15) ^ (2 * (r & 3));
+    dma16(lbuf + (int64_t)n * ld_cos + j0 + 8 * piece, dw_r<S>() + 512 * blk);
+  };
+  // Row scales of the chunk: QL 16-byte pieces (4 rows each) per wave; rows < ld_g always.
+  auto dma_scale = [&](auto st, int c) __attribute__((always_inline)) {
+    constexpr int S = decltype(st)::value;
+    const int cc = c < n_chunks ? c : n_chunks - 1;
     if (lane < QL) dma16(gsc + cc * kBwKC + 4 * (QL * wave + lane), dw_q<S>() + 4 * QL * wave);
+  };
+  auto dma_raw = [&](auto st, int c) __attribute__((always_inline)) {
+#pragma unroll
+    for (int v = 0; v < RDMA; ++v) dma_raw_piece(st, c, v);
+    dma_scale(st, c);
   };
   // X^T: block cc of the transposed batch ([d][32], contiguous); load v of this
   // wave covers d rows 16 m .. 16 m + 15 (m = wave XDMA + v), 4 pieces each;
   // lane l fills piece l & 3 of row 16 m + l / 4 with source piece
   // (l & 3) ^ ((row >> 1) & 3).
-  auto dma_x = [&](auto st, int c) {
+  auto dma_x_piece = [&](auto st, int c, int v) __attribute__((always_inline)) {
     constexpr int S = decltype(st)::value;
     const int cc = c < n_chunks ? c : n_chunks - 1;
+    const int m = wave * XDMA + v;
+    const int i = 16 * m + (lane >> 2);
+    const int piece = (lane & 3) ^ ((i >> 1) & 3);
+    dma16(xbT + ((int64_t)cc * D + i) * kBwKC + 8 * piece, dw_x<S>() + 512 * m);
+  };
+  auto dma_x = [&](auto st, int c) __attribute__((always_inline)) {
 #pragma unroll
-    for (int v = 0; v < XDMA; ++v) {
-      const int m = wave * XDMA + v;
-      const int i = 16 * m + (lane >> 2);
-      const int piece = (lane & 3) ^ ((i >> 1) & 3);
-      dma16(xbT + ((int64_t)cc * D + i) * kBwKC + 8 * piece, dw_x<S>() + 512 * m);
-    }
+    for (int v = 0; v < XDMA; ++v) dma_x_piece(st, c, v);
   };
   // Coefficients of chunk c: G^T[class][row] = p = E * gscale_row (the operand
   // X^T holds x_hat, so no 1/||x|| here).  E is 0 at targets and past |S|,
@@ -560,42 +575,54 @@ __global__ void __launch_bounds__(128 * WI) k_dw16(
       ds_read_128<16>(in.sq[u][1], qa);
     }
   };
-  auto produce_store = [&](auto st, ProdIn& in) {
+  auto pin_group = [&](ProdIn& in, int u) __attribute__((always_inline)) {
+    pin_reg(in.qlo[u]);
+    pin_reg(in.qhi[u]);
+    pin_reg(in.sq[u][0]);
+    pin_reg(in.sq[u][1]);
+  };
+  // Group u's coefficients into stage S; gmask 0 writes zeros (a chunk past
+  // the batch, whose MFMAs then add nothing).
+  auto produce_group = [&](auto st, ProdIn& in, int u, uint32_t gmask) __attribute__((always_inline)) {
     constexpr int S = decltype(st)::value;
+    const uint32_t qw[4] = {in.qlo[u].x, in.qlo[u].y, in.qhi[u].x, in.qhi[u].y};
+    const float sc[8] = {__uint_as_float(in.sq[u][0].x), __uint_as_float(in.sq[u][0].y),
+                         __uint_as_float(in.sq[u][0].z), __uint_as_float(in.sq[u][0].w),
+                         __uint_as_float(in.sq[u][1].x), __uint_as_float(in.sq[u][1].y),
+                         __uint_as_float(in.sq[u][1].z), __uint_as_float(in.sq[u][1].w)};
+    float v[8];
 #pragma unroll
-    for (int u = 0; u < GROUPS; ++u) {
-      pin_reg(in.qlo[u]);
-      pin_reg(in.qhi[u]);
-      pin_reg(in.sq[u][0]);
-      pin_reg(in.sq[u][1]);
-      const uint32_t qw[4] = {in.qlo[u].x, in.qlo[u].y, in.qhi[u].x, in.qhi[u].y};
-      const float sc[8] = {__uint_as_float(in.sq[u][0].x), __uint_as_float(in.sq[u][0].y),
-                           __uint_as_float(in.sq[u][0].z), __uint_as_float(in.sq[u][0].w),
-                           __uint_as_float(in.sq[u][1].x), __uint_as_float(in.sq[u][1].y),
-                           __uint_as_float(in.sq[u][1].z), __uint_as_float(in.sq[u][1].w)};
-      float v[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float ev = (e & 1) ? f16_hi(qw[e >> 1]) : f16_lo(qw[e >> 1]);
-        v[e] = ev * sc[e];
-      }
-      const uint4 o = pack8<Bf16Tag>(v);
-      const int cl = pcls[u];
-      ds_write_128<0>(lds_addr(dw_g<S>()) + cl * kBwKC * 2 + 16 * (prg[u] ^ ((cl >> 1) & 3)),
-                      u32x4_t{o.x, o.y, o.z, o.w});
+    for (int e = 0; e < 8; ++e) {
+      const float ev = (e & 1) ? f16_hi(qw[e >> 1]) : f16_lo(qw[e >> 1]);
+      v[e] = ev * sc[e];
     }
+    const uint4 o = pack8<Bf16Tag>(v);
+    const int cl = pcls[u];
+    ds_write_128<0>(lds_addr(dw_g<S>()) + cl * kBwKC * 2 + 16 * (prg[u] ^ ((cl >> 1) & 3)),
+                    u32x4_t{o.x & gmask, o.y & gmask, o.z & gmask, o.w & gmask});
   };
 
   // Fragment byte offsets: operand row (d entry or class) 32 q + l32 of the
   // wave's block, chunk 2 kk + half stored at chunk ^ ((row >> 1) & 3).
   const int sw = (l32 >> 1) & 3;
-  const uint32_t a_lane0 = (uint32_t)((128 * wi + l32) * kBwKC * 2 + 16 * ((0 + half) ^ sw));
-  const uint32_t a_lane1 = (uint32_t)((128 * wi + l32) * kBwKC * 2 + 16 * ((2 + half) ^ sw));
-  const uint32_t b_lane0 = (uint32_t)((64 * wj + l32) * kBwKC * 2 + 16 * ((0 + half) ^ sw));
-  const uint32_t b_lane1 = (uint32_t)((64 * wj + l32) * kBwKC * 2 + 16 * ((2 + half) ^ sw));
+  const uint32_t a_lane0 = (uint32_t)((DW * wave + l32) * kBwKC * 2 + 16 * ((0 + half) ^ sw));
+  const uint32_t a_lane1 = (uint32_t)((DW * wave + l32) * kBwKC * 2 + 16 * ((2 + half) ^ sw));
+  const uint32_t b_lane0 = (uint32_t)(l32 * kBwKC * 2 + 16 * ((0 + half) ^ sw));
+  const uint32_t b_lane1 = (uint32_t)(l32 * kBwKC * 2 + 16 * ((2 + half) ^ sw));
 
-  f32x16_t acc[4][2];
-  zero_acc(acc);
+  f32x16_t acc[MB][NB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.0f;
+  // Second k-step fragments, carried from one chunk to the next.
+  u32x4_t a1[MB], b1[NB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) a1[mb] = u32x4_t{0, 0, 0, 0};
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) b1[nb] = u32x4_t{0, 0, 0, 0};
 
   {
     using S0 = std::integral_constant<int, 0>;
@@ -611,210 +638,291 @@ __global__ void __launch_bounds__(128 * WI) k_dw16(
     ProdIn in0;
     produce_load(S0{}, in0);
     lgkm_wait<0>();
-    produce_store(S0{}, in0);
+    pin_group(in0, 0);
+    pin_group(in0, 1);
+    produce_group(S0{}, in0, 0, 0xFFFFFFFFu);
+    produce_group(S0{}, in0, 1, 0xFFFFFFFFu);
   }
+  // Instruction slots of a chunk: NMF MFMAs per k-step, each followed by
+  // the work placed after it, so that the wave issues its other instructions
+  // while the matrix pipe works through the MFMAs already issued.
+  constexpr int NMF = MB * NB;
+  constexpr int W_AT = NMF >= 16 ? 3 : NMF / 4;      // wait for the chunk's fragment and producer reads
+  constexpr int G0_AT = NMF / 2 - 1;                 // coefficient group 0 written
+  constexpr int G1_AT = NMF - 2 > G0_AT ? NMF - 2 : G0_AT + 1;  // group 1 written
+  constexpr int NITEM = RDMA + 1 + XDMA + NF;        // loads and reads spread over the second k-step
+  static_assert(G1_AT < NMF, "slots");
   for (int c = 0; c < c_stop; c += 3) {
     static_for<0, 3>([&](auto uu) {
       constexpr int u = decltype(uu)::value;
+      using SU = std::integral_constant<int, u>;
+      using SN = std::integral_constant<int, (u + 1) % 3>;
+      using SX = std::integral_constant<int, (u + 2) % 3>;
       const int cu = c + u;
       // Landed: X^T of chunk cu, raw data of chunk cu + 1; this wave's
-      // coefficient writes of the previous iteration are complete.
+      // coefficient writes and second k-step reads of the previous chunk are
+      // complete.
       wait_vmcnt_lgkm0<PER_ITER>();
       stage_barrier();
       const uint32_t xs = lds_addr(dw_x<u>());
       const uint32_t gs = lds_addr(dw_g<u>());
-      // The producer's reads go first: they are consumed while the first
-      // k-step's MFMAs run.
+      u32x4_t a0[MB], b0[NB];
+      static_for<0, MB>([&](auto mm) {
+        constexpr int mb = decltype(mm)::value;
+        ds_read_128<32 * mb * kBwKC * 2>(a0[mb], xs + a_lane0);
+      });
+      static_for<0, NB>([&](auto nn) {
+        constexpr int nb = decltype(nn)::value;
+        ds_read_128<32 * nb * kBwKC * 2>(b0[nb], gs + b_lane0);
+      });
       ProdIn pin;
-      produce_load(std::integral_constant<int, (u + 1) % 3>{}, pin);
-      u32x4_t af[2][4], bf[2][2];
-      static_for<0, 4>([&](auto mm) {
-        constexpr int mb = decltype(mm)::value;
-        ds_read_128<32 * mb * kBwKC * 2>(af[0][mb], xs + a_lane0);
-      });
-      static_for<0, 2>([&](auto nn) {
-        constexpr int nb = decltype(nn)::value;
-        ds_read_128<32 * nb * kBwKC * 2>(bf[0][nb], gs + b_lane0);
-      });
-      static_for<0, 4>([&](auto mm) {
-        constexpr int mb = decltype(mm)::value;
-        ds_read_128<32 * mb * kBwKC * 2>(af[1][mb], xs + a_lane1);
-      });
-      static_for<0, 2>([&](auto nn) {
-        constexpr int nb = decltype(nn)::value;
-        ds_read_128<32 * nb * kBwKC * 2>(bf[1][nb], gs + b_lane1);
-      });
-      dma_raw(std::integral_constant<int, u>{}, cu + 3);
-      dma_x(std::integral_constant<int, (u + 2) % 3>{}, cu + 2);
-      static_for<0, 2>([&](auto kq) {
-        constexpr int kk = decltype(kq)::value;
-        if constexpr (kk == 0) {
-          // producer reads and the first k-step's fragments have landed
-          lgkm_wait<6>(af[0][0], af[0][1], af[0][2], af[0][3], bf[0][0], bf[0][1]);
-        } else {
-          // the next coefficients are produced while the first k-step's MFMAs run
-          produce_store(std::integral_constant<int, (u + 1) % 3>{}, pin);
-          lgkm_wait<0>(af[1][0], af[1][1], af[1][2], af[1][3], bf[1][0], bf[1][1]);
+      produce_load(SN{}, pin);
+      const uint32_t gmask = cu + 1 < n_chunks ? 0xFFFFFFFFu : 0u;
+      // Second k-step of the previous chunk (fragments landed before the
+      // barrier), with the next chunk's coefficients produced alongside.
+      pin_reg(a1);
+      pin_reg(b1);
+      static_for<0, NMF>([&](auto ii) {
+        constexpr int i = decltype(ii)::value;
+        mfma_bf16_asm(acc[i / NB][i % NB], a1[i / NB], b1[i % NB]);
+        if constexpr (i == W_AT) {
+          lgkm_wait<0>(a0, b0);
+          pin_group(pin, 0);
         }
-        if (cu < n_chunks) {
-#pragma unroll
-          for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-            for (int nb = 0; nb < 2; ++nb)
-              acc[mb][nb] = mfma_32x32x16(as_uint4(af[kk][mb]), as_uint4(bf[kk][nb]),
-                                          acc[mb][nb], Bf16Tag{});
-        }
+        if constexpr (i == G0_AT) produce_group(SN{}, pin, 0, gmask);
+        if constexpr (i == G0_AT + 1) pin_group(pin, 1);
+        if constexpr (i == G1_AT) produce_group(SN{}, pin, 1, gmask);
+      });
+      // First k-step of this chunk, with the loads of later chunks and this
+      // chunk's second k-step reads spread over its slots.
+      static_for<0, NMF>([&](auto ii) {
+        constexpr int i = decltype(ii)::value;
+        mfma_bf16_asm(acc[i / NB][i % NB], a0[i / NB], b0[i % NB]);
+        static_for<(i * NITEM + NMF - 1) / NMF, ((i + 1) * NITEM + NMF - 1) / NMF>([&](auto kk) {
+          constexpr int k = decltype(kk)::value;
+          if constexpr (k < RDMA) {
+            dma_raw_piece(SU{}, cu + 3, k);
+          } else if constexpr (k == RDMA) {
+            dma_scale(SU{}, cu + 3);
+          } else if constexpr (k < RDMA + 1 + XDMA) {
+            dma_x_piece(SX{}, cu + 2, k - RDMA - 1);
+          } else if constexpr (k < RDMA + 1 + XDMA + MB) {
+            constexpr int mb = k - RDMA - 1 - XDMA;
+            ds_read_128<32 * mb * kBwKC * 2>(a1[mb], xs + a_lane1);
+          } else {
+            constexpr int nb = k - RDMA - 1 - XDMA - MB;
+            ds_read_128<32 * nb * kBwKC * 2>(b1[nb], gs + b_lane1);
+          }
+        });
       });
     });
   }
   wait_vmcnt<0>();
-
-  // ---- epilogue: lane owns class j (per nb) and 64 of its d entries.
-  // Target terms of the rows labelled with one of this wave's 64 classes.
-  const int64_t jw = j0 + 64 * wj;
-  for (int nbase = 0; nbase < B; nbase += 64) {
-    const int n = nbase + lane;
-    const int yv = n < B ? yhat[n] : -1;
-    uint64_t mask = __ballot(yv >= jw && yv < jw + 64);
-    while (mask) {
-      const int bit = __ffsll((unsigned long long)mask) - 1;
-      mask &= mask - 1;
-      const int nn = nbase + bit;
-      const int yt = __shfl(yv, bit, 64);
-      const float gt = target_coef(mg, tgtc[nn], row_lse[nn]) * inv_x[nn];
+  wait_lgkm0();
+  // Second k-step of the last chunk (zero coefficients past the batch).
+  pin_reg(a1);
+  pin_reg(b1);
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb) {
-        if (jw + 32 * nb + l32 != yt) continue;
+  for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-        for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-          for (int g = 0; g < 4; ++g)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const int i = 128 * wi + 32 * mb + 8 * g + 4 * half + e;
-              acc[mb][nb][4 * g + e] =
-                  fmaf(gt, load16<Tag>(X, (int64_t)nn * D + i), acc[mb][nb][4 * g + e]);
-            }
-      }
-    }
-  }
+    for (int nb = 0; nb < NB; ++nb) mfma_bf16_asm(acc[mb][nb], a1[mb], b1[nb]);
+  mfma_drain();
 
   // ---- update: the tile goes through LDS in four passes of 32 classes so
   // that each wave then owns whole rows: W, momentum and master rows are read
-  // and written in full contiguous segments.  Pass p = (pwj, pnb) holds the
-  // classes 64 pwj + 32 pnb + r (r < 32); entry d of row r sits in stage
-  // array d / 256 at r * kTLd + d % 256.  Lane l owns d = 256 h + 4 l .. + 3.
+  // and written in full contiguous segments.  Pass p holds the classes
+  // 32 p + r (r < 32); entry d of row r sits in stage array d / 256 at
+  // r * kTLd + d % 256.  Wave w owns rows 8 w .. 8 w + 7 of each pass; lane l
+  // owns d = 256 h + 4 l .. + 3.  A wave's rows of a pass are loaded before
+  // the pass's gradients are parked.
   constexpr int NH = D > 256 ? 2 : 1;         // 256-entry halves of a row
   constexpr int LPH = (D > 256 ? 256 : D) / 4;  // lanes that own entries
   constexpr int RPW = 32 / NW;                // rows of a pass per wave
-  constexpr int RB = RPW < 4 ? RPW : 4;       // rows per load batch
   float* const tlo = reinterpret_cast<float*>(wX0);
   float* const thi = reinterpret_cast<float*>(wX1);
   const bool lane_on = lane < LPH;
-  wait_lgkm0();
+  int* const hits = reinterpret_cast<int*>(wG0);   // NW lists of kHitCap entries
+  int* const hit_n = reinterpret_cast<int*>(wQ0);  // their lengths
+  static_assert(NW * kHitCap * 4 <= kDwCls * kBwKC * 2, "hit lists fit a coefficient stage");
+
+  struct Rows {
+    uint2 wv[RPW][NH];   // four 16-bit weights
+    float4 mv[RPW][NH], pv[RPW][NH];
+    int64_t rowa[RPW];
+    float iwr[RPW];
+    bool rv[RPW];
+  };
+  auto load_rows = [&](Rows& bt, int p) __attribute__((always_inline)) {
+#pragma unroll
+    for (int k = 0; k < RPW; ++k) {
+      const int64_t j = j0 + 32 * p + RPW * wave + k;
+      bt.rv[k] = j < K && lane_on;
+      bt.rowa[k] = j < K ? (int64_t)active[j] : 0;
+      bt.iwr[k] = j < K ? inv_w[j] : 0.0f;
+#pragma unroll
+      for (int h = 0; h < NH; ++h) {
+        const int64_t off = bt.rowa[k] * D + 256 * h + 4 * lane;
+        bt.wv[k][h] = make_uint2(0, 0);
+        bt.mv[k][h] = bt.pv[k][h] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        if (bt.rv[k]) {
+          bt.wv[k][h] = *reinterpret_cast<const uint2*>(W + off);
+          bt.mv[k][h] = *reinterpret_cast<const float4*>(M + off);
+          if (W_master) bt.pv[k][h] = *reinterpret_cast<const float4*>(W_master + off);
+        }
+      }
+    }
+  };
+  auto park = [&](auto pp) __attribute__((always_inline)) {
+    constexpr int p = decltype(pp)::value;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int d0 = DW * wave + 32 * mb + 8 * g + 4 * half;
+        *reinterpret_cast<float4*>((d0 >= 256 ? thi : tlo) + l32 * kTLd + (d0 & 255)) =
+            make_float4(acc[mb][p][4 * g], acc[mb][p][4 * g + 1], acc[mb][p][4 * g + 2],
+                        acc[mb][p][4 * g + 3]);
+      }
+  };
+  // Target term of batch row nn added to staged row r (this wave's own row).
+  auto add_target = [&](int nn, int r) {
+    const float gt = target_coef(mg, tgtc[nn], row_lse[nn]) * inv_x[nn];
+    if (!lane_on) return;
+#pragma unroll
+    for (int h = 0; h < NH; ++h) {
+      const uint2 x4 = *reinterpret_cast<const uint2*>(
+          reinterpret_cast<const uint16_t*>(X) + (int64_t)nn * D + 256 * h + 4 * lane);
+      float4* t = reinterpret_cast<float4*>((h ? thi : tlo) + r * kTLd + 4 * lane);
+      float4 a = *t;
+      a.x = fmaf(gt, to_float<Tag>((uint16_t)(x4.x & 0xFFFF)), a.x);
+      a.y = fmaf(gt, to_float<Tag>((uint16_t)(x4.x >> 16)), a.y);
+      a.z = fmaf(gt, to_float<Tag>((uint16_t)(x4.y & 0xFFFF)), a.z);
+      a.w = fmaf(gt, to_float<Tag>((uint16_t)(x4.y >> 16)), a.w);
+      *t = a;
+    }
+  };
+  auto update_rows = [&](Rows& bt) __attribute__((always_inline)) {
+#pragma unroll
+    for (int k = 0; k < RPW; ++k) {
+      const int r = RPW * wave + k;
+      float4 gv[NH], wf[NH];
+      float dot = 0.0f;
+#pragma unroll
+      for (int h = 0; h < NH; ++h) {
+        const uint2 w4 = bt.wv[k][h];
+        wf[h] = make_float4(to_float<Tag>((uint16_t)(w4.x & 0xFFFF)), to_float<Tag>((uint16_t)(w4.x >> 16)),
+                            to_float<Tag>((uint16_t)(w4.y & 0xFFFF)), to_float<Tag>((uint16_t)(w4.y >> 16)));
+        gv[h] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        if (bt.rv[k]) {
+          const float4 a4 = *reinterpret_cast<const float4*>((h ? thi : tlo) + r * kTLd + 4 * lane);
+          gv[h] = make_float4(sB * a4.x, sB * a4.y, sB * a4.z, sB * a4.w);
+          dot = fmaf(wf[h].x * bt.iwr[k], gv[h].x, dot);
+          dot = fmaf(wf[h].y * bt.iwr[k], gv[h].y, dot);
+          dot = fmaf(wf[h].z * bt.iwr[k], gv[h].z, dot);
+          dot = fmaf(wf[h].w * bt.iwr[k], gv[h].w, dot);
+        }
+      }
+      dot = wave_sum(dot);
+      if (!bt.rv[k]) continue;
+#pragma unroll
+      for (int h = 0; h < NH; ++h) {
+        const int64_t off = bt.rowa[k] * D + 256 * h + 4 * lane;
+        const float wo[4] = {wf[h].x, wf[h].y, wf[h].z, wf[h].w};
+        const float go[4] = {gv[h].x, gv[h].y, gv[h].z, gv[h].w};
+        float mo[4] = {bt.mv[k][h].x, bt.mv[k][h].y, bt.mv[k][h].z, bt.mv[k][h].w};
+        float po[4] = {bt.pv[k][h].x, bt.pv[k][h].y, bt.pv[k][h].z, bt.pv[k][h].w};
+        float wn[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float gr = bt.iwr[k] * (go[e] - wo[e] * bt.iwr[k] * dot);
+          mo[e] = mu * mo[e] + gr;
+          if (W_master) {
+            po[e] = po[e] - lr * mo[e];
+            wn[e] = po[e];
+          } else {
+            wn[e] = wo[e] - lr * mo[e];
+          }
+        }
+        *reinterpret_cast<float4*>(M + off) = make_float4(mo[0], mo[1], mo[2], mo[3]);
+        if (W_master)
+          *reinterpret_cast<float4*>(W_master + off) = make_float4(po[0], po[1], po[2], po[3]);
+        uint2 o;
+        o.x = pack2<Tag>(wn[0], wn[1]);
+        o.y = pack2<Tag>(wn[2], wn[3]);
+        *reinterpret_cast<uint2*>(W + off) = o;
+      }
+    }
+  };
+
+  Rows bat;
+  load_rows(bat, 0);
   stage_barrier();  // every wave's fragment reads of the stage arrays are done
+  // Target terms: wave w lists, in row order, the rows n of its quarter of the
+  // batch whose label is one of the tile's classes (entry n * 128 + class
+  // offset).  A quarter with more than kHitCap such rows makes each wave scan
+  // all labels instead.  Either way the terms are added to the staged
+  // gradient rows by the wave that owns the row, in increasing n.
+  {
+    const int q0 = (int)((int64_t)B * wave / NW), q1 = (int)((int64_t)B * (wave + 1) / NW);
+    int cnt = 0;
+    for (int nbase = q0; nbase < q1; nbase += 64) {
+      const int n = nbase + lane;
+      const int yv = n < q1 ? yhat[n] : -1;
+      const bool hit = yv >= j0 && yv < j0 + kDwCls;
+      const uint64_t mask = __ballot(hit);
+      const int pos = cnt + __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                                      __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
+      if (hit && pos < kHitCap) hits[kHitCap * wave + pos] = n * kDwCls + (int)(yv - j0);
+      cnt += __popcll(mask);
+    }
+    if (lane == 0) hit_n[wave] = cnt;
+  }
+  park(std::integral_constant<int, 0>{});
+  wait_lgkm0();
+  stage_barrier();
+  int hn[NW];
+  bool hit_scan = false;
 #pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    hn[w] = __builtin_amdgcn_readfirstlane(hit_n[w]);
+    hit_scan |= hn[w] > kHitCap;
+  }
   for (int p = 0; p < 4; ++p) {
-    const int pwj = p & 1, pnb = p >> 1;
-    float4 wv[RB][NH], mv[RB][NH], pv[RB][NH];
-    int64_t rowa[RB];
-    float iwr[RB];
-    bool rv[RB];
-    // Global loads of a batch of this wave's rows (issued before they are needed).
-    auto load_batch = [&](int b) {
-#pragma unroll
-      for (int q = 0; q < RB; ++q) {
-        const int r = wave * RPW + b * RB + q;
-        const int64_t j = j0 + 64 * pwj + 32 * pnb + r;
-        rv[q] = j < K && lane_on;
-        rowa[q] = j < K ? (int64_t)active[j] : 0;
-        iwr[q] = j < K ? inv_w[j] : 0.0f;
-#pragma unroll
-        for (int h = 0; h < NH; ++h) {
-          const int64_t off = rowa[q] * D + 256 * h + 4 * lane;
-          wv[q][h] = mv[q][h] = pv[q][h] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-          if (rv[q]) {
-            const uint2 w4 = *reinterpret_cast<const uint2*>(W + off);
-            wv[q][h] = make_float4(to_float<Tag>((uint16_t)(w4.x & 0xFFFF)),
-                                   to_float<Tag>((uint16_t)(w4.x >> 16)),
-                                   to_float<Tag>((uint16_t)(w4.y & 0xFFFF)),
-                                   to_float<Tag>((uint16_t)(w4.y >> 16)));
-            mv[q][h] = *reinterpret_cast<const float4*>(M + off);
-            if (W_master) pv[q][h] = *reinterpret_cast<const float4*>(W_master + off);
-          }
-        }
-      }
-    };
-    load_batch(0);
-    // The owning waves park this pass's accumulators in LDS.
-    if (wj == pwj) {
-#pragma unroll
-      for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int d0 = 128 * wi + 32 * mb + 8 * g + 4 * half;
-          *reinterpret_cast<float4*>((d0 >= 256 ? thi : tlo) + l32 * kTLd + (d0 & 255)) =
-              make_float4(acc[mb][pnb][4 * g], acc[mb][pnb][4 * g + 1], acc[mb][pnb][4 * g + 2],
-                          acc[mb][pnb][4 * g + 3]);
-        }
-    }
-    wait_lgkm0();
-    stage_barrier();
-#pragma unroll
-    for (int b = 0; b < RPW / RB; ++b) {
-      if (b > 0) load_batch(b);
-#pragma unroll
-      for (int q = 0; q < RB; ++q) {
-        const int r = wave * RPW + b * RB + q;
-        float4 gv[NH];
-        float dot = 0.0f;
-#pragma unroll
-        for (int h = 0; h < NH; ++h) {
-          gv[h] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-          if (rv[q]) {
-            const float4 a4 = *reinterpret_cast<const float4*>((h ? thi : tlo) + r * kTLd + 4 * lane);
-            gv[h] = make_float4(sB * a4.x, sB * a4.y, sB * a4.z, sB * a4.w);
-            dot = fmaf(wv[q][h].x * iwr[q], gv[h].x, dot);
-            dot = fmaf(wv[q][h].y * iwr[q], gv[h].y, dot);
-            dot = fmaf(wv[q][h].z * iwr[q], gv[h].z, dot);
-            dot = fmaf(wv[q][h].w * iwr[q], gv[h].w, dot);
-          }
-        }
-        dot = wave_sum(dot);
-        if (!rv[q]) continue;
-#pragma unroll
-        for (int h = 0; h < NH; ++h) {
-          const int64_t off = rowa[q] * D + 256 * h + 4 * lane;
-          const float wo[4] = {wv[q][h].x, wv[q][h].y, wv[q][h].z, wv[q][h].w};
-          const float go[4] = {gv[h].x, gv[h].y, gv[h].z, gv[h].w};
-          float mo[4] = {mv[q][h].x, mv[q][h].y, mv[q][h].z, mv[q][h].w};
-          float po[4] = {pv[q][h].x, pv[q][h].y, pv[q][h].z, pv[q][h].w};
-          float wn[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float gr = iwr[q] * (go[e] - wo[e] * iwr[q] * dot);
-            mo[e] = mu * mo[e] + gr;
-            if (W_master) {
-              po[e] = po[e] - lr * mo[e];
-              wn[e] = po[e];
-            } else {
-              wn[e] = wo[e] - lr * mo[e];
-            }
-          }
-          *reinterpret_cast<float4*>(M + off) = make_float4(mo[0], mo[1], mo[2], mo[3]);
-          if (W_master)
-            *reinterpret_cast<float4*>(W_master + off) = make_float4(po[0], po[1], po[2], po[3]);
-          uint2 o;
-          o.x = pack2<Tag>(wn[0], wn[1]);
-          o.y = pack2<Tag>(wn[2], wn[3]);
-          *reinterpret_cast<uint2*>(W + off) = o;
-        }
-      }
-    }
-    if (p < 3) {
+    if (p > 0) {
+      load_rows(bat, p);
       wait_lgkm0();
-      stage_barrier();  // the stage arrays are rewritten by the next pass
+      stage_barrier();  // the stage arrays are rewritten by this pass
+      switch (p) {
+        case 1: park(std::integral_constant<int, 1>{}); break;
+        case 2: park(std::integral_constant<int, 2>{}); break;
+        default: park(std::integral_constant<int, 3>{}); break;
+      }
+      wait_lgkm0();
+      stage_barrier();
     }
+    // This wave's rows of the pass: class offsets c0 .. c0 + RPW - 1.
+    const int c0 = 32 * p + RPW * wave;
+    if (!hit_scan) {
+      for (int w = 0; w < NW; ++w)
+        for (int i = 0; i < hn[w]; ++i) {
+          const int ent = hits[kHitCap * w + i];
+          const int ct = ent & (kDwCls - 1);
+          if (ct >= c0 && ct < c0 + RPW) add_target(ent / kDwCls, ct & 31);
+        }
+    } else {
+      for (int nbase = 0; nbase < B; nbase += 64) {
+        const int n = nbase + lane;
+        const int yv = n < B ? yhat[n] : -1;
+        uint64_t mask = __ballot(yv >= j0 + c0 && yv < j0 + c0 + RPW);
+        while (mask) {
+          const int bit = __ffsll((unsigned long long)mask) - 1;
+          mask &= mask - 1;
+          const int yt = __shfl(yv, bit, 64);
+          add_target(nbase + bit, (int)(yt - j0) & 31);
+        }
+      }
+    }
+    update_rows(bat);
   }
 }
 
@@ -952,7 +1060,7 @@ void launch_bwd16(const StepArgs& a, const StepWs& w, const Margin& mg, float sB
                      w.inv_x, w.inv_w, w.tgtc, B, (int)a.d, mg, sB, a.dX);
   timing_stop(5, stream);
   timing_start(6, stream);
-  hipLaunchKernelGGL((k_dw16<Tag, WI>), dim3((unsigned)ceil_div(a.cap, kDwCls)), dim3(128 * WI),
+  hipLaunchKernelGGL((k_dw16<Tag, WI>), dim3((unsigned)ceil_div(a.cap, kDwCls)), dim3(256),
                      0, stream, (const uint16_t*)w.xbT, w.ld_xt, a.X, (uint16_t*)a.W, a.W_master, a.M,
                      a.active, a.n_active, a.labels_mapped, a.row_lse, w.inv_x, w.inv_w,
                      w.tgtc, (const uint16_t*)w.lbuf, w.ld_cos, w.gscale, w.ld_g, B, mg, sB, a.lr,

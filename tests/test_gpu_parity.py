@@ -144,3 +144,12 @@ def test_sampler_full_size(dev, name):
     assert K == len(active_ref) == max(O.budget(cfg["r"], cfg["C"]), info["n_pos"])
     assert np.array_equal(shard.active[:K].cpu().numpy(), active_ref)
     assert np.array_equal(shard.labels_mapped.cpu().numpy(), mapped_ref)
+
+
+def test_many_rows_per_class(dev):
+    # Every row is labelled with one of three classes of the same 128-class
+    # tile: each quarter of the batch holds more target rows of that tile than
+    # the class-gradient kernel lists, so it scans the labels instead.
+    rng = np.random.default_rng(13)
+    labels = rng.choice(np.array([5, 6, 100]), size=2400)
+    _case(dev, 2400, 128, 3000, 0.1, "bf16", "arcface", 0.5, seed=13, labels=labels)
