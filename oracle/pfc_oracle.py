@@ -14,8 +14,8 @@ evaluate the same definitions on that subset; rows of the forward pass are
 independent, and a class gradient needs only the per-row log-sum-exp, so large
 problems can be checked on sampled outputs.
 
-Parity status: sampling, remap, forward, backward and the update are pinned
-(see tests/test_oracle.py).  "Parity unpinned": ArcFace where theta + m > pi
+Parity status: sampling, remap, forward, backward, the update and the PFC*
+conflict filter are pinned (see tests/test_oracle.py).  "Parity unpinned": ArcFace where theta + m > pi
 (only finiteness is checked there), and the exact rounding points of the GPU's
 16-bit operands (covered by tolerance only).
 """
@@ -145,13 +145,36 @@ def cosines(X, Ws):
     return xh @ wh.T
 
 
-def logits(cos, yhat, s, m, margin):
-    """f = s * cos with the margin applied at each owned row's target column."""
+def conflict_mask(cos, yhat, tau):
+    """PFC* filter (Sec. 3.3.4, Eq. noise_filtering): M[n, j] = 1 at the row's target,
+    else 1 iff the unmargined cosine is <= tau.
+
+    Reading: tau None or tau >= 1 means no filtering (PFC itself); the cosine
+    never exceeds 1, so this only removes the effect of rounding at tau = 1.
+    A row whose label is outside the shard has no target column: all its
+    columns are negatives.
+    """
+    cos = np.asarray(cos, dtype=np.float64)
+    if tau is None or tau >= 1.0:
+        return np.ones(cos.shape, dtype=bool)
+    keep = cos <= tau
+    yhat = np.asarray(yhat, dtype=np.int64)
+    n = np.nonzero(yhat >= 0)[0]
+    if n.size:
+        keep[n, yhat[n]] = True
+    return keep
+
+
+def logits(cos, yhat, s, m, margin, tau=None):
+    """f = s * cos with the margin applied at each owned row's target column;
+    -inf where the PFC* filter drops the logit from the row's denominator."""
     f = s * np.asarray(cos, dtype=np.float64)
     n = np.nonzero(np.asarray(yhat) >= 0)[0]
     if n.size:
         j = np.asarray(yhat)[n]
         f[n, j] = target_logit(cos[n, j], s, m, margin)
+    if tau is not None and tau < 1.0:
+        f = np.where(conflict_mask(cos, yhat, tau), f, -np.inf)
     return f
 
 
@@ -161,11 +184,13 @@ def log_sum_exp(f):
     return mx + np.log(np.sum(np.exp(f - mx[:, None]), axis=1))
 
 
-def forward(X, Ws, yhat, s, m, margin):
+def forward(X, Ws, yhat, s, m, margin, tau=None):
     """Sampled margin-softmax cross-entropy of the rows given.
 
     Probabilities are normalised over the active set only (Eq.
-    sampled_probability).  Row loss l_n = lse_n - f_{n, yhat_n} for owned rows.
+    sampled_probability), and with the PFC* filter (tau < 1) over the
+    unfiltered logits of each row only (Eq. noise_filtering); filtered logits
+    have probability 0.  Row loss l_n = lse_n - f_{n, yhat_n} for owned rows.
     Reading: a row whose label is outside the shard has no target here and
     contributes 0 to the reported loss (its target term belongs to the owning
     shard, Sec. 3.2.1); its gradient is still P/B, the derivative of its
@@ -175,7 +200,7 @@ def forward(X, Ws, yhat, s, m, margin):
     """
     yhat = np.asarray(yhat, dtype=np.int64)
     cos = cosines(X, Ws)
-    f = logits(cos, yhat, s, m, margin)
+    f = logits(cos, yhat, s, m, margin, tau)
     lse = log_sum_exp(f)
     P = np.exp(f - lse[:, None])
     own = np.nonzero(yhat >= 0)[0]
@@ -193,14 +218,15 @@ def batch_loss(row_loss, B):
 # Backward (Eq. proxy_update, Eq. pfc_center_update, Sec. 3.2.1 matrix form)
 # ---------------------------------------------------------------------------
 
-def cos_grad(cos, lse, yhat, B, s, m, margin):
+def cos_grad(cos, lse, yhat, B, s, m, margin, tau=None):
     """dL/dcos for the rows given, with lse the rows' log-sum-exp.
 
     dF = (P - Y)/B (Sec. 3.2.1); dcos = s * dF, times the target slope at the
-    target column (margin derivative, Sec. 3.1).
+    target column (margin derivative, Sec. 3.1).  Logits dropped by the PFC*
+    filter do not enter the loss: their P, and so their gradient, is 0.
     """
     yhat = np.asarray(yhat, dtype=np.int64)
-    f = logits(cos, yhat, s, m, margin)
+    f = logits(cos, yhat, s, m, margin, tau)
     dF = np.exp(f - np.asarray(lse)[:, None])
     own = np.nonzero(yhat >= 0)[0]
     dF[own, yhat[own]] -= 1.0
@@ -224,17 +250,17 @@ def normalise_backward(A, dAhat):
     return (dAhat - ah * radial[:, None]) / nrm[:, None]
 
 
-def grad_x(X_rows, Ws, yhat_rows, lse_rows, B, s, m, margin):
+def grad_x(X_rows, Ws, yhat_rows, lse_rows, B, s, m, margin, tau=None):
     """dL/dx for the rows given (raw head input), summed over all active classes."""
     X_rows = np.asarray(X_rows, dtype=np.float64)
     Ws = np.asarray(Ws, dtype=np.float64)
     cos = cosines(X_rows, Ws)
-    dc = cos_grad(cos, lse_rows, yhat_rows, B, s, m, margin)
+    dc = cos_grad(cos, lse_rows, yhat_rows, B, s, m, margin, tau)
     wh = Ws / row_norms(Ws)[:, None]
     return normalise_backward(X_rows, dc @ wh)
 
 
-def grad_w(X, Ws_cols, cols, yhat, lse, B, s, m, margin):
+def grad_w(X, Ws_cols, cols, yhat, lse, B, s, m, margin, tau=None):
     """dL/dw for the active classes `cols` (positions in S), raw row gradients.
 
     Contributions of all batch rows are summed (Eq. pfc_center_update), so a
@@ -252,10 +278,8 @@ def grad_w(X, Ws_cols, cols, yhat, lse, B, s, m, margin):
         if t >= 0 and int(t) in where:
             pos_in_cols[n] = where[int(t)]
     # Rows whose target lies outside the subset still owe P/B on these columns.
-    f = s * cos
+    f = logits(cos, pos_in_cols, s, m, margin, tau)
     hit = np.nonzero(pos_in_cols >= 0)[0]
-    if hit.size:
-        f[hit, pos_in_cols[hit]] = target_logit(cos[hit, pos_in_cols[hit]], s, m, margin)
     dF = np.exp(f - np.asarray(lse)[:, None])
     dF[hit, pos_in_cols[hit]] -= 1.0
     dF /= B
@@ -316,21 +340,21 @@ def momentum_update(W, M, active, g, lr, mu, w_dtype, master=None):
 # ---------------------------------------------------------------------------
 
 def step(X, W, M, labels, C, a, r, seed, s, m, margin, lr, mu, w_dtype,
-         master=None):
+         master=None, tau=None):
     """Sample, remap, forward, backward and the lazy update for the whole batch.
 
-    W, M (and master) are float64 arrays updated in place.  Returns a dict with
-    active, labels_mapped, lse, loss, dx, g (raw-row gradient of each active
-    class, in S order).
+    W, M (and master) are float64 arrays updated in place.  tau < 1 turns on
+    the PFC* conflict filter.  Returns a dict with active, labels_mapped, lse,
+    loss, dx, g (raw-row gradient of each active class, in S order).
     """
     X = np.asarray(X, dtype=np.float64)
     B = X.shape[0]
     active, mapped, info = sample_active(labels, C, a, r, seed)
     Ws = np.asarray(W[active], dtype=np.float64)
-    fw = forward(X, Ws, mapped, s, m, margin)
+    fw = forward(X, Ws, mapped, s, m, margin, tau)
     loss = batch_loss(fw["row_loss"], B)
-    dx = grad_x(X, Ws, mapped, fw["lse"], B, s, m, margin)
-    g = grad_w(X, Ws, np.arange(len(active)), mapped, fw["lse"], B, s, m, margin)
+    dx = grad_x(X, Ws, mapped, fw["lse"], B, s, m, margin, tau)
+    g = grad_w(X, Ws, np.arange(len(active)), mapped, fw["lse"], B, s, m, margin, tau)
     momentum_update(W, M, active, g, lr, mu, w_dtype, master)
     return {"active": active, "labels_mapped": mapped, "info": info,
             "lse": fw["lse"], "row_loss": fw["row_loss"], "loss": loss,

@@ -437,3 +437,113 @@ def test_lazy_step_at_r1_equals_dense_step():
     opt.step()
     assert abs(out["loss"] - loss.item()) < 1e-12
     assert np.allclose(W1, tW.detach().numpy(), atol=1e-12, rtol=2**-23)   # fp32 storage rounding
+
+
+# ------------------------------------------------- PFC* conflict filter
+
+def _conflict_problem(seed, B=10, d=12, C=30, r=0.5):
+    """Rows of X placed near the centre of an active class other than their
+    own label (a duplicated identity), so that some negative cosines exceed
+    tau = 0.4, and one row near its own centre (a positive above tau)."""
+    rng = np.random.default_rng(seed)
+    W = rng.standard_normal((C, d))
+    labels = rng.integers(0, C, size=B)
+    S, y, _ = O.sample_active(labels, C, 0, r, seed)
+    X = rng.standard_normal((B, d))
+    for n in range(0, B, 2):                      # conflicts: near another row's class
+        k = y[(n + 1) % B]
+        if k != y[n]:
+            X[n] = W[S[k]] + 0.3 * rng.standard_normal(d)
+    X[1] = W[S[y[1]]] + 0.1 * rng.standard_normal(d)   # positive far above tau
+    return X, W[S], y
+
+
+def test_filter_tau_at_least_one_is_pfc():
+    """tau >= 1 keeps every logit (cos <= 1), so PFC* reduces to PFC."""
+    X, Ws, y = _conflict_problem(21)
+    B, s, m = len(y), 64.0, 0.5
+    ref = O.forward(X, Ws, y, s, m, O.ARCFACE)
+    for tau in (1.0, 1.5):
+        fw = O.forward(X, Ws, y, s, m, O.ARCFACE, tau)
+        assert np.array_equal(fw["lse"], ref["lse"])
+        assert np.array_equal(
+            O.grad_x(X, Ws, y, fw["lse"], B, s, m, O.ARCFACE, tau),
+            O.grad_x(X, Ws, y, ref["lse"], B, s, m, O.ARCFACE))
+
+
+def test_filter_matches_brute_force_definition():
+    """Loss of Eq. noise_filtering written out with loops: a logit enters row
+    n's denominator iff it is the target or its unmargined cosine is <= tau;
+    the positive is never filtered; probabilities of the kept logits sum to 1
+    and dropped logits have probability 0."""
+    tau, s, m = 0.4, 16.0, 0.35
+    X, Ws, y = _conflict_problem(22)
+    B, K = len(y), len(Ws)
+    fw = O.forward(X, Ws, y, s, m, O.COSFACE, tau)
+    n_dropped = 0
+    for n in range(B):
+        xh = X[n] / math.sqrt(sum(v * v for v in X[n]))
+        terms, ft = [], None
+        for j in range(K):
+            wh = Ws[j] / math.sqrt(sum(v * v for v in Ws[j]))
+            c = sum(a * b for a, b in zip(xh, wh))
+            if j == y[n]:
+                ft = s * (c - m)
+                terms.append(ft)
+            elif c <= tau:
+                terms.append(s * c)
+            else:
+                n_dropped += 1
+                assert fw["P"][n, j] == 0.0
+        lse = math.log(sum(math.exp(t) for t in terms))
+        assert abs(fw["lse"][n] - lse) < 1e-12 * max(1.0, abs(lse))
+        assert abs(fw["row_loss"][n] - (lse - ft)) < 1e-11
+        assert abs(np.sum(fw["P"][n]) - 1.0) < 1e-12
+    assert n_dropped >= B // 2 - 1       # the problem does exercise the filter
+    assert fw["cos"][1, y[1]] > tau      # a positive above tau is kept (checked above)
+
+
+@pytest.mark.parametrize("margin,m", [(O.COSFACE, 0.4), (O.ARCFACE, 0.5)])
+def test_filter_gradients_match_torch_autograd(margin, m):
+    """torch float64 autograd of the filtered loss (dropped logits masked to
+    -inf; the mask is piecewise constant) with W[S] as a leaf."""
+    tau, s = 0.4, 32.0
+    X, Ws, y = _conflict_problem(23)
+    B = len(y)
+    fw = O.forward(X, Ws, y, s, m, margin, tau)
+    dx = O.grad_x(X, Ws, y, fw["lse"], B, s, m, margin, tau)
+    gw = O.grad_w(X, Ws, np.arange(len(Ws)), y, fw["lse"], B, s, m, margin, tau)
+    tX = torch.tensor(X, requires_grad=True)
+    tW = torch.tensor(Ws, requires_grad=True)
+    cos = torch.nn.functional.normalize(tX, dim=1) @ torch.nn.functional.normalize(tW, dim=1).T
+    ty = torch.tensor(y.astype(np.int64))
+    rows = torch.arange(B)
+    ct = cos[rows, ty]
+    ft = s * (ct - m) if margin == O.COSFACE else s * torch.cos(torch.acos(ct) + m)
+    f = (s * cos).index_put((rows, ty), ft)
+    drop = (cos.detach() > tau)
+    drop[rows, ty] = False
+    assert bool(drop.any())
+    f = f.masked_fill(drop, -math.inf)
+    loss = (torch.logsumexp(f, dim=1) - f[rows, ty]).sum() / B
+    loss.backward()
+    assert abs(loss.item() - O.batch_loss(fw["row_loss"], B)) < 1e-12
+    assert np.allclose(dx, tX.grad.numpy(), atol=1e-12, rtol=1e-9)
+    assert np.allclose(gw, tW.grad.numpy(), atol=1e-12, rtol=1e-9)
+
+
+def test_filter_step_at_r1_is_fc_star():
+    """FC*-1.0 (Sec. 3.3.4): PFC* at r = 1 is the filtered full softmax; the
+    step's class gradients match the dense filtered gradient of every class."""
+    rng = np.random.default_rng(24)
+    B, d, C, tau, s, m = 8, 10, 16, 0.4, 64.0, 0.5
+    X = rng.standard_normal((B, d))
+    W = rng.standard_normal((C, d))
+    labels = rng.integers(0, C, size=B)
+    X[0] = W[(labels[0] + 1) % C] + 0.2 * rng.standard_normal(d)
+    out = O.step(X, W.copy(), np.zeros((C, d)), labels, C, 0, 1.0, 3, s, m, O.ARCFACE, 0.1,
+                 0.9, "f32", tau=tau)
+    assert np.array_equal(out["active"], np.arange(C))
+    fw = O.forward(X, W, labels, s, m, O.ARCFACE, tau)
+    assert abs(out["loss"] - O.batch_loss(fw["row_loss"], B)) < 1e-12
+    assert out["P"][0, (labels[0] + 1) % C] == 0.0
