@@ -21,7 +21,7 @@
  *    outputs are then undefined).  Nothing is thrown across the ABI.
  *  - `ws` is a caller-owned device workspace of at least the size that
  *    pfc_workspace_bytes() reports.  It carries the sampler state and the
- *    forward pass's intermediates (norms, quantised cosines, softmax
+ *    forward pass's intermediates (norms, the logit store, softmax
  *    statistics) into the backward pass of the SAME step: a step's three calls
  *    must use the same workspace, in order, and no other step may use that
  *    workspace concurrently.
@@ -114,6 +114,12 @@ int pfc_sample(const int64_t* labels, int64_t B, int64_t C,
  * compute must equal w_dtype and x_dtype (fp32, bf16 or fp16 operands; the
  *         contraction always accumulates in fp32).
  * s > 0 scale; margin m >= 0 (ArcFace: m < pi).
+ * tau     PFC* conflict threshold (Sec. 3.3.4, Eq. noise_filtering): a
+ *         non-target logit whose unmargined cosine exceeds tau is left out of
+ *         the row's denominator, and so gets no gradient in the backward of
+ *         this step; the target logit is never filtered.  tau >= 1 (or +inf)
+ *         is plain PFC; NaN is PFC_ERR_INVALID_ARG.  Rows whose label is
+ *         outside the shard have only negatives.
  * loss    float[1] out: (1/B) * sum over rows with an owned label of
  *         (lse_n - f_{n, y_n}); rows whose label is outside the shard add 0
  *         (their target term belongs to the owning shard).
@@ -125,8 +131,8 @@ int pfc_forward_loss(const void* X, int x_dtype, int64_t B, int64_t d,
                      const int32_t* active, const int32_t* n_active,
                      int64_t active_cap, const int32_t* labels_mapped,
                      int compute_dtype, float s, float m, int margin,
-                     float* loss, float* row_lse, void* ws, size_t ws_bytes,
-                     void* stream);
+                     float tau, float* loss, float* row_lse, void* ws,
+                     size_t ws_bytes, void* stream);
 
 /*
  * Stage 6: backward through the margin softmax and both normalisations, then

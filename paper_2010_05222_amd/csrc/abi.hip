@@ -193,8 +193,8 @@ int pfc_sample(const int64_t* labels, int64_t B, int64_t C, int64_t class_offset
 int pfc_forward_loss(const void* X, int x_dtype, int64_t B, int64_t d, const void* W,
                      int w_dtype, int64_t C, const int32_t* active, const int32_t* n_active,
                      int64_t active_cap, const int32_t* labels_mapped, int compute_dtype,
-                     float s, float m, int margin, float* loss, float* row_lse, void* ws,
-                     size_t ws_bytes, void* stream) {
+                     float s, float m, int margin, float tau, float* loss, float* row_lse,
+                     void* ws, size_t ws_bytes, void* stream) {
   if (!X || !W || !active || !n_active || !labels_mapped || !loss || !row_lse)
     return PFC_ERR_INVALID_ARG;
   int st = check_shape(B, d, C, compute_dtype);
@@ -203,6 +203,7 @@ int pfc_forward_loss(const void* X, int x_dtype, int64_t B, int64_t d, const voi
   if (active_cap < 1 || active_cap > C) return PFC_ERR_CAPACITY;
   st = check_hparams(s, m, margin);
   if (st != PFC_OK) return st;
+  if (tau != tau) return PFC_ERR_INVALID_ARG;   // NaN
   const WsLayout L = ws_layout(B, d, C, active_cap, compute_dtype);
   if (!ws || ws_bytes < L.bytes) return PFC_ERR_WORKSPACE;
   StepArgs a{};
@@ -221,6 +222,7 @@ int pfc_forward_loss(const void* X, int x_dtype, int64_t B, int64_t d, const voi
   a.s = s;
   a.m = m;
   a.margin = margin;
+  a.tau = tau;
   (void)hipGetLastError();
   const hipError_t e = launch_forward(a, step_ws(ws, L), (hipStream_t)stream);
   return e == hipSuccess ? PFC_OK : PFC_ERR_HIP;

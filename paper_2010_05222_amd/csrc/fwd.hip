@@ -145,16 +145,19 @@ __device__ __forceinline__ void fwd_compute(f32x16_t (&acc)[4][2], int wm, int w
 // 64 classes j = jb + 32 mb + 8 g + e (jb = first class of the lane's
 // pattern, e < 4); with the partner lane (half ^ 1) they are the row's 128
 // classes of one group.  Computes the base-2 logits f2 = s c log2 e (-inf at
-// the target, whose margined logit is merged separately, and past |S|), the
+// the target, whose margined logit is merged separately, past |S|, and with
+// FILT at a negative whose cosine exceeds tau: the PFC* conflict filter,
+// Sec. 3.3.4, Eq. noise_filtering, so E = 0 there and the backward's
+// coefficient too), the
 // group maximum m (the target's margined logit included), and writes
 // E = 2^(f2 - m) as fp16 to the LDS tile row trow (16-byte block b of the row
 // at position b ^ bsw).  Returns the pair's (m, sum of E and the target term).
-template <bool CHECK_J, bool CHECK_T>
+template <bool CHECK_J, bool CHECK_T, bool FILT>
 __device__ __forceinline__ void fwd_epilogue_rows(f32x16_t (&acc)[4][2], int nb, float ix,
                                                   const float* iwp, int K, int64_t jb, int tpos,
-                                                  const Margin& mg, uint16_t* trow, int bbase,
-                                                  int bsw, int half, float* mx_out, float* sm_out,
-                                                  float* tgt_out, float* tgtc_out) {
+                                                  const Margin& mg, float tau, uint16_t* trow,
+                                                  int bbase, int bsw, int half, float* mx_out,
+                                                  float* sm_out, float* tgt_out, float* tgtc_out) {
   const float s2 = mg.s * kLog2e;
   float mx = -INFINITY;
   float ct = 0.0f;
@@ -170,6 +173,7 @@ __device__ __forceinline__ void fwd_epilogue_rows(f32x16_t (&acc)[4][2], int nb,
         const float c = acc[mb][nb][4 * g + e] * ix * iwv[e];
         float f2 = c * s2;
         if (CHECK_J && jb + o + e >= K) f2 = -INFINITY;
+        if (FILT && c > tau) f2 = -INFINITY;   // PFC* drops the negative (not the target: below)
         if (CHECK_T && tpos == o + e) {
           ct = c;
           f2 = -INFINITY;   // the margined target logit is merged below
@@ -219,13 +223,13 @@ __device__ __forceinline__ void fwd_epilogue_rows(f32x16_t (&acc)[4][2], int nb,
 // cosine round(c * 32767) is stored once; the row's (max, sum) over the tile
 // is accumulated in base 2 from the fp32 logit s*c (the margined logit at
 // the target), and the target logit itself goes to tgt[n].
-template <typename Tag, int NK>
+template <typename Tag, int NK, bool FILT>
 __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
     const int32_t* __restrict__ active, const int32_t* __restrict__ n_active_p,
     const int32_t* __restrict__ yhat, const float* __restrict__ inv_x,
     float* __restrict__ inv_w, float* __restrict__ inv_w_max, int B, int64_t ld_cos,
-    int64_t n_ctiles, int n_rt, int64_t n_tiles, int64_t per_xcd, Margin mg,
+    int64_t n_ctiles, int n_rt, int64_t n_tiles, int64_t per_xcd, Margin mg, float tau,
     uint16_t* __restrict__ lbuf, float2* __restrict__ stats, float* __restrict__ tgt,
     float* __restrict__ tgtc, float* __restrict__ gmax, int64_t ld_g) {
   constexpr int D = NK * kFwdKC;
@@ -337,12 +341,13 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
     uint16_t* trow = fwd_tile_row(nl);
     float mx, sm;
     if (full && !__any(has_t))
-      fwd_epilogue_rows<false, false>(acc, nb, ixr[nb], iwp, K, jlo + 4 * half, tpos, mg, trow,
-                                      16 * wm, nl & 15, half, &mx, &sm, nullptr, nullptr);
+      fwd_epilogue_rows<false, false, FILT>(acc, nb, ixr[nb], iwp, K, jlo + 4 * half, tpos, mg,
+                                            tau, trow, 16 * wm, nl & 15, half, &mx, &sm, nullptr,
+                                            nullptr);
     else
-      fwd_epilogue_rows<true, true>(acc, nb, ixr[nb], iwp, K, jlo + 4 * half, tpos, mg, trow,
-                                    16 * wm, nl & 15, half, &mx, &sm, has_t ? tgt + n : nullptr,
-                                    has_t ? tgtc + n : nullptr);
+      fwd_epilogue_rows<true, true, FILT>(acc, nb, ixr[nb], iwp, K, jlo + 4 * half, tpos, mg,
+                                          tau, trow, 16 * wm, nl & 15, half, &mx, &sm,
+                                          has_t ? tgt + n : nullptr, has_t ? tgtc + n : nullptr);
     if (half == 0) {
       fRed[wm][nl] = make_float2(mx, sm);
       // reference of the row's 128-class group 2 ct + wm
@@ -396,13 +401,16 @@ __global__ void __launch_bounds__(256) k_lse16(const float2* __restrict__ stats,
 }
 
 // fp32 path (small problems): one thread per (row, class) dot product.
+// With tau < 1, a negative whose cosine exceeds tau is stored as -inf (PFC*,
+// Eq. noise_filtering): its logit and its coefficient in the backward are 0.
 __global__ void __launch_bounds__(256) k_fwd32(const float* __restrict__ X,
                                                const float* __restrict__ W,
                                                const int32_t* __restrict__ active,
                                                const int32_t* __restrict__ n_active_p,
+                                               const int32_t* __restrict__ yhat,
                                                const float* __restrict__ inv_x,
                                                const float* __restrict__ inv_w, int B, int d,
-                                               int64_t cap, int64_t ld_cos,
+                                               int64_t cap, int64_t ld_cos, float tau,
                                                float* __restrict__ cos32) {
   const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int n = blockIdx.y;
@@ -411,7 +419,8 @@ __global__ void __launch_bounds__(256) k_fwd32(const float* __restrict__ X,
   const float* w = W + (int64_t)active[j] * d;
   float acc = 0.0f;
   for (int i = 0; i < d; ++i) acc = fmaf(x[i], w[i], acc);
-  cos32[(int64_t)n * ld_cos + j] = acc * inv_x[n] * inv_w[j];
+  const float c = acc * inv_x[n] * inv_w[j];
+  cos32[(int64_t)n * ld_cos + j] = (tau < 1.0f && j != yhat[n] && c > tau) ? -INFINITY : c;
 }
 
 __global__ void __launch_bounds__(256) k_lse32(const float* __restrict__ cos32, int64_t ld_cos,
@@ -467,11 +476,18 @@ __global__ void __launch_bounds__(1024) k_loss(const float* __restrict__ loss_pa
 template <typename Tag, int NK>
 void launch_fwd16_nk(unsigned grid, hipStream_t stream, const StepArgs& a, const StepWs& w, int B,
                      int n_rt, int64_t n_tiles, int64_t per_xcd, const Margin& mg) {
-  hipLaunchKernelGGL((k_fwd16<Tag, NK>), dim3(grid), dim3(kFwdThreads), 0, stream,
-                     (const uint16_t*)a.X, (const uint16_t*)a.W, a.active, a.n_active,
-                     a.labels_mapped, w.inv_x, w.inv_w, w.inv_w_max, B, w.ld_cos, w.n_ctiles,
-                     n_rt, n_tiles, per_xcd, mg, (uint16_t*)w.lbuf, w.stats, w.tgt, w.tgtc,
-                     w.gmax, w.ld_g);
+  if (a.tau < 1.0f)
+    hipLaunchKernelGGL((k_fwd16<Tag, NK, true>), dim3(grid), dim3(kFwdThreads), 0, stream,
+                       (const uint16_t*)a.X, (const uint16_t*)a.W, a.active, a.n_active,
+                       a.labels_mapped, w.inv_x, w.inv_w, w.inv_w_max, B, w.ld_cos, w.n_ctiles,
+                       n_rt, n_tiles, per_xcd, mg, a.tau, (uint16_t*)w.lbuf, w.stats, w.tgt,
+                       w.tgtc, w.gmax, w.ld_g);
+  else
+    hipLaunchKernelGGL((k_fwd16<Tag, NK, false>), dim3(grid), dim3(kFwdThreads), 0, stream,
+                       (const uint16_t*)a.X, (const uint16_t*)a.W, a.active, a.n_active,
+                       a.labels_mapped, w.inv_x, w.inv_w, w.inv_w_max, B, w.ld_cos, w.n_ctiles,
+                       n_rt, n_tiles, per_xcd, mg, a.tau, (uint16_t*)w.lbuf, w.stats, w.tgt,
+                       w.tgtc, w.gmax, w.ld_g);
 }
 
 template <typename Tag>
@@ -495,8 +511,8 @@ hipError_t launch_forward(const StepArgs& a, const StepWs& w, hipStream_t stream
     dim3 grid((unsigned)ceil_div(a.cap, 256), (unsigned)B);
     timing_start(2, stream);
     hipLaunchKernelGGL(k_fwd32, grid, dim3(256), 0, stream, (const float*)a.X,
-                       (const float*)a.W, a.active, a.n_active, w.inv_x, w.inv_w, B, d, a.cap,
-                       w.ld_cos, (float*)w.lbuf);
+                       (const float*)a.W, a.active, a.n_active, a.labels_mapped, w.inv_x,
+                       w.inv_w, B, d, a.cap, w.ld_cos, a.tau, (float*)w.lbuf);
     timing_stop(2, stream);
     timing_start(3, stream);
     hipLaunchKernelGGL(k_lse32, dim3((unsigned)ceil_div(B, 4)), dim3(256), 0, stream,

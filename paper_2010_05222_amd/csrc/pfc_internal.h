@@ -111,6 +111,7 @@ struct StepArgs {
   int dtype;      // pfc_dtype of X, W and the compute
   float s, m;
   int margin;     // pfc_margin
+  float tau;      // PFC* conflict threshold (forward); >= 1: no filtering
   float lr, mu;
 };
 

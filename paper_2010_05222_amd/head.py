@@ -31,16 +31,22 @@ def _require(t, dtype, shape, name, device):
 
 
 class PfcShard:
-    """One GPU's class shard [class_offset, class_offset + C) of a PFC head."""
+    """One GPU's class shard [class_offset, class_offset + C) of a PFC head.
+
+    tau: threshold of the PFC* conflict filter (a negative logit whose
+    unmargined cosine exceeds tau leaves the row's denominator); None, or any
+    tau >= 1, is plain PFC.
+    """
 
     def __init__(self, B, d, C, r, dtype="bf16", class_offset=0, s=64.0, m=0.5,
-                 margin="arcface", lr=0.1, mu=0.9, device="cuda:0"):
+                 margin="arcface", lr=0.1, mu=0.9, device="cuda:0", tau=None):
         self.B, self.d, self.C, self.r = int(B), int(d), int(C), float(r)
         self.class_offset = int(class_offset)
         self.dtype_name = dtype
         self.tdtype, self.code = DTYPES[dtype]
         self.s, self.m, self.margin = float(s), float(m), MARGINS[margin]
         self.lr, self.mu = float(lr), float(mu)
+        self.tau = None if tau is None else float(tau)
         self.device = torch.device(device)
         self.ws_bytes, self.cap = abi.pfc_workspace_bytes(self.B, self.d, self.C, self.r, self.code)
         dev = self.device
@@ -67,8 +73,8 @@ class PfcShard:
         abi.pfc_forward_loss(_ptr(X), self.code, self.B, self.d, _ptr(W), self.code, self.C,
                              _ptr(self.active), _ptr(self.n_active), self.cap,
                              _ptr(self.labels_mapped), self.code, self.s, self.m, self.margin,
-                             _ptr(self.loss), _ptr(self.row_lse), _ptr(self.ws), self.ws_bytes,
-                             self._stream())
+                             2.0 if self.tau is None else self.tau, _ptr(self.loss),
+                             _ptr(self.row_lse), _ptr(self.ws), self.ws_bytes, self._stream())
 
     def backward(self, X, W, M, W_master=None, row_lse=None):
         _require(X, self.tdtype, (self.B, self.d), "X", self.device)

@@ -47,7 +47,7 @@ _lib.pfc_workspace_bytes.restype = _int
 _lib.pfc_sample.argtypes = [_vp, _i64, _i64, _i64, _dbl, _u64, _vp, _i64, _vp, _vp, _vp, _sz, _vp]
 _lib.pfc_sample.restype = _int
 _lib.pfc_forward_loss.argtypes = [_vp, _int, _i64, _i64, _vp, _int, _i64, _vp, _vp, _i64, _vp,
-                                  _int, _flt, _flt, _int, _vp, _vp, _vp, _sz, _vp]
+                                  _int, _flt, _flt, _int, _flt, _vp, _vp, _vp, _sz, _vp]
 _lib.pfc_forward_loss.restype = _int
 _lib.pfc_backward_update.argtypes = [_vp, _int, _i64, _i64, _vp, _int, _vp, _vp, _i64, _vp, _vp,
                                      _i64, _vp, _int, _flt, _flt, _int, _vp, _flt, _flt, _vp,
@@ -91,11 +91,11 @@ def pfc_sample(labels, B, C, class_offset, r, seed, active, active_cap, n_active
 
 
 def pfc_forward_loss(X, x_dtype, B, d, W, w_dtype, C, active, n_active, active_cap,
-                     labels_mapped, compute_dtype, s, m, margin, loss, row_lse, ws, ws_bytes,
+                     labels_mapped, compute_dtype, s, m, margin, tau, loss, row_lse, ws, ws_bytes,
                      stream):
     _check(_lib.pfc_forward_loss(X, x_dtype, B, d, W, w_dtype, C, active, n_active, active_cap,
-                                 labels_mapped, compute_dtype, s, m, margin, loss, row_lse, ws,
-                                 ws_bytes, stream), "pfc_forward_loss")
+                                 labels_mapped, compute_dtype, s, m, margin, tau, loss, row_lse,
+                                 ws, ws_bytes, stream), "pfc_forward_loss")
 
 
 def pfc_backward_update(X, x_dtype, B, d, W, w_dtype, W_master, momentum, C, active, n_active,

@@ -107,13 +107,14 @@ def test_sample_rejects_before_launch(kw, status):
 def _fwd_args(**kw):
     a = dict(X=FAKE, x_dtype=1, B=16, d=128, W=FAKE, w_dtype=1, C=1000, active=FAKE,
              n_active=FAKE, active_cap=100, labels_mapped=FAKE, compute_dtype=1, s=64.0, m=0.5,
-             margin=1, loss=FAKE, row_lse=FAKE, ws=FAKE, ws_bytes=1 << 40, stream=0)
+             margin=1, tau=2.0, loss=FAKE, row_lse=FAKE, ws=FAKE, ws_bytes=1 << 40, stream=0)
     a.update(kw)
     return a
 
 
 @pytest.mark.parametrize("kw,status", [
     (dict(X=0), pfc.PFC_ERR_INVALID_ARG),
+    (dict(tau=float("nan")), pfc.PFC_ERR_INVALID_ARG),
     (dict(s=0.0), pfc.PFC_ERR_INVALID_ARG),
     (dict(s=float("inf")), pfc.PFC_ERR_INVALID_ARG),
     (dict(m=-0.1), pfc.PFC_ERR_INVALID_ARG),

@@ -24,20 +24,20 @@ def dev():
     return torch.device("cuda:0")
 
 
-def _shard(B, d, C, r, dtype, margin, m, class_offset=0, dev="cuda:0"):
+def _shard(B, d, C, r, dtype, margin, m, class_offset=0, dev="cuda:0", tau=None):
     from paper_2010_05222_amd.head import PfcShard
     return PfcShard(B, d, C, r, dtype=dtype, class_offset=class_offset, s=64.0, m=m,
-                    margin=margin, lr=0.1, mu=0.9, device=dev)
+                    margin=margin, lr=0.1, mu=0.9, device=dev, tau=tau)
 
 
 def _case(dev, B, d, C, r, dtype, margin, m, seed, class_offset=0, label_span=None,
-          random_m=True, master=False, labels=None):
+          random_m=True, master=False, labels=None, tau=None, conflicts=0):
     from _gpu_util import make_problem, run_and_compare
     print(f"\ncase B={B} d={d} C={C} r={r} dtype={dtype} margin={margin} seed={seed} "
-          f"offset={class_offset} master={master}", flush=True)
+          f"offset={class_offset} master={master} tau={tau}", flush=True)
     Xd, Wd, Md, Pd, Ld = make_problem(B, d, C, dtype, seed, class_offset, label_span, random_m,
-                                      master, labels, dev)
-    shard = _shard(B, d, C, r, dtype, margin, m, class_offset, dev)
+                                      master, labels, dev, conflicts)
+    shard = _shard(B, d, C, r, dtype, margin, m, class_offset, dev, tau)
     out = run_and_compare(shard, Xd, Wd, Md, Pd, Ld, seed, margin)
     print(out, flush=True)
     return out
@@ -153,3 +153,43 @@ def test_many_rows_per_class(dev):
     rng = np.random.default_rng(13)
     labels = rng.choice(np.array([5, 6, 100]), size=2400)
     _case(dev, 2400, 128, 3000, 0.1, "bf16", "arcface", 0.5, seed=13, labels=labels)
+
+
+# PFC* conflict filter (Sec. 3.3.4, Eq. noise_filtering): some rows sit near
+# the centre of another row's class, so their cosine to that (active)
+# negative is ~0.9 > tau and the logit leaves the row's denominator.
+@pytest.mark.parametrize("dtype,margin,m", [("bf16", "arcface", 0.5), ("f16", "cosface", 0.4)])
+def test_conflict_filter(dev, dtype, margin, m):
+    out = _case(dev, 300, 512, 20000, 0.1, dtype, margin, m, seed=14, tau=0.4, conflicts=3)
+    assert out["n_filtered"] >= 50
+
+
+def test_conflict_filter_ragged_and_unowned(dev):
+    out = _case(dev, 100, 256, 5000, 0.2, "bf16", "arcface", 0.5, seed=15, class_offset=1000,
+                label_span=(1000, 6500), tau=0.4, conflicts=2)
+    assert out["n_filtered"] >= 20
+
+
+def test_conflict_filter_fp32(dev):
+    out = _case(dev, 64, 128, 2000, 0.1, "f32", "cosface", 0.4, seed=16, tau=0.4, conflicts=2)
+    assert out["n_filtered"] >= 20
+
+
+def test_conflict_filter_full_softmax(dev):
+    """FC*-1.0: the filter at r = 1."""
+    out = _case(dev, 64, 128, 2000, 1.0, "bf16", "arcface", 0.5, seed=17, tau=0.4, conflicts=2)
+    assert out["K"] == 2000 and out["n_filtered"] >= 20
+
+
+def test_tau_at_least_one_is_pfc(dev):
+    """tau >= 1 runs the unfiltered kernels: bit-identical to no filter."""
+    from _gpu_util import make_problem
+    outs = []
+    for tau in (None, 1.0):
+        Xd, Wd, Md, Pd, Ld = make_problem(200, 256, 6000, "bf16", 18, device=dev, conflicts=2)
+        shard = _shard(200, 256, 6000, 0.1, "bf16", "arcface", 0.5, dev=dev, tau=tau)
+        shard.step(Xd, Ld, Wd, Md, 18)
+        torch.cuda.synchronize()
+        outs.append((shard.loss.clone(), shard.dX.clone(), Wd.clone(), Md.clone()))
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
