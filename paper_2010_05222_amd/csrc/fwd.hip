@@ -5,14 +5,16 @@
 //
 // 16-bit path: one MFMA GEMM workgroup per 256 active classes (MFMA M) x 128
 // batch rows (MFMA N), d streamed in 32-wide chunks through a three-stage
-// direct-to-LDS ring; two workgroups share a CU.  Classes sit on the MFMA M axis so that each lane holds
-// one batch row and 64 of its classes: the row max / sum-exp of the
-// epilogue is mostly in-register.  The epilogue scales by 1/||x_n|| and
-// 1/||w_j||, quantises the unmargined cosine to 16-bit fixed point (the
-// logits' only write: the tile is assembled in the idle LDS ring and stored
-// as whole rows), applies the margin at the target, and emits one
-// (max, sum exp) pair per (row, class tile).  A small kernel merges the pairs
-// into lse_n and the loss.
+// direct-to-LDS ring; two workgroups share a CU.  Classes sit on the MFMA M
+// axis so that each lane holds one batch row and 64 of its classes: the row
+// max / sum-exp of the epilogue is mostly in-register.  The epilogue scales
+// by 1/||x_n|| and 1/||w_j|| (the class-row norms are summed from the
+// contraction's own class fragments), applies the margin at the target and
+// the optional PFC* conflict filter, and writes each logit once, as its fp16
+// softmax numerator E = 2^(f - m) relative to the maximum m of its row and
+// 128-class group (the tile is assembled in the idle LDS ring and stored as
+// whole rows), with one (max, sum E) pair per (row, class tile).  A small
+// kernel merges the pairs into lse_n and the loss.
 #include "pfc_gemm.h"
 
 namespace pfc {
@@ -219,10 +221,11 @@ __device__ __forceinline__ void fwd_epilogue_rows(f32x16_t (&acc)[4][2], int nb,
 }
 
 // Tile: 256 active classes x 128 batch rows, the whole of d (= 32 * NK).
-// Epilogue, per (row, class): c = acc / (||x|| ||w||); the 16-bit fixed-point
-// cosine round(c * 32767) is stored once; the row's (max, sum) over the tile
-// is accumulated in base 2 from the fp32 logit s*c (the margined logit at
-// the target), and the target logit itself goes to tgt[n].
+// Epilogue, per (row, class): c = acc / (||x|| ||w||) and the base-2 logit
+// s c log2 e (the margined logit at the target, which also goes to tgt[n],
+// its cosine to tgtc[n]); per (row, 128-class group) the maximum m, written
+// to gmax, and E = 2^(f - m) in fp16; per (row, class tile) the pair
+// (max, sum E), merged by k_lse16.
 template <typename Tag, int NK, bool FILT>
 __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
@@ -322,7 +325,7 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
     }
   }
 
-  // ---- epilogue.  The quantised 256-class x 128-row cosine tile is
+  // ---- epilogue.  The fp16 256-class x 128-row tile of E values is
   // assembled in the (now idle) LDS ring (rows of 512 B, 16-byte block b of
   // row r at position b ^ (r & 15): conflict-free writes from the MFMA layout
   // and reads along rows), then written out in whole rows.
