@@ -37,7 +37,8 @@ def log(msg):
 def kernel_source_sha(name):
     path = os.path.join(ROOT, "paper_2010_05222_amd", "csrc", KERNEL_SOURCES[name])
     h = hashlib.sha256()
-    for p in (path, os.path.join(ROOT, "paper_2010_05222_amd", "csrc", "pfc_device.h")):
+    for p in [path] + [os.path.join(ROOT, "paper_2010_05222_amd", "csrc", f)
+                       for f in ("pfc_device.h", "pfc_gemm.h")]:
         with open(p, "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
