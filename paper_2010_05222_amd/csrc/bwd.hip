@@ -414,39 +414,49 @@ __global__ void __launch_bounds__(256) k_dx_final(
     const int32_t* __restrict__ yhat, const float* __restrict__ row_lse,
     const float* __restrict__ inv_x, const float* __restrict__ inv_w,
     const float* __restrict__ tgtc, int B, int d, Margin mg, float sB, float* __restrict__ dX) {
-  constexpr int kMaxPer = 8;  // d <= 512
-  const int lane = threadIdx.x & 63;
-  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (n >= B) return;
+  // One workgroup per batch row, thread t owns entries t and t + 256 (d <= 512):
+  // the split partials are independent loads, summed in split order.
+  __shared__ float red[4];
+  const int n = blockIdx.x;
+  const int t = threadIdx.x, lane = t & 63;
   const float ix = inv_x[n];
   const int yt = yhat[n];
-  const float lse = row_lse[n];
   float gt = 0.0f;
   int64_t wbase = 0;
   if (yt >= 0) {
-    gt = target_coef(mg, tgtc[n], lse) * inv_w[yt];
+    gt = target_coef(mg, tgtc[n], row_lse[n]) * inv_w[yt];
     wbase = (int64_t)active[yt] * d;
   }
-  float v[kMaxPer], xh[kMaxPer];
+  float v[2] = {0.0f, 0.0f}, xh[2] = {0.0f, 0.0f};
   float dot = 0.0f;
 #pragma unroll
-  for (int k = 0; k < kMaxPer; ++k) {
-    const int i = lane + 64 * k;
-    v[k] = 0.0f;
-    xh[k] = 0.0f;
-    if (i < d) {
-      float sum = 0.0f;
-      for (int s = 0; s < n_split; ++s) sum += dx_part[((int64_t)s * B + n) * d + i];
-      if (yt >= 0) sum = fmaf(gt, load16<Tag>(W, wbase + i), sum);
-      v[k] = sB * sum;
-      xh[k] = load16<Tag>(X, (int64_t)n * d + i) * ix;
-      dot = fmaf(xh[k], v[k], dot);
+  for (int k = 0; k < 2; ++k) {
+    const int i = t + 256 * k;
+    if (i >= d) continue;
+    const float* p = dx_part + (int64_t)n * d + i;
+    const int64_t stride = (int64_t)B * d;
+    float sum = 0.0f;
+    int s = 0;
+    for (; s + 8 <= n_split; s += 8) {
+      float q[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) q[u] = p[(int64_t)(s + u) * stride];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) sum += q[u];
     }
+    for (; s < n_split; ++s) sum += p[(int64_t)s * stride];
+    if (yt >= 0) sum = fmaf(gt, load16<Tag>(W, wbase + i), sum);
+    v[k] = sB * sum;
+    xh[k] = load16<Tag>(X, (int64_t)n * d + i) * ix;
+    dot = fmaf(xh[k], v[k], dot);
   }
   dot = wave_sum(dot);
+  if (lane == 0) red[t >> 6] = dot;
+  __syncthreads();
+  dot = red[0] + red[1] + red[2] + red[3];
 #pragma unroll
-  for (int k = 0; k < kMaxPer; ++k) {
-    const int i = lane + 64 * k;
+  for (int k = 0; k < 2; ++k) {
+    const int i = t + 256 * k;
     if (i < d) dX[(int64_t)n * d + i] = ix * (v[k] - xh[k] * dot);
   }
 }
@@ -1055,7 +1065,7 @@ void launch_bwd16(const StepArgs& a, const StepWs& w, const Margin& mg, float sB
                      n_tiles, per_xcd, w.dx_part);
   timing_stop(4, stream);
   timing_start(5, stream);
-  hipLaunchKernelGGL(k_dx_final<Tag>, dim3((unsigned)ceil_div(B, 4)), dim3(256), 0, stream,
+  hipLaunchKernelGGL(k_dx_final<Tag>, dim3((unsigned)B), dim3(256), 0, stream,
                      w.dx_part, w.n_split, a.X, a.W, a.active, a.labels_mapped, a.row_lse,
                      w.inv_x, w.inv_w, w.tgtc, B, (int)a.d, mg, sB, a.dX);
   timing_stop(5, stream);

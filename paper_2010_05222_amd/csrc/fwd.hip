@@ -376,28 +376,39 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
   }
 }
 
-// Merge the per-tile (max, sum) pairs of a row: lse_n, and the row's loss term.
+// Merge the per-tile (max, sum) pairs of a row: lse_n, and the row's loss
+// term.  One workgroup per row: the row maximum M over the tiles, then
+// sum_tiles sum_t * 2^(max_t - M), each a fixed-order reduction.
 __global__ void __launch_bounds__(256) k_lse16(const float2* __restrict__ stats, int64_t n_ctiles,
                                                const int32_t* __restrict__ n_active_p,
                                                const int32_t* __restrict__ yhat,
                                                const float* __restrict__ tgt, int B,
                                                float* __restrict__ row_lse,
                                                float* __restrict__ loss_part) {
-  const int lane = threadIdx.x & 63;
-  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (n >= B) return;
+  __shared__ float red[4];
+  const int n = blockIdx.x;
+  const int t = threadIdx.x, lane = t & 63;
   const int64_t nct = ceil_div((int64_t)*n_active_p, (int64_t)kFwdBM);
-  float2 acc = make_float2(-INFINITY, 0.0f);
-  for (int64_t c = lane; c < nct; c += 64) acc = lse_merge2(acc, stats[(int64_t)n * n_ctiles + c]);
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    float2 o;
-    o.x = __shfl_xor(acc.x, off, 64);
-    o.y = __shfl_xor(acc.y, off, 64);
-    acc = lse_merge2(acc, o);
-  }
-  if (lane == 0) {
-    const float lse = (acc.x + log2f(acc.y)) * 0.6931471805599453f;
+  const float2* row = stats + (int64_t)n * n_ctiles;
+  float mx = -INFINITY;
+  for (int64_t c = t; c < nct; c += 256) mx = fmaxf(mx, row[c].x);
+  mx = wave_max(mx);
+  if (lane == 0) red[t >> 6] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  __syncthreads();
+  float sm = 0.0f;
+  if (mx != -INFINITY)
+    for (int64_t c = t; c < nct; c += 256) {
+      const float2 v = row[c];
+      sm += v.y * exp2f(v.x - mx);
+    }
+  sm = wave_sum(sm);
+  if (lane == 0) red[t >> 6] = sm;
+  __syncthreads();
+  if (t == 0) {
+    sm = (red[0] + red[1]) + (red[2] + red[3]);
+    const float lse = (mx + log2f(sm)) * 0.6931471805599453f;
     row_lse[n] = lse;
     loss_part[n] = yhat[n] >= 0 ? lse - tgt[n] : 0.0f;
   }
@@ -533,7 +544,7 @@ hipError_t launch_forward(const StepArgs& a, const StepWs& w, hipStream_t stream
       launch_fwd16<F16Tag>(d, grid, stream, a, w, B, n_rt, n_tiles, per_xcd, mg);
     timing_stop(2, stream);
     timing_start(3, stream);
-    hipLaunchKernelGGL(k_lse16, dim3((unsigned)ceil_div(B, 4)), dim3(256), 0, stream, w.stats,
+    hipLaunchKernelGGL(k_lse16, dim3((unsigned)B), dim3(256), 0, stream, w.stats,
                        w.n_ctiles, a.n_active, a.labels_mapped, w.tgt, B, a.row_lse_out,
                        w.loss_part);
   }
