@@ -473,7 +473,7 @@ __global__ void __launch_bounds__(256) k_dx_final(
 // chunk c + 1 produced, chunk c contracted.  The second k-step of chunk c is
 // contracted at the start of the next chunk, from fragments read in this
 // one, so that the matrix pipe is busy while the next fragments arrive.
-template <typename Tag, int WI>
+template <typename Tag, int WI, bool MASTER>
 __global__ void __launch_bounds__(256) k_dw16(
     const uint16_t* __restrict__ xbT, int64_t ld_xt, const void* __restrict__ X,
     uint16_t* __restrict__ W, float* __restrict__ W_master, float* __restrict__ M,
@@ -757,7 +757,7 @@ __global__ void __launch_bounds__(256) k_dw16(
 
   struct Rows {
     uint2 wv[RPW][NH];   // four 16-bit weights
-    float4 mv[RPW][NH], pv[RPW][NH];
+    float4 mv[RPW][NH], pv[MASTER ? RPW : 1][NH];
     int64_t rowa[RPW];
     float iwr[RPW];
     bool rv[RPW];
@@ -773,11 +773,12 @@ __global__ void __launch_bounds__(256) k_dw16(
       for (int h = 0; h < NH; ++h) {
         const int64_t off = bt.rowa[k] * D + 256 * h + 4 * lane;
         bt.wv[k][h] = make_uint2(0, 0);
-        bt.mv[k][h] = bt.pv[k][h] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        bt.mv[k][h] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        if constexpr (MASTER) bt.pv[k][h] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
         if (bt.rv[k]) {
           bt.wv[k][h] = *reinterpret_cast<const uint2*>(W + off);
           bt.mv[k][h] = *reinterpret_cast<const float4*>(M + off);
-          if (W_master) bt.pv[k][h] = *reinterpret_cast<const float4*>(W_master + off);
+          if constexpr (MASTER) bt.pv[k][h] = *reinterpret_cast<const float4*>(W_master + off);
         }
       }
     }
@@ -840,13 +841,19 @@ __global__ void __launch_bounds__(256) k_dw16(
         const float wo[4] = {wf[h].x, wf[h].y, wf[h].z, wf[h].w};
         const float go[4] = {gv[h].x, gv[h].y, gv[h].z, gv[h].w};
         float mo[4] = {bt.mv[k][h].x, bt.mv[k][h].y, bt.mv[k][h].z, bt.mv[k][h].w};
-        float po[4] = {bt.pv[k][h].x, bt.pv[k][h].y, bt.pv[k][h].z, bt.pv[k][h].w};
+        float po[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+        if constexpr (MASTER) {
+          po[0] = bt.pv[k][h].x;
+          po[1] = bt.pv[k][h].y;
+          po[2] = bt.pv[k][h].z;
+          po[3] = bt.pv[k][h].w;
+        }
         float wn[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const float gr = bt.iwr[k] * (go[e] - wo[e] * bt.iwr[k] * dot);
           mo[e] = mu * mo[e] + gr;
-          if (W_master) {
+          if constexpr (MASTER) {
             po[e] = po[e] - lr * mo[e];
             wn[e] = po[e];
           } else {
@@ -854,7 +861,7 @@ __global__ void __launch_bounds__(256) k_dw16(
           }
         }
         *reinterpret_cast<float4*>(M + off) = make_float4(mo[0], mo[1], mo[2], mo[3]);
-        if (W_master)
+        if constexpr (MASTER)
           *reinterpret_cast<float4*>(W_master + off) = make_float4(po[0], po[1], po[2], po[3]);
         uint2 o;
         o.x = pack2<Tag>(wn[0], wn[1]);
@@ -864,8 +871,11 @@ __global__ void __launch_bounds__(256) k_dw16(
     }
   };
 
-  Rows bat;
-  load_rows(bat, 0);
+  // Without a master copy the rows of the next pass are requested before
+  // this pass is computed (two row sets in registers).
+  constexpr int NSET = MASTER ? 1 : 2;
+  Rows bat[NSET];
+  load_rows(bat[0], 0);
   stage_barrier();  // every wave's fragment reads of the stage arrays are done
   // Target terms: wave w lists, in row order, the rows n of its quarter of the
   // batch whose label is one of the tile's classes (entry n * 128 + class
@@ -897,16 +907,14 @@ __global__ void __launch_bounds__(256) k_dw16(
     hn[w] = __builtin_amdgcn_readfirstlane(hit_n[w]);
     hit_scan |= hn[w] > kHitCap;
   }
-  for (int p = 0; p < 4; ++p) {
-    if (p > 0) {
-      load_rows(bat, p);
+  static_for<0, 4>([&](auto pp) {
+    constexpr int p = decltype(pp)::value;
+    if constexpr (NSET == 2 && p + 1 < 4) load_rows(bat[(p + 1) % NSET], p + 1);
+    if constexpr (p > 0) {
+      if constexpr (NSET == 1) load_rows(bat[0], p);
       wait_lgkm0();
       stage_barrier();  // the stage arrays are rewritten by this pass
-      switch (p) {
-        case 1: park(std::integral_constant<int, 1>{}); break;
-        case 2: park(std::integral_constant<int, 2>{}); break;
-        default: park(std::integral_constant<int, 3>{}); break;
-      }
+      park(pp);
       wait_lgkm0();
       stage_barrier();
     }
@@ -932,8 +940,8 @@ __global__ void __launch_bounds__(256) k_dw16(
         }
       }
     }
-    update_rows(bat);
-  }
+    update_rows(bat[p % NSET]);
+  });
 }
 
 // ---------------------------------------------------------------- fp32 path
@@ -1070,11 +1078,18 @@ void launch_bwd16(const StepArgs& a, const StepWs& w, const Margin& mg, float sB
                      w.inv_x, w.inv_w, w.tgtc, B, (int)a.d, mg, sB, a.dX);
   timing_stop(5, stream);
   timing_start(6, stream);
-  hipLaunchKernelGGL((k_dw16<Tag, WI>), dim3((unsigned)ceil_div(a.cap, kDwCls)), dim3(256),
-                     0, stream, (const uint16_t*)w.xbT, w.ld_xt, a.X, (uint16_t*)a.W, a.W_master, a.M,
-                     a.active, a.n_active, a.labels_mapped, a.row_lse, w.inv_x, w.inv_w,
-                     w.tgtc, (const uint16_t*)w.lbuf, w.ld_cos, w.gscale, w.ld_g, B, mg, sB, a.lr,
-                     a.mu);
+  if (a.W_master)
+    hipLaunchKernelGGL((k_dw16<Tag, WI, true>), dim3((unsigned)ceil_div(a.cap, kDwCls)), dim3(256),
+                       0, stream, (const uint16_t*)w.xbT, w.ld_xt, a.X, (uint16_t*)a.W, a.W_master,
+                       a.M, a.active, a.n_active, a.labels_mapped, a.row_lse, w.inv_x, w.inv_w,
+                       w.tgtc, (const uint16_t*)w.lbuf, w.ld_cos, w.gscale, w.ld_g, B, mg, sB, a.lr,
+                       a.mu);
+  else
+    hipLaunchKernelGGL((k_dw16<Tag, WI, false>), dim3((unsigned)ceil_div(a.cap, kDwCls)), dim3(256),
+                       0, stream, (const uint16_t*)w.xbT, w.ld_xt, a.X, (uint16_t*)a.W, a.W_master,
+                       a.M, a.active, a.n_active, a.labels_mapped, a.row_lse, w.inv_x, w.inv_w,
+                       w.tgtc, (const uint16_t*)w.lbuf, w.ld_cos, w.gscale, w.ld_g, B, mg, sB, a.lr,
+                       a.mu);
   timing_stop(6, stream);
 }
 
