@@ -36,7 +36,7 @@ def dev():
     return torch.device("cuda:0")
 
 
-@pytest.mark.parametrize("name", ["massive", "one_shard"])
+@pytest.mark.parametrize("name", ["massive", "one_shard", "zipf", "full_softmax"])
 def test_full_size_step(dev, name):
     from _gpu_util import MAX_ABS, REL_ROW, row_rel_err
     from paper_2010_05222_amd.head import PfcShard
