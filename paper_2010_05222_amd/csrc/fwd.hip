@@ -334,27 +334,47 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
   const int64_t jlo = j0 + 128 * wm;
   const bool full = jlo + 128 <= (int64_t)K;   // wave-uniform: no class past |S|
   const float* iwp = fIw + 128 * wm + 4 * half;
+  // Rows of the lane, and whether the lane's class pattern holds a row's target.
+  int tpos[2];
+  bool has_t[2];
 #pragma unroll
   for (int nb = 0; nb < 2; ++nb) {
+    const int yh = yhr[nb];
+    tpos[nb] = yh - (int)(jlo + 4 * half);   // target's offset in this lane's class pattern
+    has_t[nb] = yh >= jlo && yh < jlo + 128 && ((tpos[nb] & 4) == 0);
+  }
+  auto finish = [&](int nb, float mx, float sm) __attribute__((always_inline)) {
     const int nl = 64 * wn + 32 * nb + l32;
     const int n = n0 + nl;
-    const int yh = yhr[nb];
-    const int tpos = yh - (int)(jlo + 4 * half);   // target's offset in this lane's class pattern
-    const bool has_t = yh >= jlo && yh < jlo + 128 && ((tpos & 4) == 0);
-    uint16_t* trow = fwd_tile_row(nl);
-    float mx, sm;
-    if (full && !__any(has_t))
-      fwd_epilogue_rows<false, false, FILT>(acc, nb, ixr[nb], iwp, K, jlo + 4 * half, tpos, mg,
-                                            tau, trow, 16 * wm, nl & 15, half, &mx, &sm, nullptr,
-                                            nullptr);
-    else
-      fwd_epilogue_rows<true, true, FILT>(acc, nb, ixr[nb], iwp, K, jlo + 4 * half, tpos, mg,
-                                          tau, trow, 16 * wm, nl & 15, half, &mx, &sm,
-                                          has_t ? tgt + n : nullptr, has_t ? tgtc + n : nullptr);
     if (half == 0) {
       fRed[wm][nl] = make_float2(mx, sm);
       // reference of the row's 128-class group 2 ct + wm
       if (n < B) gmax[(2 * ct + wm) * ld_g + n] = mx == -INFINITY ? 0.0f : mx;
+    }
+  };
+  // Two separate paths over both row blocks, so that the masking work of
+  // the checked one (classes past |S|, targets) stays out of the common one.
+  if (full && !__any(has_t[0] || has_t[1])) {
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      const int nl = 64 * wn + 32 * nb + l32;
+      float mx, sm;
+      fwd_epilogue_rows<false, false, FILT>(acc, nb, ixr[nb], iwp, K, jlo + 4 * half, tpos[nb],
+                                            mg, tau, fwd_tile_row(nl), 16 * wm, nl & 15, half,
+                                            &mx, &sm, nullptr, nullptr);
+      finish(nb, mx, sm);
+    }
+  } else {
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      const int nl = 64 * wn + 32 * nb + l32;
+      const int n = n0 + nl;
+      float mx, sm;
+      fwd_epilogue_rows<true, true, FILT>(acc, nb, ixr[nb], iwp, K, jlo + 4 * half, tpos[nb], mg,
+                                          tau, fwd_tile_row(nl), 16 * wm, nl & 15, half, &mx,
+                                          &sm, has_t[nb] ? tgt + n : nullptr,
+                                          has_t[nb] ? tgtc + n : nullptr);
+      finish(nb, mx, sm);
     }
   }
   wait_lgkm0();
