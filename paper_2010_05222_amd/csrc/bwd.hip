@@ -552,13 +552,13 @@ __global__ void __launch_bounds__(256) k_dw16(
   // X^T: block cc of the transposed batch ([d][32], contiguous); load v of this
   // wave covers d rows 16 m .. 16 m + 15 (m = wave XDMA + v), 4 pieces each;
   // lane l fills piece l & 3 of row 16 m + l / 4 with source piece
-  // (l & 3) ^ ((row >> 1) & 3).
+  // (l & 3) ^ ((row >> 2) & 3).
   auto dma_x_piece = [&](auto st, int c, int v) __attribute__((always_inline)) {
     constexpr int S = decltype(st)::value;
     const int cc = c < n_chunks ? c : n_chunks - 1;
     const int m = wave * XDMA + v;
     const int i = 16 * m + (lane >> 2);
-    const int piece = (lane & 3) ^ ((i >> 1) & 3);
+    const int piece = (lane & 3) ^ ((i >> 2) & 3);
     dma16(xbT + ((int64_t)cc * D + i) * kBwKC + 8 * piece, dw_x<S>() + 512 * m);
   };
   auto dma_x = [&](auto st, int c) __attribute__((always_inline)) {
@@ -608,13 +608,13 @@ __global__ void __launch_bounds__(256) k_dw16(
     }
     const uint4 o = pack8<Bf16Tag>(v);
     const int cl = pcls[u];
-    ds_write_128<0>(lds_addr(dw_g<S>()) + cl * kBwKC * 2 + 16 * (prg[u] ^ ((cl >> 1) & 3)),
+    ds_write_128<0>(lds_addr(dw_g<S>()) + cl * kBwKC * 2 + 16 * (prg[u] ^ ((cl >> 2) & 3)),
                     u32x4_t{o.x & gmask, o.y & gmask, o.z & gmask, o.w & gmask});
   };
 
   // Fragment byte offsets: operand row (d entry or class) 32 q + l32 of the
-  // wave's block, chunk 2 kk + half stored at chunk ^ ((row >> 1) & 3).
-  const int sw = (l32 >> 1) & 3;
+  // wave's block, chunk 2 kk + half stored at chunk ^ ((row >> 2) & 3).
+  const int sw = (l32 >> 2) & 3;
   const uint32_t a_lane0 = (uint32_t)((DW * wave + l32) * kBwKC * 2 + 16 * ((0 + half) ^ sw));
   const uint32_t a_lane1 = (uint32_t)((DW * wave + l32) * kBwKC * 2 + 16 * ((2 + half) ^ sw));
   const uint32_t b_lane0 = (uint32_t)(l32 * kBwKC * 2 + 16 * ((0 + half) ^ sw));

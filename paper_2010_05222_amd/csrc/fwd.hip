@@ -34,8 +34,8 @@ constexpr float kEpsNormW = 1e-12f;  // ||w|| floor of the normalisation
 // One array per stage, so the compiler can keep the direct-to-LDS loads of
 // later stages in flight while a stage is read.  Row r of a stage holds 32
 // elements (64 B) as four 16-byte chunks; chunk c is stored at position
-// c ^ ((r >> 1) & 3), so the eight lanes of a 16-byte LDS read that address
-// eight consecutive rows hit distinct banks.
+// c ^ ((r >> 2) & 3), so the sixteen lanes of a 16-byte LDS read that
+// address sixteen consecutive rows hit distinct banks (64 banks).
 __shared__ __attribute__((aligned(1024))) uint16_t fA0[kFwdStageA], fA1[kFwdStageA],
     fA2[kFwdStageA];
 __shared__ __attribute__((aligned(1024))) uint16_t fB0[kFwdStageB], fB1[kFwdStageB],
@@ -94,7 +94,7 @@ __device__ __forceinline__ float sumsq2(uint32_t v, float acc, Bf16Tag) {
 
 // Fragments of both 16-wide k-steps of a stage are requested first, then
 // consumed: lane l reads row 32 q + l % 32 of its operand block, chunk
-// 2 kk + l / 32 (stored at chunk ^ ((row >> 1) & 3)).  The class-operand
+// 2 kk + l / 32 (stored at chunk ^ ((row >> 2) & 3)).  The class-operand
 // fragments also feed the class-row norms: the wave with wn == kk adds the
 // squares of its k-step's fragments to wss[mb] (class row 128 wm + 32 mb +
 // l % 32, elements 8 (l / 32) .. + 7 of the k-step).
@@ -102,7 +102,7 @@ template <int S, typename Tag>
 __device__ __forceinline__ void fwd_compute(f32x16_t (&acc)[4][2], int wm, int wn, int lane,
                                             float (&wss)[4]) {
   const int r32 = lane & 31;
-  const int sw = (lane >> 1) & 3;
+  const int sw = (lane >> 2) & 3;
   const uint32_t arow = lds_addr(fwd_a<S>()) + (128 * wm + r32) * kFwdKC * 2;
   const uint32_t brow = lds_addr(fwd_b<S>()) + (64 * wn + r32) * kFwdKC * 2;
   u32x4_t af[2][4], bf[2][2];
@@ -253,7 +253,7 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
 
   // Per-lane source rows of the DMA segments; rows past the end are clamped
   // to a valid row (their results are masked in the epilogue).
-  const int cidx = (lane & 3) ^ ((lane >> 3) & 3);
+  const int cidx = (lane & 3) ^ ((lane >> 4) & 3);
   const uint16_t* ap[4];
   const uint16_t* bp[2];
 #pragma unroll

@@ -146,18 +146,19 @@ __device__ __forceinline__ uint4 frag_mn_major(const uint16_t* base, int k0, int
 }
 
 // Operand fragment from an LDS tile stored K-major in rows of 32 elements
-// (64 B): element (mn, k) at base[mn * 32 + (((k / 8) ^ ((mn >> 1) & 3)) * 8) + k % 8].
-// The XOR spreads eight consecutive rows of one 16-byte read over all banks.
+// (64 B): element (mn, k) at base[mn * 32 + (((k / 8) ^ ((mn >> 2) & 3)) * 8) + k % 8].
+// The XOR spreads sixteen consecutive rows of one 16-byte read over all 64
+// banks.
 __device__ __forceinline__ uint4 frag_k_major32(const uint16_t* base, int kk, int mn0, int lane) {
   const int mn = mn0 + (lane & 31);
-  const int pos = ((2 * kk + (lane >> 5)) ^ ((lane >> 1) & 3)) * 8;
+  const int pos = ((2 * kk + (lane >> 5)) ^ ((lane >> 2) & 3)) * 8;
   return *reinterpret_cast<const uint4*>(base + mn * 32 + pos);
 }
 
 // Element offset of 16-byte chunk `chunk` (0..3) of row `row` in a K-major
 // 32-element-row tile (the layout frag_k_major32 reads).
 __device__ __forceinline__ int k_major32_offset(int row, int chunk) {
-  return row * 32 + ((chunk ^ ((row >> 1) & 3)) * 8);
+  return row * 32 + ((chunk ^ ((row >> 2) & 3)) * 8);
 }
 
 }  // namespace pfc
