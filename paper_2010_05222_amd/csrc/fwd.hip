@@ -379,15 +379,24 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
   }
   wait_lgkm0();
   stage_barrier();
-  // Wave w writes rows 32 w .. 32 w + 31, two rows (2 x 512 B) per store.
+  // Wave w writes rows 32 w .. 32 w + 31, two rows (2 x 512 B) per store;
+  // all of its LDS reads are issued before the first store.
   {
     const int b = lane & 31;
+    u32x4_t v[16];
+    static_for<0, 16>([&](auto ii) {
+      constexpr int i = decltype(ii)::value;
+      const int r = 32 * wave + 2 * i + (lane >> 5);
+      ds_read_128<0>(v[i], lds_addr(fwd_tile_row(r) + 8 * (b ^ (r & 15))));
+    });
+    lgkm_wait<0>(v);
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int r = 32 * wave + 2 * i + (lane >> 5);
       const int n = n0 + r;
-      const uint4 v = *reinterpret_cast<const uint4*>(fwd_tile_row(r) + 8 * (b ^ (r & 15)));
-      if (n < B) *reinterpret_cast<uint4*>(lbuf + (int64_t)n * ld_cos + j0 + 8 * b) = v;
+      if (n < B)
+        *reinterpret_cast<uint4*>(lbuf + (int64_t)n * ld_cos + j0 + 8 * b) =
+            make_uint4(v[i].x, v[i].y, v[i].z, v[i].w);
     }
   }
   if (tid < kFwdBN) {
