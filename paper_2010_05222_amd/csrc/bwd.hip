@@ -506,6 +506,17 @@ __global__ void __launch_bounds__(256) k_dw16(
   const int c_stop = (int)ceil_div(n_chunks, 3) * 3;
   // The tile is one 128-class group of the logit store: its row scales.
   const float* gsc = gscale + (j0 / kLogitGroup) * ld_g;
+  // Row ids and 1/||w|| of the tile's classes for the update, requested now
+  // so that they have long arrived when the update forms its row addresses:
+  // lane l holds classes l (u = 0) and 64 + l (u = 1).
+  int act_l[2];
+  float iw_l[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int64_t j = j0 + 64 * u + lane;
+    act_l[u] = j < K ? active[j] : 0;
+    iw_l[u] = j < K ? inv_w[j] : 0.0f;
+  }
 
   // Producer slots: a 16-lane group owns 16 classes x 8 batch rows of a chunk;
   // lane gi of the group owns class 16 cb + gi.
@@ -750,35 +761,41 @@ __global__ void __launch_bounds__(256) k_dw16(
   constexpr int RPW = 32 / NW;                // rows of a pass per wave
   float* const tlo = reinterpret_cast<float*>(wX0);
   float* const thi = reinterpret_cast<float*>(wX1);
-  const bool lane_on = lane < LPH;
+  const bool lane_on = LPH == 64 || lane < LPH;
+  const int kt = (int)(K - j0);               // classes of the tile that exist (>= 1)
   int* const hits = reinterpret_cast<int*>(wG0);   // NW lists of kHitCap entries
   int* const hit_n = reinterpret_cast<int*>(wQ0);  // their lengths
   static_assert(NW * kHitCap * 4 <= kDwCls * kBwKC * 2, "hit lists fit a coefficient stage");
 
+  // A wave's rows of one pass.  Row ids, 1/||w|| and the count of rows that
+  // exist are wave-uniform; a row past |S| reads row 0 and is not updated.
   struct Rows {
     uint2 wv[RPW][NH];   // four 16-bit weights
     float4 mv[RPW][NH], pv[MASTER ? RPW : 1][NH];
-    int64_t rowa[RPW];
+    int row[RPW];
     float iwr[RPW];
-    bool rv[RPW];
+    int nv;              // rows k < nv exist
   };
   auto load_rows = [&](Rows& bt, int p) __attribute__((always_inline)) {
+    const int cb = 32 * p + RPW * wave;   // tile offset of the wave's first class of the pass
+    bt.nv = kt - cb < 0 ? 0 : (kt - cb > RPW ? RPW : kt - cb);
 #pragma unroll
     for (int k = 0; k < RPW; ++k) {
-      const int64_t j = j0 + 32 * p + RPW * wave + k;
-      bt.rv[k] = j < K && lane_on;
-      bt.rowa[k] = j < K ? (int64_t)active[j] : 0;
-      bt.iwr[k] = j < K ? inv_w[j] : 0.0f;
+      const int src = 32 * (p & 1) + RPW * wave + k;   // lane that holds class cb + k
+      bt.row[k] = __builtin_amdgcn_readlane(act_l[p >> 1], src);
+      bt.iwr[k] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(iw_l[p >> 1]), src));
+      const int64_t rb = (int64_t)bt.row[k] * D;   // uniform row base
 #pragma unroll
       for (int h = 0; h < NH; ++h) {
-        const int64_t off = bt.rowa[k] * D + 256 * h + 4 * lane;
+        const uint32_t o = 256u * h + 4u * (uint32_t)lane;
         bt.wv[k][h] = make_uint2(0, 0);
         bt.mv[k][h] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
         if constexpr (MASTER) bt.pv[k][h] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-        if (bt.rv[k]) {
-          bt.wv[k][h] = *reinterpret_cast<const uint2*>(W + off);
-          bt.mv[k][h] = *reinterpret_cast<const float4*>(M + off);
-          if constexpr (MASTER) bt.pv[k][h] = *reinterpret_cast<const float4*>(W_master + off);
+        if (lane_on) {
+          bt.wv[k][h] = *reinterpret_cast<const uint2*>(reinterpret_cast<const char*>(W + rb) + 2 * o);
+          bt.mv[k][h] = *reinterpret_cast<const float4*>(reinterpret_cast<const char*>(M + rb) + 4 * o);
+          if constexpr (MASTER)
+            bt.pv[k][h] = *reinterpret_cast<const float4*>(reinterpret_cast<const char*>(W_master + rb) + 4 * o);
         }
       }
     }
@@ -812,34 +829,53 @@ __global__ void __launch_bounds__(256) k_dw16(
       *t = a;
     }
   };
+  auto wf_of = [&](uint2 w4) __attribute__((always_inline)) {
+    return make_float4(to_float<Tag>((uint16_t)(w4.x & 0xFFFF)), to_float<Tag>((uint16_t)(w4.x >> 16)),
+                       to_float<Tag>((uint16_t)(w4.y & 0xFFFF)), to_float<Tag>((uint16_t)(w4.y >> 16)));
+  };
+  // Row update, with a = the staged row (dL/dw_hat = sB a), w_hat = w / ||w||:
+  // g_w = (sB a - w_hat (w_hat . sB a)) / ||w|| = ga a - gb w,
+  // ga = sB / ||w||, gb = ga (w . a) / ||w||^2; then momentum and the step.
   auto update_rows = [&](Rows& bt) __attribute__((always_inline)) {
+    // The dots w . a of all of this wave's rows first, then their reductions.
+    float dots[RPW];
 #pragma unroll
     for (int k = 0; k < RPW; ++k) {
       const int r = RPW * wave + k;
-      float4 gv[NH], wf[NH];
       float dot = 0.0f;
 #pragma unroll
       for (int h = 0; h < NH; ++h) {
-        const uint2 w4 = bt.wv[k][h];
-        wf[h] = make_float4(to_float<Tag>((uint16_t)(w4.x & 0xFFFF)), to_float<Tag>((uint16_t)(w4.x >> 16)),
-                            to_float<Tag>((uint16_t)(w4.y & 0xFFFF)), to_float<Tag>((uint16_t)(w4.y >> 16)));
-        gv[h] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-        if (bt.rv[k]) {
-          const float4 a4 = *reinterpret_cast<const float4*>((h ? thi : tlo) + r * kTLd + 4 * lane);
-          gv[h] = make_float4(sB * a4.x, sB * a4.y, sB * a4.z, sB * a4.w);
-          dot = fmaf(wf[h].x * bt.iwr[k], gv[h].x, dot);
-          dot = fmaf(wf[h].y * bt.iwr[k], gv[h].y, dot);
-          dot = fmaf(wf[h].z * bt.iwr[k], gv[h].z, dot);
-          dot = fmaf(wf[h].w * bt.iwr[k], gv[h].w, dot);
-        }
+        if (!lane_on) continue;
+        const float4 wf = wf_of(bt.wv[k][h]);
+        const float4 a4 = *reinterpret_cast<const float4*>((h ? thi : tlo) + r * kTLd + 4 * lane);
+        dot = fmaf(wf.x, a4.x, dot);
+        dot = fmaf(wf.y, a4.y, dot);
+        dot = fmaf(wf.z, a4.z, dot);
+        dot = fmaf(wf.w, a4.w, dot);
       }
-      dot = wave_sum(dot);
-      if (!bt.rv[k]) continue;
+      dots[k] = dot;
+    }
+#pragma unroll
+    for (int k = 0; k < RPW; ++k) dots[k] = wave_total(dots[k]);
+#pragma unroll
+    for (int k = 0; k < RPW; ++k) {
+      if (k >= bt.nv) break;
+      const int r = RPW * wave + k;
+      const float ga = sB * bt.iwr[k];
+      const float gb = ga * bt.iwr[k] * bt.iwr[k] * dots[k];
+      // Uniform row base, made opaque so that the stores below address it as
+      // base + lane offset instead of sharing the loads' 64-bit addresses.
+      int rw = bt.row[k];
+      asm volatile("" : "+s"(rw));
+      const int64_t rb = (int64_t)rw * D;
 #pragma unroll
       for (int h = 0; h < NH; ++h) {
-        const int64_t off = bt.rowa[k] * D + 256 * h + 4 * lane;
-        const float wo[4] = {wf[h].x, wf[h].y, wf[h].z, wf[h].w};
-        const float go[4] = {gv[h].x, gv[h].y, gv[h].z, gv[h].w};
+        if (!lane_on) continue;
+        const uint32_t o = 256u * h + 4u * (uint32_t)lane;
+        const float4 wf = wf_of(bt.wv[k][h]);
+        const float4 a4 = *reinterpret_cast<const float4*>((h ? thi : tlo) + r * kTLd + 4 * lane);
+        const float wo[4] = {wf.x, wf.y, wf.z, wf.w};
+        const float ao[4] = {a4.x, a4.y, a4.z, a4.w};
         float mo[4] = {bt.mv[k][h].x, bt.mv[k][h].y, bt.mv[k][h].z, bt.mv[k][h].w};
         float po[4] = {0.0f, 0.0f, 0.0f, 0.0f};
         if constexpr (MASTER) {
@@ -851,23 +887,27 @@ __global__ void __launch_bounds__(256) k_dw16(
         float wn[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float gr = bt.iwr[k] * (go[e] - wo[e] * bt.iwr[k] * dot);
-          mo[e] = mu * mo[e] + gr;
+          const float gr = fmaf(-gb, wo[e], ga * ao[e]);
+          mo[e] = fmaf(mu, mo[e], gr);
           if constexpr (MASTER) {
-            po[e] = po[e] - lr * mo[e];
+            po[e] = fmaf(-lr, mo[e], po[e]);
             wn[e] = po[e];
           } else {
-            wn[e] = wo[e] - lr * mo[e];
+            wn[e] = fmaf(-lr, mo[e], wo[e]);
           }
         }
-        *reinterpret_cast<float4*>(M + off) = make_float4(mo[0], mo[1], mo[2], mo[3]);
+        *reinterpret_cast<float4*>(reinterpret_cast<char*>(M + rb) + 4 * o) =
+            make_float4(mo[0], mo[1], mo[2], mo[3]);
         if constexpr (MASTER)
-          *reinterpret_cast<float4*>(W_master + off) = make_float4(po[0], po[1], po[2], po[3]);
-        uint2 o;
-        o.x = pack2<Tag>(wn[0], wn[1]);
-        o.y = pack2<Tag>(wn[2], wn[3]);
-        *reinterpret_cast<uint2*>(W + off) = o;
+          *reinterpret_cast<float4*>(reinterpret_cast<char*>(W_master + rb) + 4 * o) =
+              make_float4(po[0], po[1], po[2], po[3]);
+        uint2 ov;
+        ov.x = pack2<Tag>(wn[0], wn[1]);
+        ov.y = pack2<Tag>(wn[2], wn[3]);
+        *reinterpret_cast<uint2*>(reinterpret_cast<char*>(W + rb) + 2 * o) = ov;
       }
+      // Keep the rows' LDS reads in row order (hoisting them all costs registers).
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
 

@@ -124,6 +124,28 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// Lane move within rows of 16 lanes (DPP; CTRL: quad_perm 0x00-0xFF, row_mirror
+// 0x140, row_half_mirror 0x141).
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true));
+}
+
+// Sum over the wave's 64 lanes, returned as a wave-uniform value: butterfly
+// within each 16-lane row by lane moves (no LDS), then the four row sums in a
+// fixed order.
+__device__ __forceinline__ float wave_total(float v) {
+  v += dpp_mov<0xB1>(v);    // quad_perm [1,0,3,2]: pairs
+  v += dpp_mov<0x4E>(v);    // quad_perm [2,3,0,1]: quads
+  v += dpp_mov<0x141>(v);   // row_half_mirror: the other quad of the 8-lane half
+  v += dpp_mov<0x140>(v);   // row_mirror: the other half of the row
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+  return (r0 + r1) + (r2 + r3);
+}
+
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
