@@ -754,8 +754,8 @@ __global__ void __launch_bounds__(256) k_dw16(
   // and written in full contiguous segments.  Pass p holds the classes
   // 32 p + r (r < 32); entry d of row r sits in stage array d / 256 at
   // r * kTLd + d % 256.  Wave w owns rows 8 w .. 8 w + 7 of each pass; lane l
-  // owns d = 256 h + 4 l .. + 3.  A wave's rows of a pass are loaded before
-  // the pass's gradients are parked.
+  // owns d = 256 h + 4 l .. + 3.  A wave's rows of a pass are loaded while
+  // the previous pass is updated, one row after each row written.
   constexpr int NH = D > 256 ? 2 : 1;         // 256-entry halves of a row
   constexpr int LPH = (D > 256 ? 256 : D) / 4;  // lanes that own entries
   constexpr int RPW = 32 / NW;                // rows of a pass per wave
@@ -776,29 +776,33 @@ __global__ void __launch_bounds__(256) k_dw16(
     float iwr[RPW];
     int nv;              // rows k < nv exist
   };
-  auto load_rows = [&](Rows& bt, int p) __attribute__((always_inline)) {
+  auto set_rows = [&](Rows& bt, int p) __attribute__((always_inline)) {
     const int cb = 32 * p + RPW * wave;   // tile offset of the wave's first class of the pass
     bt.nv = kt - cb < 0 ? 0 : (kt - cb > RPW ? RPW : kt - cb);
+  };
+  auto load_row = [&](Rows& bt, int p, int k) __attribute__((always_inline)) {
+    const int src = 32 * (p & 1) + RPW * wave + k;   // lane that holds class 32 p + RPW wave + k
+    bt.row[k] = __builtin_amdgcn_readlane(act_l[p >> 1], src);
+    bt.iwr[k] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(iw_l[p >> 1]), src));
+    const int64_t rb = (int64_t)bt.row[k] * D;   // uniform row base
 #pragma unroll
-    for (int k = 0; k < RPW; ++k) {
-      const int src = 32 * (p & 1) + RPW * wave + k;   // lane that holds class cb + k
-      bt.row[k] = __builtin_amdgcn_readlane(act_l[p >> 1], src);
-      bt.iwr[k] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(iw_l[p >> 1]), src));
-      const int64_t rb = (int64_t)bt.row[k] * D;   // uniform row base
-#pragma unroll
-      for (int h = 0; h < NH; ++h) {
-        const uint32_t o = 256u * h + 4u * (uint32_t)lane;
-        bt.wv[k][h] = make_uint2(0, 0);
-        bt.mv[k][h] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-        if constexpr (MASTER) bt.pv[k][h] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-        if (lane_on) {
-          bt.wv[k][h] = *reinterpret_cast<const uint2*>(reinterpret_cast<const char*>(W + rb) + 2 * o);
-          bt.mv[k][h] = *reinterpret_cast<const float4*>(reinterpret_cast<const char*>(M + rb) + 4 * o);
-          if constexpr (MASTER)
-            bt.pv[k][h] = *reinterpret_cast<const float4*>(reinterpret_cast<const char*>(W_master + rb) + 4 * o);
-        }
+    for (int h = 0; h < NH; ++h) {
+      const uint32_t o = 256u * h + 4u * (uint32_t)lane;
+      bt.wv[k][h] = make_uint2(0, 0);
+      bt.mv[k][h] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      if constexpr (MASTER) bt.pv[k][h] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      if (lane_on) {
+        bt.wv[k][h] = *reinterpret_cast<const uint2*>(reinterpret_cast<const char*>(W + rb) + 2 * o);
+        bt.mv[k][h] = *reinterpret_cast<const float4*>(reinterpret_cast<const char*>(M + rb) + 4 * o);
+        if constexpr (MASTER)
+          bt.pv[k][h] = *reinterpret_cast<const float4*>(reinterpret_cast<const char*>(W_master + rb) + 4 * o);
       }
     }
+  };
+  auto load_rows = [&](Rows& bt, int p) __attribute__((always_inline)) {
+    set_rows(bt, p);
+#pragma unroll
+    for (int k = 0; k < RPW; ++k) load_row(bt, p, k);
   };
   auto park = [&](auto pp) __attribute__((always_inline)) {
     constexpr int p = decltype(pp)::value;
@@ -836,7 +840,11 @@ __global__ void __launch_bounds__(256) k_dw16(
   // Row update, with a = the staged row (dL/dw_hat = sB a), w_hat = w / ||w||:
   // g_w = (sB a - w_hat (w_hat . sB a)) / ||w|| = ga a - gb w,
   // ga = sB / ||w||, gb = ga (w . a) / ||w||^2; then momentum and the step.
-  auto update_rows = [&](Rows& bt) __attribute__((always_inline)) {
+  // With PN < 4 each row's registers are refilled, right after the row is
+  // written, with the same row of pass PN: the next pass's loads spread over
+  // this pass's arithmetic and stores instead of queueing behind them.
+  auto update_rows = [&](Rows& bt, auto pn_c) __attribute__((always_inline)) {
+    constexpr int PN = decltype(pn_c)::value;
     // The dots w . a of all of this wave's rows first, then their reductions.
     float dots[RPW];
 #pragma unroll
@@ -857,65 +865,67 @@ __global__ void __launch_bounds__(256) k_dw16(
     }
 #pragma unroll
     for (int k = 0; k < RPW; ++k) dots[k] = wave_total(dots[k]);
+    const int nv = bt.nv;
+    if constexpr (PN < 4) set_rows(bt, PN);
 #pragma unroll
     for (int k = 0; k < RPW; ++k) {
-      if (k >= bt.nv) break;
       const int r = RPW * wave + k;
-      const float ga = sB * bt.iwr[k];
-      const float gb = ga * bt.iwr[k] * bt.iwr[k] * dots[k];
-      // Uniform row base, made opaque so that the stores below address it as
-      // base + lane offset instead of sharing the loads' 64-bit addresses.
-      int rw = bt.row[k];
-      asm volatile("" : "+s"(rw));
-      const int64_t rb = (int64_t)rw * D;
+      if (k < nv) {
+        const float ga = sB * bt.iwr[k];
+        const float gb = ga * bt.iwr[k] * bt.iwr[k] * dots[k];
+        // Uniform row base, made opaque so that the stores below address it as
+        // base + lane offset instead of sharing the loads' 64-bit addresses.
+        int rw = bt.row[k];
+        asm volatile("" : "+s"(rw));
+        const int64_t rb = (int64_t)rw * D;
 #pragma unroll
-      for (int h = 0; h < NH; ++h) {
-        if (!lane_on) continue;
-        const uint32_t o = 256u * h + 4u * (uint32_t)lane;
-        const float4 wf = wf_of(bt.wv[k][h]);
-        const float4 a4 = *reinterpret_cast<const float4*>((h ? thi : tlo) + r * kTLd + 4 * lane);
-        const float wo[4] = {wf.x, wf.y, wf.z, wf.w};
-        const float ao[4] = {a4.x, a4.y, a4.z, a4.w};
-        float mo[4] = {bt.mv[k][h].x, bt.mv[k][h].y, bt.mv[k][h].z, bt.mv[k][h].w};
-        float po[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-        if constexpr (MASTER) {
-          po[0] = bt.pv[k][h].x;
-          po[1] = bt.pv[k][h].y;
-          po[2] = bt.pv[k][h].z;
-          po[3] = bt.pv[k][h].w;
-        }
-        float wn[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float gr = fmaf(-gb, wo[e], ga * ao[e]);
-          mo[e] = fmaf(mu, mo[e], gr);
+        for (int h = 0; h < NH; ++h) {
+          if (!lane_on) continue;
+          const uint32_t o = 256u * h + 4u * (uint32_t)lane;
+          const float4 wf = wf_of(bt.wv[k][h]);
+          const float4 a4 = *reinterpret_cast<const float4*>((h ? thi : tlo) + r * kTLd + 4 * lane);
+          const float wo[4] = {wf.x, wf.y, wf.z, wf.w};
+          const float ao[4] = {a4.x, a4.y, a4.z, a4.w};
+          float mo[4] = {bt.mv[k][h].x, bt.mv[k][h].y, bt.mv[k][h].z, bt.mv[k][h].w};
+          float po[4] = {0.0f, 0.0f, 0.0f, 0.0f};
           if constexpr (MASTER) {
-            po[e] = fmaf(-lr, mo[e], po[e]);
-            wn[e] = po[e];
-          } else {
-            wn[e] = fmaf(-lr, mo[e], wo[e]);
+            po[0] = bt.pv[k][h].x;
+            po[1] = bt.pv[k][h].y;
+            po[2] = bt.pv[k][h].z;
+            po[3] = bt.pv[k][h].w;
           }
+          float wn[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float gr = fmaf(-gb, wo[e], ga * ao[e]);
+            mo[e] = fmaf(mu, mo[e], gr);
+            if constexpr (MASTER) {
+              po[e] = fmaf(-lr, mo[e], po[e]);
+              wn[e] = po[e];
+            } else {
+              wn[e] = fmaf(-lr, mo[e], wo[e]);
+            }
+          }
+          *reinterpret_cast<float4*>(reinterpret_cast<char*>(M + rb) + 4 * o) =
+              make_float4(mo[0], mo[1], mo[2], mo[3]);
+          if constexpr (MASTER)
+            *reinterpret_cast<float4*>(reinterpret_cast<char*>(W_master + rb) + 4 * o) =
+                make_float4(po[0], po[1], po[2], po[3]);
+          uint2 ov;
+          ov.x = pack2<Tag>(wn[0], wn[1]);
+          ov.y = pack2<Tag>(wn[2], wn[3]);
+          *reinterpret_cast<uint2*>(reinterpret_cast<char*>(W + rb) + 2 * o) = ov;
         }
-        *reinterpret_cast<float4*>(reinterpret_cast<char*>(M + rb) + 4 * o) =
-            make_float4(mo[0], mo[1], mo[2], mo[3]);
-        if constexpr (MASTER)
-          *reinterpret_cast<float4*>(reinterpret_cast<char*>(W_master + rb) + 4 * o) =
-              make_float4(po[0], po[1], po[2], po[3]);
-        uint2 ov;
-        ov.x = pack2<Tag>(wn[0], wn[1]);
-        ov.y = pack2<Tag>(wn[2], wn[3]);
-        *reinterpret_cast<uint2*>(reinterpret_cast<char*>(W + rb) + 2 * o) = ov;
       }
-      // Keep the rows' LDS reads in row order (hoisting them all costs registers).
-      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (PN < 4) load_row(bt, PN, k);
     }
   };
 
-  // Without a master copy the rows of the next pass are requested before
-  // this pass is computed (two row sets in registers).
-  constexpr int NSET = MASTER ? 1 : 2;
-  Rows bat[NSET];
-  load_rows(bat[0], 0);
+  // One row set in registers: pass p's rows, refilled row by row with pass
+  // p + 1 (requesting two passes ahead measured no faster: the update's
+  // loads and stores are bound by the HBM read-modify-write rate).
+  Rows bat;
+  load_rows(bat, 0);
   stage_barrier();  // every wave's fragment reads of the stage arrays are done
   // Target terms: wave w lists, in row order, the rows n of its quarter of the
   // batch whose label is one of the tile's classes (entry n * 128 + class
@@ -949,9 +959,7 @@ __global__ void __launch_bounds__(256) k_dw16(
   }
   static_for<0, 4>([&](auto pp) {
     constexpr int p = decltype(pp)::value;
-    if constexpr (NSET == 2 && p + 1 < 4) load_rows(bat[(p + 1) % NSET], p + 1);
     if constexpr (p > 0) {
-      if constexpr (NSET == 1) load_rows(bat[0], p);
       wait_lgkm0();
       stage_barrier();  // the stage arrays are rewritten by this pass
       park(pp);
@@ -980,7 +988,7 @@ __global__ void __launch_bounds__(256) k_dw16(
         }
       }
     }
-    update_rows(bat[p % NSET]);
+    update_rows(bat, std::integral_constant<int, p + 1>{});
   });
 }
 
