@@ -220,6 +220,54 @@ __device__ __forceinline__ void fwd_epilogue_rows(f32x16_t (&acc)[4][2], int nb,
   *sm_out = sm;
 }
 
+// The common case of fwd_epilogue_rows: every class of the lane's pattern
+// exists, none is a row's target, no filter.  With q = s log2 e / ||x|| >= 0
+// the group maximum is q max_j u_j over u_j = acc_j / ||w_j||, and
+// E_j = 2^(u_j q - m) takes one fused multiply-add.
+__device__ __forceinline__ void fwd_epilogue_rows_plain(f32x16_t (&acc)[4][2], int nb, float q,
+                                                        const float* iwp, uint16_t* trow,
+                                                        int bbase, int bsw, int half,
+                                                        float* mx_out, float* sm_out) {
+  float mu = -INFINITY;
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const float4 iw4 = *reinterpret_cast<const float4*>(iwp + 32 * mb + 8 * g);
+      const float iwv[4] = {iw4.x, iw4.y, iw4.z, iw4.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float u = acc[mb][nb][4 * g + e] * iwv[e];
+        acc[mb][nb][4 * g + e] = u;
+        mu = fmaxf(mu, u);
+      }
+    }
+  }
+  mu = fmaxf(mu, __shfl_xor(mu, 32, 64));
+  const float mx = mu * q;
+  float sm = 0.0f;
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int o = 32 * mb + 8 * g;
+      float ev[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        ev[e] = __builtin_amdgcn_exp2f(fmaf(acc[mb][nb][4 * g + e], q, -mx));
+        sm += ev[e];
+      }
+      uint2 packed;
+      packed.x = pack_f16x2(ev[0], ev[1]);
+      packed.y = pack_f16x2(ev[2], ev[3]);
+      *reinterpret_cast<uint2*>(trow + 8 * ((bbase + o / 8) ^ bsw) + 4 * half) = packed;
+    }
+  }
+  sm += __shfl_xor(sm, 32, 64);
+  *mx_out = mx;
+  *sm_out = sm;
+}
+
 // Tile: 256 active classes x 128 batch rows, the whole of d (= 32 * NK).
 // Epilogue, per (row, class): c = acc / (||x|| ||w||) and the base-2 logit
 // s c log2 e (the margined logit at the target, which also goes to tgt[n],
@@ -359,9 +407,13 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
     for (int nb = 0; nb < 2; ++nb) {
       const int nl = 64 * wn + 32 * nb + l32;
       float mx, sm;
-      fwd_epilogue_rows<false, false, FILT>(acc, nb, ixr[nb], iwp, K, jlo + 4 * half, tpos[nb],
-                                            mg, tau, fwd_tile_row(nl), 16 * wm, nl & 15, half,
-                                            &mx, &sm, nullptr, nullptr);
+      if constexpr (FILT)
+        fwd_epilogue_rows<false, false, true>(acc, nb, ixr[nb], iwp, K, jlo + 4 * half, tpos[nb],
+                                              mg, tau, fwd_tile_row(nl), 16 * wm, nl & 15, half,
+                                              &mx, &sm, nullptr, nullptr);
+      else
+        fwd_epilogue_rows_plain(acc, nb, ixr[nb] * (mg.s * kLog2e), iwp, fwd_tile_row(nl),
+                                16 * wm, nl & 15, half, &mx, &sm);
       finish(nb, mx, sm);
     }
   } else {
