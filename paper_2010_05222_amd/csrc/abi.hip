@@ -74,8 +74,9 @@ WsLayout ws_layout(int64_t B, int64_t d, int64_t C, int64_t cap, int compute) {
   L.off_bitmap = take((size_t)ceil_div(C, 32) * 4);
   L.off_hist = take((size_t)(1 << kTopBitsMax) * 4);
   L.off_state = take(sizeof(SampleState));
-  L.off_keys = take((size_t)C * 8);
+  L.off_digits = take((size_t)round_up(C, 4) * 2);   // read four at a time
   L.off_cand = take((size_t)C * 4);
+  L.off_cand_key = take((size_t)C * 8);
   L.off_grp_sure = take((size_t)L.n_groups * 4);
   L.off_grp_tie = take((size_t)L.n_groups * 4);
   L.off_grp_out = take((size_t)L.n_groups * 4);
@@ -121,8 +122,9 @@ SampleWs sample_ws(void* ws, const WsLayout& L) {
   w.bitmap = (uint32_t*)(b + L.off_bitmap);
   w.hist = (uint32_t*)(b + L.off_hist);
   w.state = (SampleState*)(b + L.off_state);
-  w.keys = (uint64_t*)(b + L.off_keys);
+  w.digits = (uint16_t*)(b + L.off_digits);
   w.cand = (uint32_t*)(b + L.off_cand);
+  w.cand_key = (uint64_t*)(b + L.off_cand_key);
   w.grp_sure = (uint32_t*)(b + L.off_grp_sure);
   w.grp_tie = (uint32_t*)(b + L.off_grp_tie);
   w.grp_out = (uint32_t*)(b + L.off_grp_out);

@@ -32,8 +32,9 @@ struct SampleWs {
   uint32_t* bitmap;      // ceil(C/32) words: bit c set iff class c is positive
   uint32_t* hist;        // 2^kTopBitsMax bins
   SampleState* state;
-  uint64_t* keys;        // C keys (only in kSelectKeys mode)
+  uint16_t* digits;      // C top-bit digits of the keys (only in kSelectKeys mode)
   uint32_t* cand;        // C candidate class ids (worst case)
+  uint64_t* cand_key;    // their full keys
   uint32_t* grp_sure;    // per compaction group: classes surely selected
   uint32_t* grp_tie;     // per compaction group: non-positive keys == thresh
   uint32_t* grp_out;     // per compaction group: output offset
@@ -76,7 +77,7 @@ struct StepWs {
 struct WsLayout {
   size_t bytes;
   size_t sample_bytes;   // prefix used by the sampler
-  size_t off_bitmap, off_hist, off_state, off_keys, off_cand;
+  size_t off_bitmap, off_hist, off_state, off_digits, off_cand, off_cand_key;
   size_t off_grp_sure, off_grp_tie, off_grp_out, off_grp_tie_off;
   size_t off_inv_x, off_xb, off_wmax, off_inv_w, off_cos, off_stats, off_tgt, off_tgtc,
       off_gmax, off_gscale, off_dx, off_loss;

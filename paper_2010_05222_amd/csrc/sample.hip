@@ -8,11 +8,15 @@
 // Kernel sequence (no host synchronisation; every kernel reads the
 // device-side mode and returns early when it has nothing to do):
 //   clear -> mark positives (bitmap, |P|) -> plan (mode, n_neg)
-//   -> keys + top-bit histogram (one Philox pass, keys kept in the workspace)
+//   -> keys + top-bit histogram (one Philox pass; only each key's top-bit
+//      digit is kept, 2 bytes per class)
 //   -> pick the top bucket holding the n_neg-th key -> collect that bucket
+//      (its keys recomputed in full)
 //   -> resolve the remaining key bits inside one workgroup (exact threshold)
 //   -> count / scan / write compaction in class order (wavefront ballots),
 //      which yields S already sorted -> remap by binary search.
+// A class whose digit differs from the threshold's is decided by the digit
+// alone; the few in the threshold's bucket compare their recomputed key.
 #include "pfc_internal.h"
 
 namespace pfc {
@@ -55,6 +59,12 @@ __device__ __forceinline__ U64x4 philox4x64_10(uint64_t c0, uint64_t seed) {
   out.v[2] = x2;
   out.v[3] = x3;
   return out;
+}
+
+// Key of class c of the shard starting at global class a.
+__device__ __forceinline__ uint64_t class_key(uint64_t seed, int64_t a, int64_t c) {
+  const int64_t g = a + c;
+  return philox4x64_10((uint64_t)(g >> 2), seed).v[g & 3];
 }
 
 __device__ __forceinline__ bool is_positive(const uint32_t* bitmap, int64_t c) {
@@ -198,7 +208,7 @@ __global__ void k_sample_plan(SampleState* st, int64_t budget, int64_t C) {
 // One Philox block per thread: global ids 4q .. 4q+3, q = q_lo + thread.
 __global__ void __launch_bounds__(256) k_keys_hist(uint64_t seed, int64_t a, int64_t C,
                                                    int top_bits, const uint32_t* bitmap,
-                                                   uint64_t* keys, uint32_t* hist,
+                                                   uint16_t* digits, uint32_t* hist,
                                                    const SampleState* st) {
   if (st->mode != kSelectKeys) return;
   __shared__ uint32_t lhist[1 << kTopBitsMax];
@@ -216,8 +226,9 @@ __global__ void __launch_bounds__(256) k_keys_hist(uint64_t seed, int64_t a, int
     for (int i = 0; i < 4; ++i) {
       const int64_t c = 4 * q + i - a;
       if (c < 0 || c >= C) continue;
-      keys[c] = w.v[i];
-      if (!is_positive(bitmap, c)) atomicAdd(&lhist[w.v[i] >> (64 - top_bits)], 1u);
+      const uint32_t dg = (uint32_t)(w.v[i] >> (64 - top_bits));
+      digits[c] = (uint16_t)dg;
+      if (!is_positive(bitmap, c)) atomicAdd(&lhist[dg], 1u);
     }
   }
   __syncthreads();
@@ -250,32 +261,46 @@ __global__ void __launch_bounds__(1024) k_select_top(const uint32_t* hist, int t
   }
 }
 
-// Collect the non-positive classes whose key's top bits equal the bucket.
-__global__ void __launch_bounds__(256) k_collect(const uint64_t* keys, const uint32_t* bitmap,
-                                                 int64_t C, int top_bits, SampleState* st,
-                                                 uint32_t* cand) {
+// Collect the non-positive classes whose key's top bits equal the bucket,
+// with their full keys.
+__global__ void __launch_bounds__(256) k_collect(const uint16_t* digits, const uint32_t* bitmap,
+                                                 int64_t C, uint64_t seed, int64_t a,
+                                                 SampleState* st, uint32_t* cand,
+                                                 uint64_t* cand_key) {
   if (st->mode != kSelectKeys) return;
-  const uint64_t digit = st->top_digit;
+  const uint32_t digit = st->top_digit;
   const int64_t c0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
-#pragma unroll
+  // c0 is a multiple of 4: one bitmap word and one 8-byte digit word.
+  uint32_t pos = 0xFu;
+  uint64_t dg4 = 0;
+  if (c0 < C) {
+    pos = (bitmap[c0 >> 5] >> (c0 & 31)) & 0xFu;
+    dg4 = *reinterpret_cast<const uint64_t*>(digits + c0);
+  }
+  // Not unrolled: one copy of the key generator.
+#pragma unroll 1
   for (int i = 0; i < 4; ++i) {
     const int64_t c = c0 + i;
     bool take = false;
-    if (c < C) take = !is_positive(bitmap, c) && (keys[c] >> (64 - top_bits)) == digit;
+    if (c < C) take = ((uint32_t)(dg4 >> (16 * i)) & 0xFFFFu) == digit && !((pos >> i) & 1u);
     const uint64_t mask = __ballot(take);
     if (mask == 0) continue;
     uint32_t base = 0;
     const int leader = __ffsll((unsigned long long)mask) - 1;
     if (lane_id() == leader) base = atomicAdd(&st->cand_count, (uint32_t)__popcll(mask));
     base = __shfl(base, leader, 64);
-    if (take) cand[base + popc_below(mask)] = (uint32_t)c;
+    if (take) {
+      const uint32_t slot = base + popc_below(mask);
+      cand[slot] = (uint32_t)c;
+      cand_key[slot] = class_key(seed, a, c);
+    }
   }
 }
 
 // One workgroup: resolve the remaining 64 - top_bits bits of the threshold
 // among the collected candidates, 11 bits per round.
-__global__ void __launch_bounds__(1024) k_refine(const uint64_t* keys, const uint32_t* cand,
-                                                 int top_bits, SampleState* st) {
+__global__ void __launch_bounds__(1024) k_refine(const uint64_t* cand_key, int top_bits,
+                                                 SampleState* st) {
   if (st->mode != kSelectKeys) return;
   constexpr int kBits = 11;
   __shared__ uint32_t lh[1 << kBits];
@@ -291,7 +316,7 @@ __global__ void __launch_bounds__(1024) k_refine(const uint64_t* keys, const uin
     for (int i = threadIdx.x; i < (1 << kBits); i += blockDim.x) lh[i] = 0u;
     __syncthreads();
     for (uint32_t i = threadIdx.x; i < n; i += blockDim.x) {
-      const uint64_t key = keys[cand[i]];
+      const uint64_t key = cand_key[i];
       if ((key >> (64 - known)) == prefix)
         atomicAdd(&lh[(key >> shift) & ((1u << bits) - 1u)], 1u);
     }
@@ -308,36 +333,60 @@ __global__ void __launch_bounds__(1024) k_refine(const uint64_t* keys, const uin
   }
 }
 
-// Per class of one thread: bit i of `sure` / `tie` for class c0 + i.
-__device__ __forceinline__ void class_flags(const uint64_t* keys, const uint32_t* bitmap,
-                                            int64_t C, uint32_t mode, uint64_t thresh,
-                                            int64_t c0, uint32_t* sure, uint32_t* tie) {
-  uint32_t s = 0, t = 0;
+// Per class of one thread: bit i of `sure` / `tie` for class c0 + i.  The
+// threshold's top-bit digit decides every class outside its bucket; a class
+// inside compares its recomputed key.
+__device__ __forceinline__ void class_flags(const uint16_t* digits, const uint32_t* bitmap,
+                                            int64_t C, uint64_t seed, int64_t a,
+                                            const SampleState* st, int64_t c0, uint32_t* sure,
+                                            uint32_t* tie) {
+  const uint32_t mode = st->mode;
+  const uint32_t top = st->top_digit;
+  uint32_t s = 0, t = 0, need = 0;
+  if (c0 >= C) {
+    *sure = 0;
+    *tie = 0;
+    return;
+  }
+  // c0 is a multiple of 4: one bitmap word holds the four classes' bits, and
+  // their four digits are one 8-byte word (the digit array is padded).
+  const uint32_t pos = (bitmap[c0 >> 5] >> (c0 & 31)) & 0xFu;
+  const uint64_t dg4 = mode == kSelectKeys ? *reinterpret_cast<const uint64_t*>(digits + c0) : 0;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int64_t c = c0 + i;
-    if (c >= C) continue;
-    if (is_positive(bitmap, c)) {
+    if (c0 + i >= C) continue;
+    if ((pos >> i) & 1u) {
       s |= 1u << i;
     } else if (mode == kSelectAll) {
       s |= 1u << i;
     } else if (mode == kSelectKeys) {
-      const uint64_t key = keys[c];
+      const uint32_t dg = (uint32_t)(dg4 >> (16 * i)) & 0xFFFFu;
+      if (dg < top) s |= 1u << i;
+      else if (dg == top) need |= 1u << i;
+    }
+  }
+  // Classes in the threshold's bucket (rare): one key generator in a loop.
+  if (need) {
+    const uint64_t thresh = st->thresh;
+    do {
+      const int i = __ffs(need) - 1;
+      need &= need - 1;
+      const uint64_t key = class_key(seed, a, c0 + i);
       if (key < thresh) s |= 1u << i;
       else if (key == thresh) t |= 1u << i;
-    }
+    } while (need);
   }
   *sure = s;
   *tie = t;
 }
 
 __global__ void __launch_bounds__(kCompactThreads) k_compact_count(
-    const uint64_t* keys, const uint32_t* bitmap, int64_t C, const SampleState* st,
-    uint32_t* grp_sure, uint32_t* grp_tie) {
+    const uint16_t* digits, const uint32_t* bitmap, int64_t C, uint64_t seed, int64_t a,
+    const SampleState* st, uint32_t* grp_sure, uint32_t* grp_tie) {
   __shared__ uint32_t smem[kCompactThreads / 64];
   const int64_t c0 = ((int64_t)blockIdx.x * kCompactThreads + threadIdx.x) * 4;
   uint32_t s, t;
-  class_flags(keys, bitmap, C, st->mode, st->thresh, c0, &s, &t);
+  class_flags(digits, bitmap, C, seed, a, st, c0, &s, &t);
   uint32_t tot_s, tot_t;
   block_exclusive_scan((uint32_t)__popc(s), smem, &tot_s);
   block_exclusive_scan((uint32_t)__popc(t), smem, &tot_t);
@@ -348,47 +397,59 @@ __global__ void __launch_bounds__(kCompactThreads) k_compact_count(
 }
 
 // One workgroup of 1024 threads: per-group tie offsets, selected counts and
-// output offsets; n_active.
+// output offsets; n_active.  The groups go in tiles of four per thread
+// (independent, coalesced loads), with running totals carried across tiles.
 __global__ void __launch_bounds__(1024) k_compact_scan(const uint32_t* grp_sure,
                                                        const uint32_t* grp_tie,
                                                        int64_t n_groups, const SampleState* st,
                                                        uint32_t* grp_out, uint32_t* grp_tie_off,
                                                        int32_t* n_active) {
+  constexpr int PER = 4;
   __shared__ uint64_t smem[16];
-  const int64_t per = ceil_div(n_groups, (int64_t)blockDim.x);
-  const int64_t g0 = (int64_t)threadIdx.x * per;
-  const int64_t g1 = g0 + per < n_groups ? g0 + per : n_groups;
   const int64_t k_rem = st->k_rem;
-  // Ties before each group.
-  uint64_t local_t = 0;
-  for (int64_t g = g0; g < g1; ++g) local_t += grp_tie[g];
-  uint64_t tot;
-  uint64_t tie_before = block_exclusive_scan64(local_t, smem, &tot);
-  // Selected count of each group: sure + the ties whose class-order rank is below k_rem.
-  uint64_t local_sel = 0;
-  {
-    uint64_t tb = tie_before;
-    for (int64_t g = g0; g < g1; ++g) {
-      const uint64_t t = grp_tie[g];
-      int64_t take = k_rem - (int64_t)tb;
-      take = take < 0 ? 0 : (take > (int64_t)t ? (int64_t)t : take);
-      local_sel += grp_sure[g] + (uint64_t)take;
-      tb += t;
+  const int64_t tile = (int64_t)blockDim.x * PER;
+  uint64_t carry_tie = 0, carry_sel = 0;
+  for (int64_t base = 0; base < n_groups; base += tile) {
+    const int64_t g0 = base + (int64_t)threadIdx.x * PER;
+    uint32_t t[PER], sr[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int64_t g = g0 + i;
+      t[i] = g < n_groups ? grp_tie[g] : 0u;
+      sr[i] = g < n_groups ? grp_sure[g] : 0u;
     }
+    // Ties before each group.
+    uint64_t tile_tie;
+    uint64_t tb = carry_tie +
+                  block_exclusive_scan64((uint64_t)t[0] + t[1] + t[2] + t[3], smem, &tile_tie);
+    // Selected count of each group: sure + the ties whose class-order rank is below k_rem.
+    uint32_t sel[PER];
+    uint64_t tie_off[PER];
+    uint64_t local_sel = 0;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      int64_t take = k_rem - (int64_t)tb;
+      take = take < 0 ? 0 : (take > (int64_t)t[i] ? (int64_t)t[i] : take);
+      sel[i] = sr[i] + (uint32_t)take;
+      tie_off[i] = tb;
+      local_sel += sel[i];
+      tb += t[i];
+    }
+    uint64_t tile_sel;
+    uint64_t ob = carry_sel + block_exclusive_scan64(local_sel, smem, &tile_sel);
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int64_t g = g0 + i;
+      if (g < n_groups) {
+        grp_tie_off[g] = (uint32_t)tie_off[i];
+        grp_out[g] = (uint32_t)ob;
+      }
+      ob += sel[i];
+    }
+    carry_tie += tile_tie;
+    carry_sel += tile_sel;
   }
-  uint64_t total_sel;
-  uint64_t out_before = block_exclusive_scan64(local_sel, smem, &total_sel);
-  uint64_t tb = tie_before, ob = out_before;
-  for (int64_t g = g0; g < g1; ++g) {
-    const uint64_t t = grp_tie[g];
-    int64_t take = k_rem - (int64_t)tb;
-    take = take < 0 ? 0 : (take > (int64_t)t ? (int64_t)t : take);
-    grp_tie_off[g] = (uint32_t)tb;
-    grp_out[g] = (uint32_t)ob;
-    ob += grp_sure[g] + (uint64_t)take;
-    tb += t;
-  }
-  if (threadIdx.x == 0) *n_active = (int32_t)total_sel;
+  if (threadIdx.x == 0) *n_active = (int32_t)carry_sel;
 }
 
 // Exclusive class-order prefix of the flag bits over the workgroup, where
@@ -421,12 +482,13 @@ __device__ __forceinline__ void ordered_ranks(uint32_t flags, uint32_t* wave_tot
 }
 
 __global__ void __launch_bounds__(kCompactThreads) k_compact_write(
-    const uint64_t* keys, const uint32_t* bitmap, int64_t C, const SampleState* st,
-    const uint32_t* grp_out, const uint32_t* grp_tie_off, int32_t* active) {
+    const uint16_t* digits, const uint32_t* bitmap, int64_t C, uint64_t seed, int64_t a,
+    const SampleState* st, const uint32_t* grp_out, const uint32_t* grp_tie_off,
+    int32_t* active) {
   __shared__ uint32_t smem[kCompactThreads / 64];
   const int64_t c0 = ((int64_t)blockIdx.x * kCompactThreads + threadIdx.x) * 4;
   uint32_t s, t;
-  class_flags(keys, bitmap, C, st->mode, st->thresh, c0, &s, &t);
+  class_flags(digits, bitmap, C, seed, a, st, c0, &s, &t);
   uint32_t trank[4], ttot;
   ordered_ranks(t, smem, trank, &ttot);
   const int64_t tie_base = grp_tie_off[blockIdx.x];
@@ -480,18 +542,17 @@ hipError_t launch_sample(const int64_t* labels, int64_t B, int64_t C, int64_t a,
   const int64_t n_blocks_philox = ((a + C - 1) >> 2) - (a >> 2) + 1;
   const int64_t hist_wgs = ceil_div(n_blocks_philox, 256);
   hipLaunchKernelGGL(k_keys_hist, dim3((unsigned)(hist_wgs < 512 ? hist_wgs : 512)), dim3(256), 0,
-                     stream, seed, a, C, top_bits, w.bitmap, w.keys, w.hist, w.state);
+                     stream, seed, a, C, top_bits, w.bitmap, w.digits, w.hist, w.state);
   hipLaunchKernelGGL(k_select_top, dim3(1), dim3(1024), 0, stream, w.hist, top_bits, w.state);
-  hipLaunchKernelGGL(k_collect, dim3((unsigned)ceil_div(C, 1024)), dim3(256), 0, stream, w.keys,
-                     w.bitmap, C, top_bits, w.state, w.cand);
-  hipLaunchKernelGGL(k_refine, dim3(1), dim3(1024), 0, stream, w.keys, w.cand, top_bits,
-                     w.state);
+  hipLaunchKernelGGL(k_collect, dim3((unsigned)ceil_div(C, 1024)), dim3(256), 0, stream,
+                     w.digits, w.bitmap, C, seed, a, w.state, w.cand, w.cand_key);
+  hipLaunchKernelGGL(k_refine, dim3(1), dim3(1024), 0, stream, w.cand_key, top_bits, w.state);
   hipLaunchKernelGGL(k_compact_count, dim3((unsigned)n_groups), dim3(kCompactThreads), 0, stream,
-                     w.keys, w.bitmap, C, w.state, w.grp_sure, w.grp_tie);
+                     w.digits, w.bitmap, C, seed, a, w.state, w.grp_sure, w.grp_tie);
   hipLaunchKernelGGL(k_compact_scan, dim3(1), dim3(1024), 0, stream, w.grp_sure, w.grp_tie,
                      n_groups, w.state, w.grp_out, w.grp_tie_off, n_active);
   hipLaunchKernelGGL(k_compact_write, dim3((unsigned)n_groups), dim3(kCompactThreads), 0, stream,
-                     w.keys, w.bitmap, C, w.state, w.grp_out, w.grp_tie_off, active);
+                     w.digits, w.bitmap, C, seed, a, w.state, w.grp_out, w.grp_tie_off, active);
   hipLaunchKernelGGL(k_remap, dim3((unsigned)ceil_div(B, 256)), dim3(256), 0, stream, labels, B,
                      C, a, active, n_active, labels_mapped);
   timing_stop(0, stream);
