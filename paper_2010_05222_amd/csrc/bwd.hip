@@ -18,7 +18,7 @@
 //   operands with transposing LDS reads, so they are never staged in
 //   registers.  k_dx_final sums the split partials in a fixed order, adds the
 //   target terms and applies the normalisation backward of x.
-// dW + update (k_dw16): a workgroup (four waves, one per SIMD) owns 128
+// dW + update (k_dw16): a workgroup (eight waves, two per SIMD) owns 128
 //   active classes x all of d and reduces over the whole batch, so its
 //   epilogue has complete rows: target terms, tangent projection, momentum,
 //   weight step and the scatter into the persistent W / momentum rows (unique
@@ -35,7 +35,7 @@ constexpr int kRowStage = kBwKC * kRowLd;
 constexpr int kDxRows = 128;       // batch rows of a dX workgroup
 constexpr int kDwCls = 128;        // classes of a dW workgroup
 constexpr int kTLd = 260;         // LDS row stride (floats) of the update's staged gradient rows
-constexpr int kHitCap = 512;      // target rows listed per wave of a dW workgroup
+constexpr int kHitCap = 256;      // target rows listed per wave of a dW workgroup
 
 // Every operand reaches LDS through direct-to-LDS loads into three-stage
 // rings (one array per stage, so the compiler can keep later stages in
@@ -463,9 +463,10 @@ __global__ void __launch_bounds__(256) k_dx_final(
 
 // ------------------------------------------------------------------ dW
 
-// D = 128 * WI; four waves, one per SIMD: wave w owns d entries
-// [D/4 w, +D/4) and all 128 classes of the workgroup (MB x 4 accumulator
-// tiles of 32 x 32).  Both MFMA operands are K-major in LDS, so every fragment
+// D = 128 * WI; eight waves, two per SIMD: wave w owns d entries
+// [D/4 (w % 4), +D/4) and classes [64 (w / 4), +64) of the workgroup (MB x 2
+// accumulator tiles of 32 x 32), so that a SIMD's second wave issues while
+// the first waits at a barrier or on its loads.  Both MFMA operands are K-major in LDS, so every fragment
 // is one 16-byte read: X^T from the transposed bf16 copy of the batch, and G^T
 // written by the producer.
 // Pipeline per chunk c (32 batch rows): raw logit-store values and row
@@ -474,7 +475,7 @@ __global__ void __launch_bounds__(256) k_dx_final(
 // contracted at the start of the next chunk, from fragments read in this
 // one, so that the matrix pipe is busy while the next fragments arrive.
 template <typename Tag, int WI, bool MASTER>
-__global__ void __launch_bounds__(256) k_dw16(
+__global__ void __launch_bounds__(512) k_dw16(
     const uint16_t* __restrict__ xbT, int64_t ld_xt, const void* __restrict__ X,
     uint16_t* __restrict__ W, float* __restrict__ W_master, float* __restrict__ M,
     const int32_t* __restrict__ active, const int32_t* __restrict__ n_active_p,
@@ -484,14 +485,15 @@ __global__ void __launch_bounds__(256) k_dw16(
     const float* __restrict__ gscale, int64_t ld_g, int B, Margin mg, float sB, float lr,
     float mu) {
   constexpr int D = 128 * WI;
-  constexpr int NW = 4;
-  constexpr int DW = D / NW;            // d entries of a wave
+  constexpr int NW = 8;
+  constexpr int DW = D / 4;             // d entries of a wave
+  constexpr int CW = kDwCls / 2;        // classes of a wave
   constexpr int MB = DW / 32;           // 32-entry d blocks of a wave
-  constexpr int NB = kDwCls / 32;       // 32-class blocks
+  constexpr int NB = CW / 32;           // 32-class blocks of a wave
   constexpr int XDMA = D / 16 / NW;     // X^T loads (16 d rows each) per wave per chunk
   constexpr int RDMA = 8 / NW;          // logit-store loads (4 rows each) per wave
   constexpr int QL = 8 / NW;            // row-scale pieces (4 rows each) per wave
-  constexpr int GROUPS = 2;             // producer slots per thread (512 / 256)
+  constexpr int GROUPS = 1;             // producer slots per thread (512 / 512)
   constexpr int PER_ITER = XDMA + RDMA + 1;
   constexpr int NF = MB + NB;           // fragment reads per k-step
   static_assert(PER_ITER + 2 * (RDMA + 1) < 64, "vmcnt range");
@@ -501,6 +503,7 @@ __global__ void __launch_bounds__(256) k_dw16(
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wd = wave & 3, wc = wave >> 2;   // the wave's d quarter and class half
   const int half = lane >> 5, l32 = lane & 31;
   const int n_chunks = (int)ceil_div(B, kBwKC);
   const int c_stop = (int)ceil_div(n_chunks, 3) * 3;
@@ -626,10 +629,10 @@ __global__ void __launch_bounds__(256) k_dw16(
   // Fragment byte offsets: operand row (d entry or class) 32 q + l32 of the
   // wave's block, chunk 2 kk + half stored at chunk ^ ((row >> 2) & 3).
   const int sw = (l32 >> 2) & 3;
-  const uint32_t a_lane0 = (uint32_t)((DW * wave + l32) * kBwKC * 2 + 16 * ((0 + half) ^ sw));
-  const uint32_t a_lane1 = (uint32_t)((DW * wave + l32) * kBwKC * 2 + 16 * ((2 + half) ^ sw));
-  const uint32_t b_lane0 = (uint32_t)(l32 * kBwKC * 2 + 16 * ((0 + half) ^ sw));
-  const uint32_t b_lane1 = (uint32_t)(l32 * kBwKC * 2 + 16 * ((2 + half) ^ sw));
+  const uint32_t a_lane0 = (uint32_t)((DW * wd + l32) * kBwKC * 2 + 16 * ((0 + half) ^ sw));
+  const uint32_t a_lane1 = (uint32_t)((DW * wd + l32) * kBwKC * 2 + 16 * ((2 + half) ^ sw));
+  const uint32_t b_lane0 = (uint32_t)((CW * wc + l32) * kBwKC * 2 + 16 * ((0 + half) ^ sw));
+  const uint32_t b_lane1 = (uint32_t)((CW * wc + l32) * kBwKC * 2 + 16 * ((2 + half) ^ sw));
 
   f32x16_t acc[MB][NB];
 #pragma unroll
@@ -659,10 +662,11 @@ __global__ void __launch_bounds__(256) k_dw16(
     ProdIn in0;
     produce_load(S0{}, in0);
     lgkm_wait<0>();
-    pin_group(in0, 0);
-    pin_group(in0, 1);
-    produce_group(S0{}, in0, 0, 0xFFFFFFFFu);
-    produce_group(S0{}, in0, 1, 0xFFFFFFFFu);
+#pragma unroll
+    for (int u = 0; u < GROUPS; ++u) {
+      pin_group(in0, u);
+      produce_group(S0{}, in0, u, 0xFFFFFFFFu);
+    }
   }
   // Instruction slots of a chunk: NMF MFMAs per k-step, each followed by
   // the work placed after it, so that the wave issues its other instructions
@@ -711,8 +715,8 @@ __global__ void __launch_bounds__(256) k_dw16(
           pin_group(pin, 0);
         }
         if constexpr (i == G0_AT) produce_group(SN{}, pin, 0, gmask);
-        if constexpr (i == G0_AT + 1) pin_group(pin, 1);
-        if constexpr (i == G1_AT) produce_group(SN{}, pin, 1, gmask);
+        if constexpr (GROUPS > 1 && i == G0_AT + 1) pin_group(pin, 1);
+        if constexpr (GROUPS > 1 && i == G1_AT) produce_group(SN{}, pin, 1, gmask);
       });
       // First k-step of this chunk, with the loads of later chunks and this
       // chunk's second k-step reads spread over its slots.
@@ -753,7 +757,7 @@ __global__ void __launch_bounds__(256) k_dw16(
   // that each wave then owns whole rows: W, momentum and master rows are read
   // and written in full contiguous segments.  Pass p holds the classes
   // 32 p + r (r < 32); entry d of row r sits in stage array d / 256 at
-  // r * kTLd + d % 256.  Wave w owns rows 8 w .. 8 w + 7 of each pass; lane l
+  // r * kTLd + d % 256.  Wave w owns rows 4 w .. 4 w + 3 of each pass; lane l
   // owns d = 256 h + 4 l .. + 3.  A wave's rows of a pass are loaded while
   // the previous pass is updated, one row after each row written.
   constexpr int NH = D > 256 ? 2 : 1;         // 256-entry halves of a row
@@ -804,16 +808,18 @@ __global__ void __launch_bounds__(256) k_dw16(
 #pragma unroll
     for (int k = 0; k < RPW; ++k) load_row(bt, p, k);
   };
+  // Pass p's classes are block p % 2 of the waves of class half p / 2.
   auto park = [&](auto pp) __attribute__((always_inline)) {
     constexpr int p = decltype(pp)::value;
+    if (wc != p / 2) return;
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int d0 = DW * wave + 32 * mb + 8 * g + 4 * half;
+        const int d0 = DW * wd + 32 * mb + 8 * g + 4 * half;
         *reinterpret_cast<float4*>((d0 >= 256 ? thi : tlo) + l32 * kTLd + (d0 & 255)) =
-            make_float4(acc[mb][p][4 * g], acc[mb][p][4 * g + 1], acc[mb][p][4 * g + 2],
-                        acc[mb][p][4 * g + 3]);
+            make_float4(acc[mb][p % 2][4 * g], acc[mb][p % 2][4 * g + 1],
+                        acc[mb][p % 2][4 * g + 2], acc[mb][p % 2][4 * g + 3]);
       }
   };
   // Target term of batch row nn added to staged row r (this wave's own row).
@@ -1127,13 +1133,13 @@ void launch_bwd16(const StepArgs& a, const StepWs& w, const Margin& mg, float sB
   timing_stop(5, stream);
   timing_start(6, stream);
   if (a.W_master)
-    hipLaunchKernelGGL((k_dw16<Tag, WI, true>), dim3((unsigned)ceil_div(a.cap, kDwCls)), dim3(256),
+    hipLaunchKernelGGL((k_dw16<Tag, WI, true>), dim3((unsigned)ceil_div(a.cap, kDwCls)), dim3(512),
                        0, stream, (const uint16_t*)w.xbT, w.ld_xt, a.X, (uint16_t*)a.W, a.W_master,
                        a.M, a.active, a.n_active, a.labels_mapped, a.row_lse, w.inv_x, w.inv_w,
                        w.tgtc, (const uint16_t*)w.lbuf, w.ld_cos, w.gscale, w.ld_g, B, mg, sB, a.lr,
                        a.mu);
   else
-    hipLaunchKernelGGL((k_dw16<Tag, WI, false>), dim3((unsigned)ceil_div(a.cap, kDwCls)), dim3(256),
+    hipLaunchKernelGGL((k_dw16<Tag, WI, false>), dim3((unsigned)ceil_div(a.cap, kDwCls)), dim3(512),
                        0, stream, (const uint16_t*)w.xbT, w.ld_xt, a.X, (uint16_t*)a.W, a.W_master,
                        a.M, a.active, a.n_active, a.labels_mapped, a.row_lse, w.inv_x, w.inv_w,
                        w.tgtc, (const uint16_t*)w.lbuf, w.ld_cos, w.gscale, w.ld_g, B, mg, sB, a.lr,
