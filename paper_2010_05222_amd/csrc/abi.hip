@@ -112,6 +112,8 @@ WsLayout ws_layout(int64_t B, int64_t d, int64_t C, int64_t cap, int compute) {
   L.off_tgtc = take((size_t)B * 4);
   L.off_gmax = take(compute == PFC_F32 ? 0 : (size_t)L.n_lgroups * L.ld_g * 4);
   L.off_gscale = take(compute == PFC_F32 ? 0 : (size_t)L.n_lgroups * L.ld_g * 4);
+  L.n_act_pad = round_up(cap, 32);
+  L.off_act_pad = take(compute == PFC_F32 ? 0 : (size_t)L.n_act_pad * 4);
   L.bytes = off;
   return L;
 }
@@ -153,6 +155,8 @@ StepWs step_ws(void* ws, const WsLayout& L) {
   w.gscale = (float*)(b + L.off_gscale);
   w.ld_g = L.ld_g;
   w.n_groups = L.n_lgroups;
+  w.act_pad = (int32_t*)(b + L.off_act_pad);
+  w.n_act_pad = L.n_act_pad;
   return w;
 }
 

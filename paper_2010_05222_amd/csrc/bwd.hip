@@ -51,6 +51,8 @@ __shared__ __attribute__((aligned(16))) float xI0[kBwKC], xI1[kBwKC], xI2[kBwKC]
 __shared__ __attribute__((aligned(16))) float xS0[kDxRows], xS1[kDxRows], xS2[kDxRows];
 __shared__ __attribute__((aligned(1024))) uint16_t xG0[kDxRows * kBwKC], xG1[kDxRows * kBwKC],
     xG2[kDxRows * kBwKC];
+// dX: active row ids of four chunks (a ring: chunk c in slot c % 4).
+__shared__ __attribute__((aligned(16))) int32_t xIds[4][kBwKC];
 // dW: X^T rows (K-major: d rows of 32 batch rows, bf16), raw logit-store
 // values [32 rows x 128 classes] (16-byte pieces swizzled per row), the rows'
 // scales, and the coefficient tile G^T (K-major: 128 class rows of 32 batch
@@ -151,7 +153,7 @@ __device__ __forceinline__ void zero_acc(T (&acc)[4][2]) {
 // chunk c + 1 are produced, and chunk c is contracted.
 template <typename Tag, int WI>
 __global__ void __launch_bounds__(128 * WI) k_dx16(
-    const uint16_t* __restrict__ W, const int32_t* __restrict__ active,
+    const uint16_t* __restrict__ W, const int32_t* __restrict__ act_pad,
     const int32_t* __restrict__ n_active_p, const float* __restrict__ inv_w,
     const float* __restrict__ inv_w_max, const uint16_t* __restrict__ lbuf, int64_t ld_cos,
     const float* __restrict__ gscale, int64_t ld_g, int B, int n_rt, int n_split,
@@ -162,7 +164,7 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
   constexpr int WROWS = kBwKC / NW;         // W rows DMA'd by each wave per chunk
   constexpr int RDMA = 8 / NW;              // 1-KB logit-store blocks DMA'd by each wave
   constexpr int GROUPS = 512 / NT;          // 8-coefficient groups per thread per chunk
-  constexpr int PER_ITER = WROWS + RDMA + 2;  // DMAs a wave issues per chunk
+  constexpr int PER_ITER = WROWS + RDMA + 3;  // DMAs a wave issues per chunk
   const int64_t t = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
   if (t >= n_tiles) return;
   // The batch-row tiles of one split share its class range: they run on one
@@ -212,15 +214,34 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
     const float* gs = gscale + (jb / kLogitGroup) * ld_g + n0;
     if (lane < 32 / NW) dma16(gs + 4 * (wave * (32 / NW) + lane), dx_s<S>() + 4 * wave * (32 / NW));
   };
-  // Active-set indices of the W rows this wave DMAs for a chunk, loaded one
-  // chunk ahead of their DMA (wave-uniform: scalar loads).
+  // Active-set indices of the W rows this wave DMAs for a chunk.  The first
+  // two chunks' come from scalar loads; later chunks' travel with the loads,
+  // four chunks ahead, into the index ring (their wait is then the chunk's
+  // load wait, not a scalar-load round trip inside the loop).  The padded copy
+  // holds a valid row id at every index of a chunk.
   int32_t rows_pf[WROWS];
   auto load_rows = [&](int64_t c) {
-    const int64_t jb = c * kBwKC;
+    const int64_t jb = (c < n_chunks ? c : n_chunks - 1) * kBwKC;
 #pragma unroll
-    for (int v = 0; v < WROWS; ++v) {
-      const int64_t j = jb + wave * WROWS + v;
-      rows_pf[v] = active[__builtin_amdgcn_readfirstlane((int)(j < K ? j : K - 1))];
+    for (int v = 0; v < WROWS; ++v)
+      rows_pf[v] = act_pad[__builtin_amdgcn_readfirstlane((int)(jb + wave * WROWS + v))];
+  };
+  auto dma_ids = [&](int64_t c) {
+    const int64_t jb = (c < n_chunks ? c : n_chunks - 1) * kBwKC;
+    if (lane < WROWS / 4) dma16(act_pad + jb + wave * WROWS + 4 * lane, &xIds[c & 3][wave * WROWS]);
+  };
+  auto read_ids = [&](int64_t c, u32x4_t (&iv)[WROWS / 4]) {
+#pragma unroll
+    for (int q = 0; q < WROWS / 4; ++q)
+      ds_read_128<0>(iv[q], lds_addr(&xIds[c & 3][wave * WROWS + 4 * q]));
+  };
+  auto rows_of = [&](u32x4_t (&iv)[WROWS / 4]) {
+#pragma unroll
+    for (int q = 0; q < WROWS / 4; ++q) {
+      rows_pf[4 * q + 0] = __builtin_amdgcn_readfirstlane((int)iv[q].x);
+      rows_pf[4 * q + 1] = __builtin_amdgcn_readfirstlane((int)iv[q].y);
+      rows_pf[4 * q + 2] = __builtin_amdgcn_readfirstlane((int)iv[q].z);
+      rows_pf[4 * q + 3] = __builtin_amdgcn_readfirstlane((int)iv[q].w);
     }
   };
   auto dma_w = [&](auto st) {
@@ -300,10 +321,11 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
     dma_w(S0{});
     load_rows(c_begin + 1);
     dma_raw(S1{}, c_begin + 1);
+    dma_ids(c_begin + 2);
+    dma_ids(c_begin + 3);
     dma_w(S1{});
-    load_rows(c_begin + 2);
     dma_raw(S2{}, c_begin + 2);
-    wait_vmcnt_lgkm0<2 * (RDMA + 1) + WROWS>();
+    wait_vmcnt_lgkm0<2 * (RDMA + 1) + WROWS + 2>();
     stage_barrier();
     ProdIn in0;
     produce_load(S0{}, in0);
@@ -317,8 +339,12 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
         // coefficient writes of the previous iteration are complete.
         wait_vmcnt_lgkm0<PER_ITER>();
         stage_barrier();
-        // The producer's reads of chunk cu + 1 go first (consumed while the
-        // first k-step's MFMAs run), then the fragments of chunk cu...
+        // The row ids of chunk cu + 2 (landed: requested before the W rows of
+        // chunk cu) and the producer's reads of chunk cu + 1 go first
+        // (consumed while the first k-step's MFMAs run), then the fragments of
+        // chunk cu...
+        u32x4_t idv[WROWS / 4];
+        read_ids(cu + 2, idv);
         ProdIn pin;
         produce_load(std::integral_constant<int, (u + 1) % 3>{}, pin);
         const uint32_t wb = lds_addr(dx_w<u>()) + a_lane;
@@ -343,13 +369,15 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
         // ... then later chunks' loads; the next coefficients are produced
         // while the first k-step's MFMAs run.
         dma_raw(std::integral_constant<int, u>{}, cu + 3);
-        dma_w(std::integral_constant<int, (u + 2) % 3>{});
-        load_rows(cu + 3);
+        dma_ids(cu + 4);
         static_for<0, 2>([&](auto kq) {
           constexpr int kk = decltype(kq)::value;
           if constexpr (kk == 0) {
             lgkm_wait<10>(alo[0][0], alo[0][1], alo[0][2], alo[0][3], ahi[0][0], ahi[0][1],
-                          ahi[0][2], ahi[0][3], bq[0][0], bq[0][1]);
+                          ahi[0][2], ahi[0][3], bq[0][0], bq[0][1], idv);
+            // W rows of chunk cu + 2, from the ids read above.
+            rows_of(idv);
+            dma_w(std::integral_constant<int, (u + 2) % 3>{});
           } else {
             produce_store(std::integral_constant<int, (u + 1) % 3>{}, cu + 1, pin);
             lgkm_wait<0>(alo[1][0], alo[1][1], alo[1][2], alo[1][3], ahi[1][0], ahi[1][1],
@@ -389,12 +417,20 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
 // Row scales of the logit store: gscale[g][n] = 2^(m_gn - lse_n log2 e), so that
 // E * gscale is the softmax probability (0 for rows past the batch).  Groups
 // past |S| are never read and are skipped.
+// Also writes the padded copy of the active row ids that the dX kernel reads
+// a chunk at a time: act_pad[j] = active[min(j, |S| - 1)] (0 if S is empty).
 __global__ void __launch_bounds__(256) k_scales(const float* __restrict__ gmax,
                                                 const float* __restrict__ row_lse, int B,
                                                 int64_t ld_g, int64_t n_groups,
                                                 const int32_t* __restrict__ n_active_p,
-                                                float* __restrict__ gscale) {
+                                                float* __restrict__ gscale,
+                                                const int32_t* __restrict__ active,
+                                                int32_t* __restrict__ act_pad, int64_t n_pad) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n_pad) {
+    const int64_t K = *n_active_p;
+    act_pad[i] = K > 0 ? active[i < K ? i : K - 1] : 0;
+  }
   if (i >= n_groups * ld_g) return;
   const int64_t g = i / ld_g;
   const int n = (int)(i - g * ld_g);
@@ -1120,9 +1156,10 @@ void launch_bwd16(const StepArgs& a, const StepWs& w, const Margin& mg, float sB
   timing_start(4, stream);
   // Row scales of the logit store from the lse the gradient is normalised with.
   hipLaunchKernelGGL(k_scales, dim3((unsigned)ceil_div(w.n_groups * w.ld_g, 256)), dim3(256), 0,
-                     stream, w.gmax, a.row_lse, B, w.ld_g, w.n_groups, a.n_active, w.gscale);
+                     stream, w.gmax, a.row_lse, B, w.ld_g, w.n_groups, a.n_active, w.gscale,
+                     a.active, w.act_pad, w.n_act_pad);
   hipLaunchKernelGGL((k_dx16<Tag, WI>), dim3((unsigned)(8 * per_xcd)), dim3(128 * WI), 0, stream,
-                     (const uint16_t*)a.W, a.active, a.n_active, w.inv_w, w.inv_w_max,
+                     (const uint16_t*)a.W, w.act_pad, a.n_active, w.inv_w, w.inv_w_max,
                      (const uint16_t*)w.lbuf, w.ld_cos, w.gscale, w.ld_g, B, n_rt, w.n_split,
                      n_tiles, per_xcd, w.dx_part);
   timing_stop(4, stream);
