@@ -191,7 +191,7 @@ int pfc_sample(const int64_t* labels, int64_t B, int64_t C, int64_t class_offset
   if (ws_bytes < L.sample_bytes) return PFC_ERR_WORKSPACE;
   (void)hipGetLastError();
   const hipError_t e = launch_sample(labels, B, C, class_offset, budget_of(r, C), seed, L.top_bits,
-                                     L.n_groups, sample_ws(ws, L), active, n_active,
+                                     L.n_groups, sample_ws(ws, L), active, active_cap, n_active,
                                      labels_mapped, (hipStream_t)stream);
   return e == hipSuccess ? PFC_OK : PFC_ERR_HIP;
 }

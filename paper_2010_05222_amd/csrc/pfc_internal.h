@@ -96,7 +96,7 @@ StepWs step_ws(void* ws, const WsLayout& L);
 hipError_t launch_sample(const int64_t* labels, int64_t B, int64_t C,
                          int64_t a, int64_t budget, uint64_t seed,
                          int top_bits, int64_t n_groups, const SampleWs& w,
-                         int32_t* active, int32_t* n_active,
+                         int32_t* active, int64_t cap, int32_t* n_active,
                          int32_t* labels_mapped, hipStream_t stream);
 
 struct StepArgs {

@@ -130,9 +130,15 @@ __device__ uint64_t block_exclusive_scan64(uint64_t v, uint64_t* smem, uint64_t*
 
 // Find the bin holding the k-th (1-based) element of an LDS histogram of
 // `nbins` bins (nbins a multiple of blockDim.x).  Returns through shared
-// out[0] = bin, out[1] = count before the bin, out[2] = count of the bin.
+// out[0] = bin, out[1] = count before the bin, out[2] = count of the bin
+// (the last bin and zero counts if the histogram holds fewer than k).
 __device__ void find_kth_bin(const uint32_t* hist, int nbins, int64_t k,
                              uint64_t* scan_smem, int64_t* out) {
+  if (threadIdx.x == 0) {   // ordered before the writes below by the scan's barriers
+    out[0] = nbins - 1;
+    out[1] = 0;
+    out[2] = 0;
+  }
   const int per = nbins / blockDim.x;
   const int b0 = threadIdx.x * per;
   uint64_t local = 0;
@@ -402,7 +408,8 @@ __global__ void __launch_bounds__(kCompactThreads) k_compact_count(
 __global__ void __launch_bounds__(1024) k_compact_scan(const uint32_t* grp_sure,
                                                        const uint32_t* grp_tie,
                                                        int64_t n_groups, const SampleState* st,
-                                                       uint32_t* grp_out, uint32_t* grp_tie_off,
+                                                       int64_t cap, uint32_t* grp_out,
+                                                       uint32_t* grp_tie_off,
                                                        int32_t* n_active) {
   constexpr int PER = 4;
   __shared__ uint64_t smem[16];
@@ -449,7 +456,8 @@ __global__ void __launch_bounds__(1024) k_compact_scan(const uint32_t* grp_sure,
     carry_tie += tile_tie;
     carry_sel += tile_sel;
   }
-  if (threadIdx.x == 0) *n_active = (int32_t)carry_sel;
+  // |S| <= cap by construction; the clamp keeps every later index in bounds.
+  if (threadIdx.x == 0) *n_active = (int32_t)(carry_sel < (uint64_t)cap ? carry_sel : cap);
 }
 
 // Exclusive class-order prefix of the flag bits over the workgroup, where
@@ -483,7 +491,7 @@ __device__ __forceinline__ void ordered_ranks(uint32_t flags, uint32_t* wave_tot
 
 __global__ void __launch_bounds__(kCompactThreads) k_compact_write(
     const uint16_t* digits, const uint32_t* bitmap, int64_t C, uint64_t seed, int64_t a,
-    const SampleState* st, const uint32_t* grp_out, const uint32_t* grp_tie_off,
+    const SampleState* st, const uint32_t* grp_out, const uint32_t* grp_tie_off, int64_t cap,
     int32_t* active) {
   __shared__ uint32_t smem[kCompactThreads / 64];
   const int64_t c0 = ((int64_t)blockIdx.x * kCompactThreads + threadIdx.x) * 4;
@@ -502,7 +510,7 @@ __global__ void __launch_bounds__(kCompactThreads) k_compact_write(
   const int64_t out_base = grp_out[blockIdx.x];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
-    if ((sel >> i) & 1u) active[out_base + srank[i]] = (int32_t)(c0 + i);
+    if (((sel >> i) & 1u) && out_base + srank[i] < cap) active[out_base + srank[i]] = (int32_t)(c0 + i);
 }
 
 __global__ void k_remap(const int64_t* labels, int64_t B, int64_t C, int64_t a,
@@ -529,7 +537,7 @@ __global__ void k_remap(const int64_t* labels, int64_t B, int64_t C, int64_t a,
 
 hipError_t launch_sample(const int64_t* labels, int64_t B, int64_t C, int64_t a,
                          int64_t budget, uint64_t seed, int top_bits, int64_t n_groups,
-                         const SampleWs& w, int32_t* active, int32_t* n_active,
+                         const SampleWs& w, int32_t* active, int64_t cap, int32_t* n_active,
                          int32_t* labels_mapped, hipStream_t stream) {
   timing_start(0, stream);
   const int64_t nwords = ceil_div(C, 32);
@@ -550,9 +558,10 @@ hipError_t launch_sample(const int64_t* labels, int64_t B, int64_t C, int64_t a,
   hipLaunchKernelGGL(k_compact_count, dim3((unsigned)n_groups), dim3(kCompactThreads), 0, stream,
                      w.digits, w.bitmap, C, seed, a, w.state, w.grp_sure, w.grp_tie);
   hipLaunchKernelGGL(k_compact_scan, dim3(1), dim3(1024), 0, stream, w.grp_sure, w.grp_tie,
-                     n_groups, w.state, w.grp_out, w.grp_tie_off, n_active);
+                     n_groups, w.state, cap, w.grp_out, w.grp_tie_off, n_active);
   hipLaunchKernelGGL(k_compact_write, dim3((unsigned)n_groups), dim3(kCompactThreads), 0, stream,
-                     w.digits, w.bitmap, C, seed, a, w.state, w.grp_out, w.grp_tie_off, active);
+                     w.digits, w.bitmap, C, seed, a, w.state, w.grp_out, w.grp_tie_off, cap,
+                     active);
   hipLaunchKernelGGL(k_remap, dim3((unsigned)ceil_div(B, 256)), dim3(256), 0, stream, labels, B,
                      C, a, active, n_active, labels_mapped);
   timing_stop(0, stream);
