@@ -432,7 +432,10 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
   wait_lgkm0();
   stage_barrier();
   // Wave w writes rows 32 w .. 32 w + 31, two rows (2 x 512 B) per store;
-  // all of its LDS reads are issued before the first store.
+  // all of its LDS reads are issued before the first store.  The stores are
+  // non-temporal: the logit store is read back only by later kernels, after
+  // gigabytes of other traffic, so it should not take L2 space from the
+  // operands this kernel re-reads.
   {
     const int b = lane & 31;
     u32x4_t v[16];
@@ -447,8 +450,8 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
       const int r = 32 * wave + 2 * i + (lane >> 5);
       const int n = n0 + r;
       if (n < B)
-        *reinterpret_cast<uint4*>(lbuf + (int64_t)n * ld_cos + j0 + 8 * b) =
-            make_uint4(v[i].x, v[i].y, v[i].z, v[i].w);
+        __builtin_nontemporal_store(
+            v[i], reinterpret_cast<u32x4_t*>(lbuf + (int64_t)n * ld_cos + j0 + 8 * b));
     }
   }
   if (tid < kFwdBN) {
