@@ -83,6 +83,15 @@ def test_f16_d512_zero_momentum(dev):
     _case(dev, 260, 512, 12000, 0.1, "f16", "arcface", 0.5, seed=5, random_m=False)
 
 
+def test_f16_d512_master(dev):
+    # fp16 weights with an fp32 master at d = 512; |S| = 910, B ragged.
+    _case(dev, 190, 512, 9100, 0.1, "f16", "cosface", 0.4, seed=18, master=True)
+
+
+def test_f16_d128(dev):
+    _case(dev, 150, 128, 4100, 0.1, "f16", "cosface", 0.4, seed=19)
+
+
 def test_positives_exceed_budget(dev):
     out = _case(dev, 512, 128, 1000, 0.05, "bf16", "cosface", 0.4, seed=6)
     assert out["K"] == out["n_pos"] > 50
