@@ -426,18 +426,27 @@ __global__ void __launch_bounds__(256) k_scales(const float* __restrict__ gmax,
                                                 float* __restrict__ gscale,
                                                 const int32_t* __restrict__ active,
                                                 int32_t* __restrict__ act_pad, int64_t n_pad) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  // Four consecutive entries per thread (ld_g and n_pad are multiples of 4,
+  // so the four rows share one group and the 16-byte accesses are aligned).
+  const int64_t i = 4 * ((int64_t)blockIdx.x * blockDim.x + threadIdx.x);
+  const int64_t K = *n_active_p;
   if (i < n_pad) {
-    const int64_t K = *n_active_p;
-    act_pad[i] = K > 0 ? active[i < K ? i : K - 1] : 0;
+    int o[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = K > 0 ? active[i + e < K ? i + e : K - 1] : 0;
+    *reinterpret_cast<int4*>(act_pad + i) = make_int4(o[0], o[1], o[2], o[3]);
   }
   if (i >= n_groups * ld_g) return;
   const int64_t g = i / ld_g;
   const int n = (int)(i - g * ld_g);
-  if (g * kLogitGroup >= (int64_t)*n_active_p) return;
-  float v = 0.0f;
-  if (n < B) v = __builtin_amdgcn_exp2f(gmax[i] - row_lse[n] * kLog2e);
-  gscale[i] = v;
+  if (g * kLogitGroup >= K) return;
+  const float4 m4 = *reinterpret_cast<const float4*>(gmax + i);
+  const float mv[4] = {m4.x, m4.y, m4.z, m4.w};
+  float v[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    v[e] = n + e < B ? __builtin_amdgcn_exp2f(mv[e] - row_lse[n + e] * kLog2e) : 0.0f;
+  *reinterpret_cast<float4*>(gscale + i) = make_float4(v[0], v[1], v[2], v[3]);
 }
 
 // Sum the split partials of a row in split order, add the row's target term
@@ -1155,7 +1164,7 @@ void launch_bwd16(const StepArgs& a, const StepWs& w, const Margin& mg, float sB
   const int64_t per_xcd = ceil_div(n_tiles, 8);
   timing_start(4, stream);
   // Row scales of the logit store from the lse the gradient is normalised with.
-  hipLaunchKernelGGL(k_scales, dim3((unsigned)ceil_div(w.n_groups * w.ld_g, 256)), dim3(256), 0,
+  hipLaunchKernelGGL(k_scales, dim3((unsigned)ceil_div(w.n_groups * w.ld_g, 4 * 256)), dim3(256), 0,
                      stream, w.gmax, a.row_lse, B, w.ld_g, w.n_groups, a.n_active, w.gscale,
                      a.active, w.act_pad, w.n_act_pad);
   hipLaunchKernelGGL((k_dx16<Tag, WI>), dim3((unsigned)(8 * per_xcd)), dim3(128 * WI), 0, stream,
