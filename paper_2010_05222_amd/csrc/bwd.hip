@@ -511,9 +511,9 @@ __global__ void __launch_bounds__(256) k_dx_final(
 // D = 128 * WI; eight waves, two per SIMD: wave w owns d entries
 // [D/4 (w % 4), +D/4) and classes [64 (w / 4), +64) of the workgroup (MB x 2
 // accumulator tiles of 32 x 32), so that a SIMD's second wave issues while
-// the first waits at a barrier or on its loads.  Both MFMA operands are K-major in LDS, so every fragment
-// is one 16-byte read: X^T from the transposed bf16 copy of the batch, and G^T
-// written by the producer.
+// the first waits at a barrier or on its loads.  Both MFMA operands are
+// K-major in LDS, so every fragment is one 16-byte read: X^T from the
+// transposed bf16 copy of the batch, and G^T written by the producer.
 // Pipeline per chunk c (32 batch rows): raw logit-store values and row
 // scales of chunk c + 3 and X^T of chunk c + 2 requested, coefficients of
 // chunk c + 1 produced, chunk c contracted.  The second k-step of chunk c is
