@@ -74,7 +74,7 @@ WsLayout ws_layout(int64_t B, int64_t d, int64_t C, int64_t cap, int compute) {
   L.off_bitmap = take((size_t)ceil_div(C, 32) * 4);
   L.off_hist = take((size_t)(1 << kTopBitsMax) * 4);
   L.off_state = take(sizeof(SampleState));
-  L.off_digits = take((size_t)round_up(C, 4) * 2);   // read four at a time
+  L.off_digits = take((size_t)round_up(C, kCompactPer) * 2);   // read 16 at a time
   L.off_cand = take((size_t)C * 4);
   L.off_cand_key = take((size_t)C * 8);
   L.off_grp_sure = take((size_t)L.n_groups * 4);

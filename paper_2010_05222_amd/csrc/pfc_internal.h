@@ -25,7 +25,8 @@ struct SampleState {
 
 // Compaction works on groups of kCompactClasses consecutive classes.
 constexpr int kCompactThreads = 256;
-constexpr int kCompactClasses = 4 * kCompactThreads;
+constexpr int kCompactPer = 16;   // classes per thread
+constexpr int kCompactClasses = kCompactPer * kCompactThreads;
 constexpr int kTopBitsMax = 12;
 
 struct SampleWs {

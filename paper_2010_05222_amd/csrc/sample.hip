@@ -71,6 +71,18 @@ __device__ __forceinline__ bool is_positive(const uint32_t* bitmap, int64_t c) {
   return (bitmap[c >> 5] >> (c & 31)) & 1u;
 }
 
+// Digits of the 16 classes c0 .. c0 + 15 (c0 a multiple of 16; the digit
+// array is padded to whole groups of 16): two 16-byte loads.
+__device__ __forceinline__ void load_digits16(const uint16_t* digits, int64_t c0, uint32_t (&w)[8]) {
+  const uint4 d0 = *reinterpret_cast<const uint4*>(digits + c0);
+  const uint4 d1 = *reinterpret_cast<const uint4*>(digits + c0 + 8);
+  w[0] = d0.x; w[1] = d0.y; w[2] = d0.z; w[3] = d0.w;
+  w[4] = d1.x; w[5] = d1.y; w[6] = d1.z; w[7] = d1.w;
+}
+__device__ __forceinline__ uint32_t digit_of(const uint32_t (&w)[8], int i) {
+  return (w[i >> 1] >> (16 * (i & 1))) & 0xFFFFu;
+}
+
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 
 __device__ __forceinline__ uint32_t popc_below(uint64_t mask) {
@@ -268,38 +280,42 @@ __global__ void __launch_bounds__(1024) k_select_top(const uint32_t* hist, int t
 }
 
 // Collect the non-positive classes whose key's top bits equal the bucket,
-// with their full keys.
+// with their full keys: kCompactPer classes per thread, one slot reservation
+// per wave.
 __global__ void __launch_bounds__(256) k_collect(const uint16_t* digits, const uint32_t* bitmap,
                                                  int64_t C, uint64_t seed, int64_t a,
                                                  SampleState* st, uint32_t* cand,
                                                  uint64_t* cand_key) {
   if (st->mode != kSelectKeys) return;
   const uint32_t digit = st->top_digit;
-  const int64_t c0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
-  // c0 is a multiple of 4: one bitmap word and one 8-byte digit word.
-  uint32_t pos = 0xFu;
-  uint64_t dg4 = 0;
+  const int64_t c0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * kCompactPer;
+  uint32_t take = 0;
   if (c0 < C) {
-    pos = (bitmap[c0 >> 5] >> (c0 & 31)) & 0xFu;
-    dg4 = *reinterpret_cast<const uint64_t*>(digits + c0);
+    const uint32_t pos = (bitmap[c0 >> 5] >> (c0 & 31)) & 0xFFFFu;
+    uint32_t w[8];
+    load_digits16(digits, c0, w);
+#pragma unroll
+    for (int i = 0; i < kCompactPer; ++i)
+      if (c0 + i < C && digit_of(w, i) == digit && !((pos >> i) & 1u)) take |= 1u << i;
   }
-  // Not unrolled: one copy of the key generator.
-#pragma unroll 1
-  for (int i = 0; i < 4; ++i) {
-    const int64_t c = c0 + i;
-    bool take = false;
-    if (c < C) take = ((uint32_t)(dg4 >> (16 * i)) & 0xFFFFu) == digit && !((pos >> i) & 1u);
-    const uint64_t mask = __ballot(take);
-    if (mask == 0) continue;
-    uint32_t base = 0;
-    const int leader = __ffsll((unsigned long long)mask) - 1;
-    if (lane_id() == leader) base = atomicAdd(&st->cand_count, (uint32_t)__popcll(mask));
-    base = __shfl(base, leader, 64);
-    if (take) {
-      const uint32_t slot = base + popc_below(mask);
-      cand[slot] = (uint32_t)c;
-      cand_key[slot] = class_key(seed, a, c);
-    }
+  const uint32_t n = (uint32_t)__popc(take);
+  if (__ballot(n != 0) == 0) return;
+  // The wave's exclusive prefix of the counts, and one reservation by lane 63.
+  uint32_t incl = n;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t v = __shfl_up(incl, off, 64);
+    if (lane_id() >= off) incl += v;
+  }
+  uint32_t base = 0;
+  if (lane_id() == 63) base = atomicAdd(&st->cand_count, incl);
+  base = __shfl(base, 63, 64) + incl - n;
+  while (take) {
+    const int i = __ffs(take) - 1;
+    take &= take - 1;
+    cand[base] = (uint32_t)(c0 + i);
+    cand_key[base] = class_key(seed, a, c0 + i);
+    ++base;
   }
 }
 
@@ -339,9 +355,9 @@ __global__ void __launch_bounds__(1024) k_refine(const uint64_t* cand_key, int t
   }
 }
 
-// Per class of one thread: bit i of `sure` / `tie` for class c0 + i.  The
-// threshold's top-bit digit decides every class outside its bucket; a class
-// inside compares its recomputed key.
+// Per class of one thread: bit i of `sure` / `tie` for class c0 + i
+// (i < kCompactPer).  The threshold's top-bit digit decides every class
+// outside its bucket; a class inside compares its recomputed key.
 __device__ __forceinline__ void class_flags(const uint16_t* digits, const uint32_t* bitmap,
                                             int64_t C, uint64_t seed, int64_t a,
                                             const SampleState* st, int64_t c0, uint32_t* sure,
@@ -354,19 +370,19 @@ __device__ __forceinline__ void class_flags(const uint16_t* digits, const uint32
     *tie = 0;
     return;
   }
-  // c0 is a multiple of 4: one bitmap word holds the four classes' bits, and
-  // their four digits are one 8-byte word (the digit array is padded).
-  const uint32_t pos = (bitmap[c0 >> 5] >> (c0 & 31)) & 0xFu;
-  const uint64_t dg4 = mode == kSelectKeys ? *reinterpret_cast<const uint64_t*>(digits + c0) : 0;
+  // c0 is a multiple of 16: one bitmap word holds the classes' bits.
+  const uint32_t pos = (bitmap[c0 >> 5] >> (c0 & 31)) & 0xFFFFu;
+  uint32_t w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  if (mode == kSelectKeys) load_digits16(digits, c0, w);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < kCompactPer; ++i) {
     if (c0 + i >= C) continue;
     if ((pos >> i) & 1u) {
       s |= 1u << i;
     } else if (mode == kSelectAll) {
       s |= 1u << i;
     } else if (mode == kSelectKeys) {
-      const uint32_t dg = (uint32_t)(dg4 >> (16 * i)) & 0xFFFFu;
+      const uint32_t dg = digit_of(w, i);
       if (dg < top) s |= 1u << i;
       else if (dg == top) need |= 1u << i;
     }
@@ -390,7 +406,7 @@ __global__ void __launch_bounds__(kCompactThreads) k_compact_count(
     const uint16_t* digits, const uint32_t* bitmap, int64_t C, uint64_t seed, int64_t a,
     const SampleState* st, uint32_t* grp_sure, uint32_t* grp_tie) {
   __shared__ uint32_t smem[kCompactThreads / 64];
-  const int64_t c0 = ((int64_t)blockIdx.x * kCompactThreads + threadIdx.x) * 4;
+  const int64_t c0 = ((int64_t)blockIdx.x * kCompactThreads + threadIdx.x) * kCompactPer;
   uint32_t s, t;
   class_flags(digits, bitmap, C, seed, a, st, c0, &s, &t);
   uint32_t tot_s, tot_t;
@@ -460,57 +476,35 @@ __global__ void __launch_bounds__(1024) k_compact_scan(const uint32_t* grp_sure,
   if (threadIdx.x == 0) *n_active = (int32_t)(carry_sel < (uint64_t)cap ? carry_sel : cap);
 }
 
-// Exclusive class-order prefix of the flag bits over the workgroup, where
-// thread t owns classes 4t .. 4t+3: per-class rank in bit order, via one
-// wavefront ballot per class slot plus a cross-wave offset.
-__device__ __forceinline__ void ordered_ranks(uint32_t flags, uint32_t* wave_tot_smem,
-                                              uint32_t rank[4], uint32_t* total) {
-  uint32_t before_lanes = 0;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) before_lanes += popc_below(__ballot((flags >> i) & 1u));
-  const uint32_t mine = (uint32_t)__popc(flags);
-  // Wave total = before_lanes of lane 63 + its own count.
-  const int wave = threadIdx.x >> 6;
-  if (lane_id() == 63) wave_tot_smem[wave] = before_lanes + mine;
-  __syncthreads();
-  uint32_t wave_off = 0, sum = 0;
-  for (int w = 0; w < (int)(blockDim.x >> 6); ++w) {
-    const uint32_t t = wave_tot_smem[w];
-    if (w < wave) wave_off += t;
-    sum += t;
-  }
-  __syncthreads();
-  uint32_t r = wave_off + before_lanes;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    rank[i] = r;
-    r += (flags >> i) & 1u;
-  }
-  *total = sum;
-}
-
 __global__ void __launch_bounds__(kCompactThreads) k_compact_write(
     const uint16_t* digits, const uint32_t* bitmap, int64_t C, uint64_t seed, int64_t a,
     const SampleState* st, const uint32_t* grp_out, const uint32_t* grp_tie_off, int64_t cap,
     int32_t* active) {
   __shared__ uint32_t smem[kCompactThreads / 64];
-  const int64_t c0 = ((int64_t)blockIdx.x * kCompactThreads + threadIdx.x) * 4;
+  const int64_t c0 = ((int64_t)blockIdx.x * kCompactThreads + threadIdx.x) * kCompactPer;
   uint32_t s, t;
   class_flags(digits, bitmap, C, seed, a, st, c0, &s, &t);
-  uint32_t trank[4], ttot;
-  ordered_ranks(t, smem, trank, &ttot);
-  const int64_t tie_base = grp_tie_off[blockIdx.x];
+  // Class-order ranks: thread t owns classes kCompactPer t .. + kCompactPer - 1,
+  // so a class's rank is the block's exclusive prefix of the per-thread
+  // counts plus the bits below it in the thread.
+  uint32_t ttot;
+  const uint32_t tpre = block_exclusive_scan((uint32_t)__popc(t), smem, &ttot);
+  const int64_t tie_base = (int64_t)grp_tie_off[blockIdx.x] + tpre;
   const int64_t k_rem = st->k_rem;
   uint32_t sel = s;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-    if (((t >> i) & 1u) && tie_base + (int64_t)trank[i] < k_rem) sel |= 1u << i;
-  uint32_t srank[4], stot;
-  ordered_ranks(sel, smem, srank, &stot);
-  const int64_t out_base = grp_out[blockIdx.x];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-    if (((sel >> i) & 1u) && out_base + srank[i] < cap) active[out_base + srank[i]] = (int32_t)(c0 + i);
+  for (int i = 0; i < kCompactPer; ++i)
+    if (((t >> i) & 1u) && tie_base + __popc(t & ((1u << i) - 1u)) < k_rem) sel |= 1u << i;
+  uint32_t stot;
+  const uint32_t spre = block_exclusive_scan((uint32_t)__popc(sel), smem, &stot);
+  const int64_t out_base = (int64_t)grp_out[blockIdx.x] + spre;
+  uint32_t rest = sel;
+  while (rest) {
+    const int i = __ffs(rest) - 1;
+    rest &= rest - 1;
+    const int64_t o = out_base + __popc(sel & ((1u << i) - 1u));
+    if (o < cap) active[o] = (int32_t)(c0 + i);
+  }
 }
 
 __global__ void k_remap(const int64_t* labels, int64_t B, int64_t C, int64_t a,
@@ -552,7 +546,7 @@ hipError_t launch_sample(const int64_t* labels, int64_t B, int64_t C, int64_t a,
   hipLaunchKernelGGL(k_keys_hist, dim3((unsigned)(hist_wgs < 512 ? hist_wgs : 512)), dim3(256), 0,
                      stream, seed, a, C, top_bits, w.bitmap, w.digits, w.hist, w.state);
   hipLaunchKernelGGL(k_select_top, dim3(1), dim3(1024), 0, stream, w.hist, top_bits, w.state);
-  hipLaunchKernelGGL(k_collect, dim3((unsigned)ceil_div(C, 1024)), dim3(256), 0, stream,
+  hipLaunchKernelGGL(k_collect, dim3((unsigned)ceil_div(C, 256 * kCompactPer)), dim3(256), 0, stream,
                      w.digits, w.bitmap, C, seed, a, w.state, w.cand, w.cand_key);
   hipLaunchKernelGGL(k_refine, dim3(1), dim3(1024), 0, stream, w.cand_key, top_bits, w.state);
   hipLaunchKernelGGL(k_compact_count, dim3((unsigned)n_groups), dim3(kCompactThreads), 0, stream,
