@@ -102,6 +102,7 @@ WsLayout ws_layout(int64_t B, int64_t d, int64_t C, int64_t cap, int compute) {
   const size_t cos_elt = compute == PFC_F32 ? 4 : 2;
   L.off_inv_x = take((size_t)B * 4);
   L.off_xb = take(compute == PFC_F32 ? 0 : (size_t)L.ld_xt * d * 2);
+  L.off_xblk = take(compute == PFC_F32 ? 0 : (size_t)L.ld_xt * d * 2);
   L.off_wmax = take(4);
   L.off_inv_w = take((size_t)L.ld_cos * 4);
   L.off_cos = take((size_t)B * L.ld_cos * cos_elt);
@@ -139,6 +140,7 @@ StepWs step_ws(void* ws, const WsLayout& L) {
   StepWs w;
   w.inv_x = (float*)(b + L.off_inv_x);
   w.xbT = b + L.off_xb;
+  w.xblk = b + L.off_xblk;
   w.ld_xt = L.ld_xt;
   w.inv_w_max = (float*)(b + L.off_wmax);
   w.inv_w = (float*)(b + L.off_inv_w);

@@ -74,11 +74,11 @@ __device__ __forceinline__ uint16_t* fwd_tile_row(int r) {
 // batch operand rows 16 (2 wave + u) + lane / 4 (u < 2).
 template <int S>
 __device__ __forceinline__ void fwd_issue(const uint16_t* const ap[4], const uint16_t* const bp[2],
-                                          int k0, int wave) {
+                                          int k0, int64_t kb, int wave) {
 #pragma unroll
   for (int u = 0; u < 4; ++u) dma16(ap[u] + k0, fwd_a<S>() + (4 * wave + u) * 16 * kFwdKC);
 #pragma unroll
-  for (int u = 0; u < 2; ++u) dma16(bp[u] + k0, fwd_b<S>() + (2 * wave + u) * 16 * kFwdKC);
+  for (int u = 0; u < 2; ++u) dma16(bp[u] + kb, fwd_b<S>() + (2 * wave + u) * 16 * kFwdKC);
 }
 
 // a0^2 + a1^2 + acc for a packed pair of 16-bit values (v_dot2_f32_*).
@@ -273,10 +273,12 @@ __device__ __forceinline__ void fwd_epilogue_rows_plain(f32x16_t (&acc)[4][2], i
 // s c log2 e (the margined logit at the target, which also goes to tgt[n],
 // its cosine to tgtc[n]); per (row, 128-class group) the maximum m, written
 // to gmax, and E = 2^(f - m) in fp16; per (row, class tile) the pair
-// (max, sum E), merged by k_lse16.
+// (max, sum E), merged by k_lse16.  The batch operand comes from the
+// column-blocked copy of X (block k = [ld_xb][32]), so a stage's 128 batch
+// rows are one contiguous 8 KB run.
 template <typename Tag, int NK, bool FILT>
 __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
-    const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
+    const uint16_t* __restrict__ Xb, int64_t ld_xb, const uint16_t* __restrict__ W,
     const int32_t* __restrict__ active, const int32_t* __restrict__ n_active_p,
     const int32_t* __restrict__ yhat, const float* __restrict__ inv_x,
     float* __restrict__ inv_w, float* __restrict__ inv_w_max, int B, int64_t ld_cos,
@@ -314,7 +316,7 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
   for (int u = 0; u < 2; ++u) {
     const int row = 16 * (2 * wave + u) + (lane >> 2);
     const int nr = n0 + row < B ? n0 + row : B - 1;
-    bp[u] = X + (int64_t)nr * D + 8 * cidx;
+    bp[u] = Xb + (int64_t)nr * kFwdKC + 8 * cidx;
   }
 
   f32x16_t acc[4][2];
@@ -337,8 +339,8 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
 
   float wss[4] = {0.0f, 0.0f, 0.0f, 0.0f};  // partial ||w||^2 of the lane's class rows
   constexpr int kPerStage = 6;  // DMAs per thread per stage
-  fwd_issue<0>(ap, bp, 0, wave);
-  if constexpr (NK > 1) fwd_issue<1>(ap, bp, kFwdKC, wave);
+  fwd_issue<0>(ap, bp, 0, 0, wave);
+  if constexpr (NK > 1) fwd_issue<1>(ap, bp, kFwdKC, (int64_t)kFwdKC * ld_xb, wave);
   static_for<0, NK>([&](auto cc) {
     constexpr int c = decltype(cc)::value;
     constexpr int ahead = (NK - 1 - c) < 1 ? (NK - 1 - c) : 1;
@@ -346,7 +348,7 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
     // have, and every wave is done with chunk c - 1, whose stage is refilled.
     wait_vmcnt<kPerStage * ahead>();
     stage_barrier();
-    if constexpr (c + 2 < NK) fwd_issue<(c + 2) % 3>(ap, bp, (c + 2) * kFwdKC, wave);
+    if constexpr (c + 2 < NK) fwd_issue<(c + 2) % 3>(ap, bp, (c + 2) * kFwdKC, (int64_t)(c + 2) * kFwdKC * ld_xb, wave);
     fwd_compute<c % 3, Tag>(acc, wm, wn, lane, wss);
   });
 
@@ -576,13 +578,13 @@ void launch_fwd16_nk(unsigned grid, hipStream_t stream, const StepArgs& a, const
                      int n_rt, int64_t n_tiles, int64_t per_xcd, const Margin& mg) {
   if (a.tau < 1.0f)
     hipLaunchKernelGGL((k_fwd16<Tag, NK, true>), dim3(grid), dim3(kFwdThreads), 0, stream,
-                       (const uint16_t*)a.X, (const uint16_t*)a.W, a.active, a.n_active,
+                       (const uint16_t*)w.xblk, w.ld_xt, (const uint16_t*)a.W, a.active, a.n_active,
                        a.labels_mapped, w.inv_x, w.inv_w, w.inv_w_max, B, w.ld_cos, w.n_ctiles,
                        n_rt, n_tiles, per_xcd, mg, a.tau, (uint16_t*)w.lbuf, w.stats, w.tgt,
                        w.tgtc, w.gmax, w.ld_g);
   else
     hipLaunchKernelGGL((k_fwd16<Tag, NK, false>), dim3(grid), dim3(kFwdThreads), 0, stream,
-                       (const uint16_t*)a.X, (const uint16_t*)a.W, a.active, a.n_active,
+                       (const uint16_t*)w.xblk, w.ld_xt, (const uint16_t*)a.W, a.active, a.n_active,
                        a.labels_mapped, w.inv_x, w.inv_w, w.inv_w_max, B, w.ld_cos, w.n_ctiles,
                        n_rt, n_tiles, per_xcd, mg, a.tau, (uint16_t*)w.lbuf, w.stats, w.tgt,
                        w.tgtc, w.gmax, w.ld_g);

@@ -55,6 +55,9 @@ struct StepWs {
   void* xbT;             // [ld_xt / 32][d][32] x_hat (normalised rows) transposed in blocks of
                          // 32 rows, bf16, zero past B (the class-gradient operand)
   int64_t ld_xt;         // B rounded up to 32
+  void* xblk;            // [d / 32][ld_xt][32] the raw 16-bit batch rows in 32-wide column
+                         // blocks, zero past B (the forward's batch operand: one block is
+                         // a contiguous run of whole rows)
   float* inv_w_max;      // [1] max_j 1/||W[S_j]|| (scale of the fp16 feature-gradient operand)
   float* inv_w;          // [ld_cos] 1/max(||W[S_j]||, eps), 0 past |S| within the last tile
   void* lbuf;            // [B x ld_cos] logit store.  16-bit paths: fp16 E = 2^(f log2 e - m)
@@ -83,7 +86,7 @@ struct WsLayout {
   size_t sample_bytes;   // prefix used by the sampler
   size_t off_bitmap, off_hist, off_state, off_digits, off_cand, off_cand_key;
   size_t off_grp_sure, off_grp_tie, off_grp_out, off_grp_tie_off;
-  size_t off_inv_x, off_xb, off_wmax, off_inv_w, off_cos, off_stats, off_tgt, off_tgtc,
+  size_t off_inv_x, off_xb, off_xblk, off_wmax, off_inv_w, off_cos, off_stats, off_tgt, off_tgtc,
       off_gmax, off_gscale, off_dx, off_loss, off_act_pad;
   int64_t ld_cos, n_ctiles, n_groups, ld_xt, ld_g, n_lgroups, n_act_pad;
   int n_split;

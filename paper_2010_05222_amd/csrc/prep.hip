@@ -27,16 +27,19 @@ __device__ __forceinline__ float sumsq8(const uint4& v) {
   return acc;
 }
 
-// inv_x[n] and a transposed bf16 copy of the normalised batch x_hat in blocks
+// inv_x[n]; a transposed bf16 copy of the normalised batch x_hat in blocks
 // of 32 rows (block c = [d][32]: entry (i, r) = x_hat[32 c + r][i]), the
-// K-major operand of the class-gradient contraction; a workgroup transposes
-// one block through LDS.  Rows n in [B, ld_xt) are zero.  Also clears the
-// running max of 1/||w_j||.
+// K-major operand of the class-gradient contraction, which a workgroup
+// transposes through LDS; and the raw rows in 32-wide column blocks (block k
+// = [ld_xt][32]: entry (n, e) = X[n][32 k + e]), the forward's operand, whose
+// k-th chunk of a run of rows is then contiguous.  Rows n in [B, ld_xt) are
+// zero in both.  Also clears the running max of 1/||w_j||.
 constexpr int kPrepRows = 32;
 template <typename Tag>
 __global__ void __launch_bounds__(256) k_prep_x16(const uint16_t* __restrict__ X, int B, int d,
                                                   int64_t ld_xt, float* __restrict__ inv_x,
                                                   uint16_t* __restrict__ xbT,
+                                                  uint16_t* __restrict__ xblk,
                                                   float* __restrict__ inv_w_max) {
   __shared__ uint16_t tile[kPrepRows][512 + 8];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -51,6 +54,7 @@ __global__ void __launch_bounds__(256) k_prep_x16(const uint16_t* __restrict__ X
     const float ix = 1.0f / fmaxf(sqrtf(ss), kEpsNorm);
     if (lane == 0 && n < B) inv_x[n] = ix;
     if (c_ok) {
+      *reinterpret_cast<uint4*>(xblk + ((int64_t)(lane >> 2) * ld_xt + n) * 32 + 8 * (lane & 3)) = v;
       const uint16_t* h = reinterpret_cast<const uint16_t*>(&v);
       uint16_t o[8];
 #pragma unroll
@@ -119,11 +123,11 @@ hipError_t launch_prep(const StepArgs& a, const StepWs& w, hipStream_t stream) {
   } else if (a.dtype == 1) {
     hipLaunchKernelGGL(k_prep_x16<Bf16Tag>, dim3((unsigned)(w.ld_xt / kPrepRows)), dim3(256), 0,
                        stream, (const uint16_t*)a.X, B, d, w.ld_xt, w.inv_x, (uint16_t*)w.xbT,
-                       w.inv_w_max);
+                       (uint16_t*)w.xblk, w.inv_w_max);
   } else {
     hipLaunchKernelGGL(k_prep_x16<F16Tag>, dim3((unsigned)(w.ld_xt / kPrepRows)), dim3(256), 0,
                        stream, (const uint16_t*)a.X, B, d, w.ld_xt, w.inv_x, (uint16_t*)w.xbT,
-                       w.inv_w_max);
+                       (uint16_t*)w.xblk, w.inv_w_max);
   }
   timing_stop(1, stream);
   return hipGetLastError();
