@@ -194,6 +194,60 @@ typedef enum {
 int pfc_timing_begin(int kernel, int max_launches);
 int pfc_timing_end(double* total_ms /*host*/, int* launches /*host*/);
 
+/*
+ * Tiered class storage (Sec. 3.3.3, the paragraph on asynchronous
+ * hierarchical class storage, Fig. async_pipeline): the shard's class bank
+ * (W, momentum, and the fp32 master if any) lives in pinned host memory, and
+ * a step runs on a device SLOT holding only its active rows, slot row j being
+ * bank row active[j].  The step itself is the three calls above with the slot
+ * as W / momentum / W_master and an identity active list 0, 1, ..., cap - 1
+ * (the sampler's list stays in active space for these copies; labels_mapped is
+ * already a position in S).  With two slots and a side stream, the rows of
+ * step t+1 are staged while step t runs:
+ *   stage      cold rows, S(t+1) minus S(t), bank -> slot B (any time after the
+ *              write-back of the step that last used slot B);
+ *   patch      rows in both S(t) and S(t+1), slot A -> slot B, after step t's
+ *              update; slot B is ready for step t+1 after stage and patch;
+ *   writeback  slot A -> bank, after step t; slot A is free for step t+2
+ *              after the write-back.
+ * Each copy is a byte copy of `row_bytes` per row (a multiple of 16, at most
+ * 65536): d * 2 for 16-bit W, d * 4 for momentum and the master; one call per
+ * array.  active / next_active / prev_active are sorted ascending id lists of
+ * active_cap entries (pfc_sample's output) with their device counts n;
+ * entries past the count are ignored, and counts are clamped to [0, cap].
+ * Slots are [active_cap x row] device buffers.  Bank pointers (and
+ * bank_version) must be host memory allocated pinned and mapped (hipHostMalloc,
+ * or torch's pin_memory) or device memory; anything else - pageable host memory
+ * in particular - is PFC_ERR_INVALID_ARG, checked before any launch.
+ *
+ * Versions (optional, pass both or neither, on one of a step's stage calls):
+ * bank_version int32[C] (host, pinned) holds the version of each bank row's
+ * last write-back; row_version int32[C] (device) the version of each row's
+ * last staging, starting from all zeros on both sides.  stage stamps
+ * row_version[c] = version for every c in S(t+1), and a cold row whose
+ * bank_version differs from its row_version (an update of it not yet written
+ * back) adds 1 to stale[0]; writeback stamps bank_version[c] = version after
+ * the row's data.  Ids outside [0, C) are not copied and also add 1 to stale.
+ * stale (device int32[1]) may be NULL.  A caller uses version = t + 1 for the
+ * rows of step t.
+ */
+int pfc_bank_stage(const void* bank, int64_t C, int64_t row_bytes,
+                   const int32_t* next_active, const int32_t* next_n,
+                   const int32_t* prev_active /*or NULL*/,
+                   const int32_t* prev_n /*or NULL*/, int64_t active_cap,
+                   void* slot, const int32_t* bank_version /*host, or NULL*/,
+                   int32_t* row_version /*or NULL*/, int32_t version,
+                   int32_t* stale /*or NULL*/, void* stream);
+int pfc_bank_patch(const void* prev_slot, const int32_t* prev_active,
+                   const int32_t* prev_n, const int32_t* next_active,
+                   const int32_t* next_n, int64_t active_cap, int64_t row_bytes,
+                   void* next_slot, void* stream);
+int pfc_bank_writeback(const void* slot, const int32_t* active,
+                       const int32_t* n_active, int64_t active_cap,
+                       int64_t row_bytes, int64_t C, void* bank,
+                       int32_t* bank_version /*host, or NULL*/, int32_t version,
+                       void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -95,3 +95,161 @@ class PfcShard:
         self.sample(labels, seed)
         self.forward(X, W)
         self.backward(X, W, M, W_master)
+
+
+class TieredShard:
+    """A class shard whose bank lives in pinned host memory (Sec. 3.3.3, the
+    paragraph on asynchronous hierarchical class storage, Fig. async_pipeline).
+
+    The bank - W in the storage dtype, fp32 momentum, and an fp32 master when
+    `master` - holds all C rows (`W_bank`, `M_bank`, `P_bank`: pinned host
+    tensors the caller fills).  Each step runs on a device slot of `cap` rows
+    holding only its active rows; two slots alternate.  While step t runs on
+    slot A, a side stream samples step t+1 and stages its cold rows into slot
+    B; after step t's update the rows S(t) and S(t+1) share are patched from A
+    into B (which then becomes ready), and A is written back to the bank.
+    HIP events order the two streams; every copy is a libpfc kernel.
+
+        ts = TieredShard(B, d, C, r, ...)
+        ts.W_bank.copy_(W0); ts.M_bank.zero_()
+        ts.begin(labels[0], seeds[0])
+        for t in range(T):
+            out = ts.step(X[t], labels[t + 1] if t + 1 < T else None, seeds[t + 1] ...)
+            # out.loss, out.row_lse, out.dX belong to step t (valid on the
+            # current stream until step t + 2)
+        ts.finish()          # the bank holds every update
+        ts.stale_rows()      # 0 unless a cold row was staged before its write-back
+    """
+
+    def __init__(self, B, d, C, r, dtype="bf16", class_offset=0, s=64.0, m=0.5,
+                 margin="arcface", lr=0.1, mu=0.9, device="cuda:0", tau=None, master=False):
+        kw = dict(dtype=dtype, class_offset=class_offset, s=s, m=m, margin=margin, lr=lr, mu=mu,
+                  device=device, tau=tau)
+        self.parts = [PfcShard(B, d, C, r, **kw), PfcShard(B, d, C, r, **kw)]
+        p = self.parts[0]
+        self.B, self.d, self.C, self.cap, self.device = p.B, p.d, p.C, p.cap, p.device
+        dev, cap = self.device, self.cap
+        self.W_bank = torch.empty((C, d), dtype=p.tdtype, pin_memory=True)
+        self.M_bank = torch.zeros((C, d), dtype=torch.float32, pin_memory=True)
+        self.P_bank = torch.empty((C, d), dtype=torch.float32, pin_memory=True) if master else None
+        self.bank_version = torch.zeros(C, dtype=torch.int32, pin_memory=True)
+        self.row_version = torch.zeros(C, dtype=torch.int32, device=dev)
+        self.stale = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.slots = []
+        for _ in range(2):
+            sl = {"W": torch.empty((cap, d), dtype=p.tdtype, device=dev),
+                  "M": torch.empty((cap, d), dtype=torch.float32, device=dev)}
+            if master:
+                sl["P"] = torch.empty((cap, d), dtype=torch.float32, device=dev)
+            self.slots.append(sl)
+        self.banks = {"W": self.W_bank, "M": self.M_bank}
+        if master:
+            self.banks["P"] = self.P_bank
+        self.iota = torch.arange(cap, dtype=torch.int32, device=dev)
+        self.side = torch.cuda.Stream(device=dev)
+        self.ready = [torch.cuda.Event(), torch.cuda.Event()]
+        self.staged = [False, False]
+        self.t = 0
+
+    def _row_bytes(self, key):
+        return self.d * self.banks[key].element_size()
+
+    def _stage(self, nxt, prv, slot, version):
+        stream = self.side.cuda_stream
+        for key in ("M", "P", "W"):
+            if key not in slot:
+                continue
+            ver = key == "W"
+            abi.pfc_bank_stage(_ptr(self.banks[key]), self.C, self._row_bytes(key),
+                               _ptr(nxt.active), _ptr(nxt.n_active),
+                               _ptr(prv.active) if prv else 0, _ptr(prv.n_active) if prv else 0,
+                               self.cap, _ptr(slot[key]),
+                               _ptr(self.bank_version) if ver else 0,
+                               _ptr(self.row_version) if ver else 0, version,
+                               _ptr(self.stale) if ver else 0, stream)
+
+    def _patch(self, prv, src, nxt, dst):
+        for key in src:
+            abi.pfc_bank_patch(_ptr(src[key]), _ptr(prv.active), _ptr(prv.n_active),
+                               _ptr(nxt.active), _ptr(nxt.n_active), self.cap,
+                               self._row_bytes(key), _ptr(dst[key]), self.side.cuda_stream)
+
+    def _writeback(self, part, slot, version):
+        # The W rows go last and stamp the version, so a stamped row's
+        # momentum (and master) rows are already in the bank.
+        for key in ("M", "P", "W"):
+            if key not in slot:
+                continue
+            abi.pfc_bank_writeback(_ptr(slot[key]), _ptr(part.active), _ptr(part.n_active),
+                                   self.cap, self._row_bytes(key), self.C, _ptr(self.banks[key]),
+                                   _ptr(self.bank_version) if key == "W" else 0, version,
+                                   self.side.cuda_stream)
+
+    def _run_step(self, part, X, slot):
+        _require(X, part.tdtype, (self.B, self.d), "X", self.device)
+        stream = torch.cuda.current_stream(self.device).cuda_stream
+        tau = 2.0 if part.tau is None else part.tau
+        abi.pfc_forward_loss(_ptr(X), part.code, self.B, self.d, _ptr(slot["W"]), part.code,
+                             self.C, _ptr(self.iota), _ptr(part.n_active), self.cap,
+                             _ptr(part.labels_mapped), part.code, part.s, part.m, part.margin,
+                             tau, _ptr(part.loss), _ptr(part.row_lse), _ptr(part.ws),
+                             part.ws_bytes, stream)
+        abi.pfc_backward_update(_ptr(X), part.code, self.B, self.d, _ptr(slot["W"]), part.code,
+                                _ptr(slot.get("P")), _ptr(slot["M"]), self.C, _ptr(self.iota),
+                                _ptr(part.n_active), self.cap, _ptr(part.labels_mapped),
+                                part.code, part.s, part.m, part.margin, _ptr(part.row_lse),
+                                part.lr, part.mu, _ptr(part.dX), _ptr(part.ws), part.ws_bytes,
+                                stream)
+
+    def _side_after_main(self):
+        ev = torch.cuda.Event()
+        ev.record(torch.cuda.current_stream(self.device))
+        self.side.wait_event(ev)
+
+    def begin(self, labels, seed):
+        """Samples step 0 and stages all of its rows (side stream)."""
+        self.t = 0
+        self._side_after_main()
+        with torch.cuda.stream(self.side):
+            self.parts[0].sample(labels, seed)
+            self._stage(self.parts[0], None, self.slots[0], 1)
+            self.ready[0].record(self.side)
+        self.staged = [True, False]
+        labels.record_stream(self.side)
+
+    def step(self, X, labels_next=None, seed_next=None):
+        """Step t on the current stream; step t+1's staging on the side stream."""
+        t, a = self.t, self.t % 2
+        b = 1 - a
+        cur, nxt = self.parts[a], self.parts[b]
+        if not self.staged[a]:
+            raise RuntimeError("TieredShard.step: no staged rows (call begin(), and pass the "
+                               "next step's labels to every step but the last)")
+        self.staged[a] = False
+        if labels_next is not None:
+            self._side_after_main()
+            with torch.cuda.stream(self.side):
+                nxt.sample(labels_next, seed_next)
+                self._stage(nxt, cur, self.slots[b], t + 2)
+            labels_next.record_stream(self.side)
+        main = torch.cuda.current_stream(self.device)
+        main.wait_event(self.ready[a])
+        self._run_step(cur, X, self.slots[a])
+        self._side_after_main()
+        if labels_next is not None:
+            self._patch(cur, self.slots[a], nxt, self.slots[b])
+            self.ready[b].record(self.side)
+            self.staged[b] = True
+        self._writeback(cur, self.slots[a], t + 1)
+        self.t += 1
+        return cur
+
+    def finish(self):
+        """The current stream waits for the last write-back."""
+        torch.cuda.current_stream(self.device).wait_stream(self.side)
+
+    def stale_rows(self):
+        """Rows staged from the bank before their last update was written back
+        (or with an id outside the shard); synchronises."""
+        self.finish()
+        return int(self.stale.item())

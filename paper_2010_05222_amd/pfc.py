@@ -30,7 +30,8 @@ KERNEL_NAMES = {PFC_K_SAMPLE: "sample", PFC_K_PREP: "prep", PFC_K_FWD_GEMM: "fwd
                 PFC_K_DW_UPDATE: "dw_update"}
 
 EXPORTS = ("pfc_workspace_bytes", "pfc_sample", "pfc_forward_loss",
-           "pfc_backward_update", "pfc_status_string", "pfc_timing_begin", "pfc_timing_end")
+           "pfc_backward_update", "pfc_status_string", "pfc_timing_begin", "pfc_timing_end",
+           "pfc_bank_stage", "pfc_bank_patch", "pfc_bank_writeback")
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it first "
@@ -59,6 +60,14 @@ _lib.pfc_timing_begin.argtypes = [_int, _int]
 _lib.pfc_timing_begin.restype = _int
 _lib.pfc_timing_end.argtypes = [ctypes.POINTER(_dbl), ctypes.POINTER(_int)]
 _lib.pfc_timing_end.restype = _int
+_lib.pfc_bank_stage.argtypes = [_vp, _i64, _i64, _vp, _vp, _vp, _vp, _i64, _vp, _vp, _vp,
+                                ctypes.c_int32, _vp, _vp]
+_lib.pfc_bank_stage.restype = _int
+_lib.pfc_bank_patch.argtypes = [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _vp, _vp]
+_lib.pfc_bank_patch.restype = _int
+_lib.pfc_bank_writeback.argtypes = [_vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, ctypes.c_int32,
+                                    _vp]
+_lib.pfc_bank_writeback.restype = _int
 
 
 class PfcError(RuntimeError):
@@ -116,3 +125,22 @@ def pfc_timing_end():
     ms, n = _dbl(0.0), _int(0)
     _check(_lib.pfc_timing_end(ctypes.byref(ms), ctypes.byref(n)), "pfc_timing_end")
     return ms.value, n.value
+
+
+def pfc_bank_stage(bank, C, row_bytes, next_active, next_n, prev_active, prev_n, active_cap,
+                   slot, bank_version, row_version, version, stale, stream):
+    _check(_lib.pfc_bank_stage(bank, C, row_bytes, next_active, next_n, prev_active, prev_n,
+                               active_cap, slot, bank_version, row_version, version, stale,
+                               stream), "pfc_bank_stage")
+
+
+def pfc_bank_patch(prev_slot, prev_active, prev_n, next_active, next_n, active_cap, row_bytes,
+                   next_slot, stream):
+    _check(_lib.pfc_bank_patch(prev_slot, prev_active, prev_n, next_active, next_n, active_cap,
+                               row_bytes, next_slot, stream), "pfc_bank_patch")
+
+
+def pfc_bank_writeback(slot, active, n_active, active_cap, row_bytes, C, bank, bank_version,
+                       version, stream):
+    _check(_lib.pfc_bank_writeback(slot, active, n_active, active_cap, row_bytes, C, bank,
+                                   bank_version, version, stream), "pfc_bank_writeback")

@@ -156,6 +156,59 @@ def test_backward_rejects_before_launch(kw, status):
     assert e.value.status == status
 
 
+def _stage_args(**kw):
+    a = dict(bank=FAKE, C=1000, row_bytes=256, next_active=FAKE, next_n=FAKE, prev_active=0,
+             prev_n=0, active_cap=100, slot=FAKE, bank_version=0, row_version=0, version=1,
+             stale=0, stream=0)
+    a.update(kw)
+    return a
+
+
+@pytest.mark.parametrize("kw", [
+    dict(bank=0), dict(slot=0), dict(next_active=0), dict(next_n=0),
+    dict(C=0), dict(row_bytes=8), dict(row_bytes=24), dict(row_bytes=1 << 17),
+    dict(active_cap=0),
+    dict(prev_active=FAKE),                   # a previous list without its count
+    dict(bank_version=FAKE),                  # versions come in pairs
+])
+def test_bank_stage_rejects_before_launch(kw):
+    with pytest.raises(pfc.PfcError) as e:
+        pfc.pfc_bank_stage(**_stage_args(**kw))
+    assert e.value.status == pfc.PFC_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("kw", [
+    dict(prev_slot=0), dict(next_slot=0), dict(prev_active=0), dict(next_n=0),
+    dict(next_slot=FAKE), dict(row_bytes=0),
+])
+def test_bank_patch_rejects_before_launch(kw):
+    a = dict(prev_slot=FAKE + 16, prev_active=FAKE, prev_n=FAKE, next_active=FAKE, next_n=FAKE,
+             active_cap=100, row_bytes=256, next_slot=FAKE + 32, stream=0)
+    if kw.get("next_slot") == FAKE:
+        kw = dict(prev_slot=FAKE, next_slot=FAKE)           # a slot patched onto itself
+    a.update(kw)
+    with pytest.raises(pfc.PfcError) as e:
+        pfc.pfc_bank_patch(**a)
+    assert e.value.status == pfc.PFC_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("kw", [dict(slot=0), dict(bank=0), dict(C=-1), dict(row_bytes=100)])
+def test_bank_writeback_rejects_before_launch(kw):
+    a = dict(slot=FAKE, active=FAKE, n_active=FAKE, active_cap=100, row_bytes=256, C=1000,
+             bank=FAKE, bank_version=0, version=1, stream=0)
+    a.update(kw)
+    with pytest.raises(pfc.PfcError) as e:
+        pfc.pfc_bank_writeback(**a)
+    assert e.value.status == pfc.PFC_ERR_INVALID_ARG
+
+
+@pytest.mark.skipif(torch.cuda.device_count() > 0, reason="only meaningful without a GPU")
+def test_bank_without_device_reports_hip_error():
+    with pytest.raises(pfc.PfcError) as e:
+        pfc.pfc_bank_stage(**_stage_args())
+    assert e.value.status == pfc.PFC_ERR_HIP
+
+
 @pytest.mark.skipif(torch.cuda.device_count() > 0, reason="only meaningful without a GPU")
 def test_no_device_reports_hip_error():
     """With no HIP device the launch fails and the ABI reports PFC_ERR_HIP."""
