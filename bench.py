@@ -143,6 +143,95 @@ def cpu_baseline(cfg, W_dev, rows):
     return entry
 
 
+def run_tiered(args, cfg):
+    """The same workload with the class bank in pinned host memory: every step
+    stages its cold rows over the host link and writes its rows back
+    (TieredShard); prints one JSON line of its own."""
+    import numpy as np
+    import torch
+    import workloads
+    from paper_2010_05222_amd.head import TieredShard
+
+    dev = torch.device("cuda:0")
+    tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[cfg["dtype"]]
+    B, d, C = cfg["B"], cfg["d"], cfg["C"]
+    ts = TieredShard(B, d, C, cfg["r"], dtype=cfg["dtype"], class_offset=cfg["a"], s=cfg["s"],
+                     m=cfg["m"], margin=cfg["margin"], lr=cfg["lr"], mu=cfg["mu"], device=dev,
+                     master=cfg["master"])
+    W, master = workloads.make_weights_device(cfg, dev)
+    ts.W_bank.copy_(W)
+    if master is not None:
+        ts.P_bank.copy_(master)
+    del W, master
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    wbytes = ts.W_bank.element_size() * d + 4 * d * (2 if cfg["master"] else 1)
+    log(f"[bench] tiered: bank of {C} rows in pinned host memory "
+        f"({C * wbytes / 2**30:.2f} GiB), {ts.n} slots of {ts.cap} rows")
+    n = args.warmup + args.steps
+    batches = []
+    for t in range(n + 1):
+        seed = t - args.warmup if t >= args.warmup else 10**6 + t
+        X, L = workloads.make_batch(cfg, seed)
+        batches.append((torch.from_numpy(X).to(tdt).to(dev), torch.from_numpy(L).to(dev), seed))
+    torch.cuda.synchronize()
+    ts.begin(batches[0][1], batches[0][2])
+    sets = []
+    t0 = None
+    for t in range(n):
+        if t == args.warmup:
+            ts.finish()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+        nxt = batches[t + 1] if t + 1 < n else None
+        out = ts.step(batches[t][0], nxt[1] if nxt else None, nxt[2] if nxt else None)
+        if t >= args.warmup:
+            sets.append((out.active.clone(), out.n_active.clone()))
+    ts.finish()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    stale = ts.stale_rows()
+    loss = float(out.loss.item())
+    ms = elapsed * 1e3 / args.steps
+    # Rows over the host link per step: up, the rows of S(t) in none of the
+    # sets still held in slots; down, the rows of S(t) not in S(t+1) (those
+    # are written back by the next step; the last step writes all).
+    acts = [a[:int(k.item())].cpu().numpy() for a, k in sets]
+    Ks = [len(a) for a in acts]
+    cold, gone = [], []
+    for t, a in enumerate(acts):
+        held = acts[max(0, t - ts.n + 1):t]
+        cold.append(len(np.setdiff1d(a, np.concatenate(held))) if held else len(a))
+        gone.append(len(np.setdiff1d(a, acts[t + 1])) if t + 1 < len(acts) else len(a))
+    up = float(np.mean(cold[ts.n - 1:] if len(cold) >= ts.n else cold)) * wbytes
+    down = float(np.mean(gone[:-1] if len(gone) > 1 else gone)) * wbytes
+    peak = 64.0       # PCIe 5.0 x16, one direction
+    log(f"[bench] tiered {args.steps} steps: {ms:.2f} ms/step, up {up / 1e9:.2f} GB/step "
+        f"({up / ms / 1e6:.1f} GB/s), down {down / 1e9:.2f} GB/step ({down / ms / 1e6:.1f} GB/s), "
+        f"stale rows {stale}, last loss {loss:.4f}")
+    if stale or not np.isfinite(loss):
+        raise RuntimeError("tiered run: stale rows or non-finite loss")
+    print(json.dumps({
+        "metric": METRIC + " (tiered: class bank in pinned host memory)",
+        "value": B * args.steps / elapsed, "unit": "samples/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": cfg["dtype"], "data": "synthetic",
+        "config": {"workload": f"{cfg['name']} with the class bank in host memory: B={B} d={d} "
+                               f"C_shard={C} r={cfg['r']}", "global_batch": B, "d": d,
+                   "C_shard": C, "r": cfg["r"], "bank": "pinned host memory",
+                   "parallelism": "one class shard on one GPU"},
+        "roofline": {"bound": "host-link", "achieved": max(up, down) / ms / 1e6, "peak": peak,
+                     "unit": "GB/s", "frac": max(up, down) / ms / 1e6 / peak, "traffic": None,
+                     "kernel": "bank stage + write-back"},
+        "host_link": {"up_GB_per_step": up / 1e9, "down_GB_per_step": down / 1e9,
+                      "up_GBps": up / ms / 1e6, "down_GBps": down / ms / 1e6,
+                      "cold_rows_mean": up / wbytes, "written_rows_mean": down / wbytes,
+                      "active_mean": float(np.mean(Ks)), "slots": ts.n},
+        "last_loss": loss,
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -155,6 +244,8 @@ def main():
     ap.add_argument("--cpu-rows", type=int, default=32)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration)")
+    ap.add_argument("--tiered", action="store_true",
+                    help="keep the class bank in pinned host memory (staged per step)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -174,6 +265,9 @@ def main():
     tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[cfg["dtype"]]
     B, d, C = cfg["B"], cfg["d"], cfg["C"]
     log(f"[bench] workload {cfg['name']}: B={B} d={d} C={C} r={cfg['r']} {cfg['dtype']}")
+    if args.tiered:
+        run_tiered(args, cfg)
+        return
 
     W, master = workloads.make_weights_device(cfg, dev)
     M = torch.zeros((C, d), dtype=torch.float32, device=dev)

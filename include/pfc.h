@@ -202,18 +202,25 @@ int pfc_timing_end(double* total_ms /*host*/, int* launches /*host*/);
  * bank row active[j].  The step itself is the three calls above with the slot
  * as W / momentum / W_master and an identity active list 0, 1, ..., cap - 1
  * (the sampler's list stays in active space for these copies; labels_mapped is
- * already a position in S).  With two slots and a side stream, the rows of
- * step t+1 are staged while step t runs:
- *   stage      cold rows, S(t+1) minus S(t), bank -> slot B (any time after the
- *              write-back of the step that last used slot B);
- *   patch      rows in both S(t) and S(t+1), slot A -> slot B, after step t's
- *              update; slot B is ready for step t+1 after stage and patch;
- *   writeback  slot A -> bank, after step t; slot A is free for step t+2
+ * already a position in S).  With a ring of slots and side streams, the rows
+ * of step t+1 are staged while step t runs:
+ *   stage      cold rows - S(t+1) minus the previous sets still held in slots
+ *              (prev: S(t), prev2: S(t-1) or NULL) - bank -> the next slot,
+ *              any time after the write-back of the step that last used it
+ *              and of every step whose rows it may read from the bank;
+ *   patch      rows S(t+1) shares with an earlier set, that set's slot -> the
+ *              next slot, after that step's update, older sets first (the
+ *              newest copy wins); the next slot is ready after stage and patch;
+ *   writeback  a slot -> bank, after its step, skipping the rows of the next
+ *              step's set when it is given (next_active / next_n, or NULL):
+ *              that step writes them back with newer values, and the next
+ *              stages take them from its slot; the slot is free for reuse
  *              after the write-back.
  * Each copy is a byte copy of `row_bytes` per row (a multiple of 16, at most
  * 65536): d * 2 for 16-bit W, d * 4 for momentum and the master; one call per
  * array.  active / next_active / prev_active are sorted ascending id lists of
- * active_cap entries (pfc_sample's output) with their device counts n;
+ * active_cap entries (pfc_sample's output) with their device counts n (a list
+ * and its count are given together or both NULL);
  * entries past the count are ignored, and counts are clamped to [0, cap].
  * Slots are [active_cap x row] device buffers.  Bank pointers (and
  * bank_version) must be host memory allocated pinned and mapped (hipHostMalloc,
@@ -234,7 +241,9 @@ int pfc_timing_end(double* total_ms /*host*/, int* launches /*host*/);
 int pfc_bank_stage(const void* bank, int64_t C, int64_t row_bytes,
                    const int32_t* next_active, const int32_t* next_n,
                    const int32_t* prev_active /*or NULL*/,
-                   const int32_t* prev_n /*or NULL*/, int64_t active_cap,
+                   const int32_t* prev_n /*or NULL*/,
+                   const int32_t* prev2_active /*or NULL*/,
+                   const int32_t* prev2_n /*or NULL*/, int64_t active_cap,
                    void* slot, const int32_t* bank_version /*host, or NULL*/,
                    int32_t* row_version /*or NULL*/, int32_t version,
                    int32_t* stale /*or NULL*/, void* stream);
@@ -243,7 +252,9 @@ int pfc_bank_patch(const void* prev_slot, const int32_t* prev_active,
                    const int32_t* next_n, int64_t active_cap, int64_t row_bytes,
                    void* next_slot, void* stream);
 int pfc_bank_writeback(const void* slot, const int32_t* active,
-                       const int32_t* n_active, int64_t active_cap,
+                       const int32_t* n_active,
+                       const int32_t* next_active /*or NULL*/,
+                       const int32_t* next_n /*or NULL*/, int64_t active_cap,
                        int64_t row_bytes, int64_t C, void* bank,
                        int32_t* bank_version /*host, or NULL*/, int32_t version,
                        void* stream);

@@ -3,23 +3,32 @@
 // for the step (Sec. 3.3.3, the paragraph on asynchronous hierarchical class
 // storage, and Fig. async_pipeline).
 //
-// Three copies, each one wave per slot row, 16 bytes per lane:
-//  - stage:     cold rows S(t+1) \ S(t) from the bank into the next slot,
-//               with a check of the per-row versions (the host copy of a row
-//               must carry the version of its last update);
-//  - patch:     overlapping rows S(t) and S(t+1) from the current slot into
-//               the next one, once step t has updated them;
-//  - writeback: the slot's rows back into the bank, stamping their version.
+// Three copies, each a row per wave at a time, 16 bytes per lane:
+//  - stage:     cold rows of S(t+1) - those in neither of the (up to two)
+//               previous active sets still held in slots - from the bank
+//               into the next slot, with a check of the per-row versions
+//               (the host copy of a row must carry the version of its last
+//               update);
+//  - patch:     rows S(t+1) shares with an earlier set, from that set's slot
+//               into the next one, once its step has updated them;
+//  - writeback: the slot's rows back into the bank, stamping their version,
+//               except rows the next step also holds (its write-back carries
+//               their newer values).
 // The host side of each copy goes over the host link with ordinary vector
 // loads and stores on the mapped pinned pages; the device side is HBM.
-// Membership in S(t) is a binary search over its sorted id list.
+// Membership in S(t) is a binary search over its sorted id list.  The copies
+// run on a fixed grid of 2048 waves that walks the rows, eight rows per wave
+// at a time with all eight loads issued before the stores: they wait on the
+// host link most of the time, and a grid of one wave per row would hold the
+// CUs and starve the step's kernels running beside them on other streams.
 #include "pfc_device.h"
 #include "pfc.h"
 
 namespace pfc {
 namespace {
 
-constexpr int kBankWaves = 4;   // slot rows per workgroup (one per wave)
+constexpr int kBankWaves = 4;     // waves per workgroup
+constexpr int kBankGrid = 512;    // workgroups of a copy
 constexpr int64_t kMaxRowBytes = 1 << 16;
 
 // Index of v in the ascending a[0, n), or -1.
@@ -39,32 +48,77 @@ __device__ __forceinline__ int64_t rows_of(const int32_t* n_p, int64_t cap) {
   return n < 0 ? 0 : (n > cap ? cap : n);
 }
 
-__device__ __forceinline__ void copy_row(const uint4* __restrict__ src, uint4* __restrict__ dst,
-                                         int row16, int lane) {
-  for (int i = lane; i < row16; i += 64) dst[i] = src[i];
+__device__ __forceinline__ int64_t wave_index() {
+  return (int64_t)blockIdx.x * kBankWaves + (threadIdx.x >> 6);
+}
+__device__ __forceinline__ int64_t wave_count() { return (int64_t)gridDim.x * kBankWaves; }
+
+// A wave copies kGroup rows at a time: all their loads are issued before the
+// first store, so a wave keeps kGroup x 1 KB in flight on the host link.
+constexpr int kGroup = 8;
+
+struct RowGroup {
+  const uint4* src[kGroup];
+  uint4* dst[kGroup];
+  bool ok[kGroup];
+};
+
+__device__ __forceinline__ void copy_group(const RowGroup& g, int row16, int lane) {
+  for (int i = lane; i < row16; i += 64) {
+    uint4 v[kGroup];
+#pragma unroll
+    for (int k = 0; k < kGroup; ++k)
+      if (g.ok[k]) v[k] = g.src[k][i];
+#pragma unroll
+    for (int k = 0; k < kGroup; ++k)
+      if (g.ok[k]) g.dst[k][i] = v[k];
+  }
 }
 
 __global__ void __launch_bounds__(64 * kBankWaves) k_bank_stage(
     const uint4* __restrict__ bank, int64_t C, int row16, const int32_t* __restrict__ next_active,
     const int32_t* __restrict__ next_n, const int32_t* __restrict__ prev_active,
-    const int32_t* __restrict__ prev_n, int64_t cap, uint4* __restrict__ slot,
+    const int32_t* __restrict__ prev_n, const int32_t* __restrict__ prev2_active,
+    const int32_t* __restrict__ prev2_n, int64_t cap, uint4* __restrict__ slot,
     const int32_t* __restrict__ bank_version, int32_t* __restrict__ row_version,
     int32_t version, int32_t* __restrict__ stale) {
   const int lane = threadIdx.x & 63;
-  const int64_t j = (int64_t)blockIdx.x * kBankWaves + (threadIdx.x >> 6);
-  if (j >= rows_of(next_n, cap)) return;
-  const int32_t c = next_active[j];
-  if (c < 0 || c >= C) {   // not a row of the bank: nothing is copied
-    if (lane == 0 && stale) atomicAdd(stale, 1);
-    return;
+  const int64_t n = rows_of(next_n, cap);
+  const int64_t np = prev_active ? rows_of(prev_n, cap) : 0;
+  const int64_t np2 = prev2_active ? rows_of(prev2_n, cap) : 0;
+  for (int64_t j0 = wave_index() * kGroup; j0 < n; j0 += wave_count() * kGroup) {
+    RowGroup g;
+    int32_t cls[kGroup];
+#pragma unroll
+    for (int k = 0; k < kGroup; ++k) {
+      const int64_t j = j0 + k;
+      cls[k] = -1;
+      g.ok[k] = false;
+      g.src[k] = bank;
+      g.dst[k] = slot;
+      if (j >= n) continue;
+      const int32_t c = next_active[j];
+      if (c < 0 || c >= C) {   // not a row of the bank: nothing is copied
+        if (lane == 0 && stale) atomicAdd(stale, 1);
+        continue;
+      }
+      cls[k] = c;
+      const bool overlap = (np > 0 && find_sorted(prev_active, np, c) >= 0) ||
+                           (np2 > 0 && find_sorted(prev2_active, np2, c) >= 0);
+      if (overlap) continue;
+      if (row_version && lane == 0 && bank_version[c] != row_version[c] && stale)
+        atomicAdd(stale, 1);
+      g.ok[k] = true;
+      g.src[k] = bank + (int64_t)c * row16;
+      g.dst[k] = slot + j * row16;
+    }
+    copy_group(g, row16, lane);
+    if (row_version && lane == 0) {
+#pragma unroll
+      for (int k = 0; k < kGroup; ++k)
+        if (cls[k] >= 0) row_version[cls[k]] = version;
+    }
   }
-  const bool overlap = prev_active && find_sorted(prev_active, rows_of(prev_n, cap), c) >= 0;
-  if (!overlap) {
-    if (row_version && lane == 0 && bank_version[c] != row_version[c] && stale)
-      atomicAdd(stale, 1);
-    copy_row(bank + (int64_t)c * row16, slot + j * row16, row16, lane);
-  }
-  if (row_version && lane == 0) row_version[c] = version;
 }
 
 __global__ void __launch_bounds__(64 * kBankWaves) k_bank_patch(
@@ -72,27 +126,52 @@ __global__ void __launch_bounds__(64 * kBankWaves) k_bank_patch(
     const int32_t* __restrict__ prev_n, const int32_t* __restrict__ next_active,
     const int32_t* __restrict__ next_n, int64_t cap, int row16, uint4* __restrict__ next_slot) {
   const int lane = threadIdx.x & 63;
-  const int64_t j = (int64_t)blockIdx.x * kBankWaves + (threadIdx.x >> 6);
-  if (j >= rows_of(next_n, cap)) return;
-  const int64_t i = find_sorted(prev_active, rows_of(prev_n, cap), next_active[j]);
-  if (i < 0) return;
-  copy_row(prev_slot + i * row16, next_slot + j * row16, row16, lane);
+  const int64_t n = rows_of(next_n, cap), np = rows_of(prev_n, cap);
+  for (int64_t j0 = wave_index() * kGroup; j0 < n; j0 += wave_count() * kGroup) {
+    RowGroup g;
+#pragma unroll
+    for (int k = 0; k < kGroup; ++k) {
+      const int64_t j = j0 + k;
+      const int64_t i = j < n ? find_sorted(prev_active, np, next_active[j]) : -1;
+      g.ok[k] = i >= 0;
+      g.src[k] = i >= 0 ? prev_slot + i * row16 : prev_slot;
+      g.dst[k] = i >= 0 ? next_slot + j * row16 : next_slot;
+    }
+    copy_group(g, row16, lane);
+  }
 }
 
 __global__ void __launch_bounds__(64 * kBankWaves) k_bank_writeback(
     const uint4* __restrict__ slot, const int32_t* __restrict__ active,
-    const int32_t* __restrict__ n_active, int64_t cap, int row16, int64_t C,
+    const int32_t* __restrict__ n_active, const int32_t* __restrict__ next_active,
+    const int32_t* __restrict__ next_n, int64_t cap, int row16, int64_t C,
     uint4* __restrict__ bank, int32_t* __restrict__ bank_version, int32_t version) {
   const int lane = threadIdx.x & 63;
-  const int64_t j = (int64_t)blockIdx.x * kBankWaves + (threadIdx.x >> 6);
-  if (j >= rows_of(n_active, cap)) return;
-  const int32_t c = active[j];
-  if (c < 0 || c >= C) return;
-  copy_row(slot + j * row16, bank + (int64_t)c * row16, row16, lane);
-  if (bank_version) {
-    // The row's data reach system scope before its version does.
-    __threadfence_system();
-    if (lane == 0) bank_version[c] = version;
+  const int64_t n = rows_of(n_active, cap);
+  const int64_t nn = next_active ? rows_of(next_n, cap) : 0;
+  for (int64_t j0 = wave_index() * kGroup; j0 < n; j0 += wave_count() * kGroup) {
+    RowGroup g;
+    int32_t cls[kGroup];
+#pragma unroll
+    for (int k = 0; k < kGroup; ++k) {
+      const int64_t j = j0 + k;
+      const int32_t c = j < n ? active[j] : -1;
+      const bool ok = c >= 0 && c < C && !(nn > 0 && find_sorted(next_active, nn, c) >= 0);
+      cls[k] = ok ? c : -1;
+      g.ok[k] = ok;
+      g.src[k] = ok ? slot + j * row16 : slot;
+      g.dst[k] = ok ? bank + (int64_t)c * row16 : bank;
+    }
+    copy_group(g, row16, lane);
+    if (bank_version) {
+      // The rows' data reach system scope before their versions do.
+      __threadfence_system();
+      if (lane == 0) {
+#pragma unroll
+        for (int k = 0; k < kGroup; ++k)
+          if (cls[k] >= 0) bank_version[cls[k]] = version;
+      }
+    }
   }
 }
 
@@ -124,7 +203,10 @@ int device_present() {
   return PFC_OK;
 }
 
-unsigned grid_of(int64_t cap) { return (unsigned)ceil_div(cap, kBankWaves); }
+unsigned grid_of(int64_t cap) {
+  const int64_t g = ceil_div(cap, kBankWaves);
+  return (unsigned)(g < kBankGrid ? g : kBankGrid);
+}
 
 }  // namespace
 }  // namespace pfc
@@ -135,11 +217,13 @@ extern "C" {
 
 int pfc_bank_stage(const void* bank, int64_t C, int64_t row_bytes, const int32_t* next_active,
                    const int32_t* next_n, const int32_t* prev_active, const int32_t* prev_n,
-                   int64_t active_cap, void* slot, const int32_t* bank_version,
-                   int32_t* row_version, int32_t version, int32_t* stale, void* stream) {
+                   const int32_t* prev2_active, const int32_t* prev2_n, int64_t active_cap,
+                   void* slot, const int32_t* bank_version, int32_t* row_version,
+                   int32_t version, int32_t* stale, void* stream) {
   if (!bank || !next_active || !next_n || !slot) return PFC_ERR_INVALID_ARG;
   if (C < 1 || C > PFC_MAX_CLASSES) return PFC_ERR_INVALID_ARG;
   if ((prev_active == nullptr) != (prev_n == nullptr)) return PFC_ERR_INVALID_ARG;
+  if ((prev2_active == nullptr) != (prev2_n == nullptr)) return PFC_ERR_INVALID_ARG;
   if ((bank_version == nullptr) != (row_version == nullptr)) return PFC_ERR_INVALID_ARG;
   const int st = common_checks(row_bytes, active_cap);
   if (st != PFC_OK) return st;
@@ -150,7 +234,8 @@ int pfc_bank_stage(const void* bank, int64_t C, int64_t row_bytes, const int32_t
   (void)hipGetLastError();
   hipLaunchKernelGGL(k_bank_stage, dim3(grid_of(active_cap)), dim3(64 * kBankWaves), 0,
                      (hipStream_t)stream, (const uint4*)bank, C, (int)(row_bytes / 16),
-                     next_active, next_n, prev_active, prev_n, active_cap, (uint4*)slot,
+                     next_active, next_n, prev_active, prev_n, prev2_active, prev2_n,
+                     active_cap, (uint4*)slot,
                      bank_version, row_version, version, stale);
   return hipGetLastError() == hipSuccess ? PFC_OK : PFC_ERR_HIP;
 }
@@ -167,16 +252,20 @@ int pfc_bank_patch(const void* prev_slot, const int32_t* prev_active, const int3
   if (dv != PFC_OK) return dv;
   if (!device_accessible(prev_slot) || !device_accessible(next_slot)) return PFC_ERR_INVALID_ARG;
   (void)hipGetLastError();
-  hipLaunchKernelGGL(k_bank_patch, dim3(grid_of(active_cap)), dim3(64 * kBankWaves), 0,
+  // A device-to-device copy: enough waves for every group of rows at once.
+  hipLaunchKernelGGL(k_bank_patch, dim3((unsigned)ceil_div(active_cap, kGroup * kBankWaves)),
+                     dim3(64 * kBankWaves), 0,
                      (hipStream_t)stream, (const uint4*)prev_slot, prev_active, prev_n,
                      next_active, next_n, active_cap, (int)(row_bytes / 16), (uint4*)next_slot);
   return hipGetLastError() == hipSuccess ? PFC_OK : PFC_ERR_HIP;
 }
 
 int pfc_bank_writeback(const void* slot, const int32_t* active, const int32_t* n_active,
-                       int64_t active_cap, int64_t row_bytes, int64_t C, void* bank,
-                       int32_t* bank_version, int32_t version, void* stream) {
+                       const int32_t* next_active, const int32_t* next_n, int64_t active_cap,
+                       int64_t row_bytes, int64_t C, void* bank, int32_t* bank_version,
+                       int32_t version, void* stream) {
   if (!slot || !active || !n_active || !bank) return PFC_ERR_INVALID_ARG;
+  if ((next_active == nullptr) != (next_n == nullptr)) return PFC_ERR_INVALID_ARG;
   if (C < 1 || C > PFC_MAX_CLASSES) return PFC_ERR_INVALID_ARG;
   const int st = common_checks(row_bytes, active_cap);
   if (st != PFC_OK) return st;
@@ -186,7 +275,8 @@ int pfc_bank_writeback(const void* slot, const int32_t* active, const int32_t* n
   if (bank_version && !device_accessible(bank_version)) return PFC_ERR_INVALID_ARG;
   (void)hipGetLastError();
   hipLaunchKernelGGL(k_bank_writeback, dim3(grid_of(active_cap)), dim3(64 * kBankWaves), 0,
-                     (hipStream_t)stream, (const uint4*)slot, active, n_active, active_cap,
+                     (hipStream_t)stream, (const uint4*)slot, active, n_active, next_active,
+                     next_n, active_cap,
                      (int)(row_bytes / 16), C, (uint4*)bank, bank_version, version);
   return hipGetLastError() == hipSuccess ? PFC_OK : PFC_ERR_HIP;
 }

@@ -104,11 +104,22 @@ class TieredShard:
     The bank - W in the storage dtype, fp32 momentum, and an fp32 master when
     `master` - holds all C rows (`W_bank`, `M_bank`, `P_bank`: pinned host
     tensors the caller fills).  Each step runs on a device slot of `cap` rows
-    holding only its active rows; two slots alternate.  While step t runs on
-    slot A, a side stream samples step t+1 and stages its cold rows into slot
-    B; after step t's update the rows S(t) and S(t+1) share are patched from A
-    into B (which then becomes ready), and A is written back to the bank.
-    HIP events order the two streams; every copy is a libpfc kernel.
+    holding only its active rows; `n_slots` slots (2 or 3) are used in turn.
+    While step t runs on its slot (current stream), an upload stream samples
+    step t+1 and stages its cold rows into the next slot; rows that S(t+1)
+    shares with S(t) (and, with three slots, with S(t-1)) are patched from
+    those slots once their steps have updated them, and a download stream
+    writes each slot back to the bank after its step.  HIP events order the
+    three streams:
+      upload(t+1)   after download(t+1-n_slots)  (the slot and its id lists are
+                    free, and every bank row it may read is current)
+      patch(t-1 -> t+1), then patch(t -> t+1) after step t  (the newest copy wins)
+      download(t)   after step t and the sampling of step t+1, whose rows it
+                    leaves to download(t+1)
+      step t+1      after its patches
+    With three slots the upload of step t+1 need not wait for the download of
+    step t-1, so the two directions of the host link run at once.  Every copy
+    is a libpfc kernel.
 
         ts = TieredShard(B, d, C, r, ...)
         ts.W_bank.copy_(W0); ts.M_bank.zero_()
@@ -116,16 +127,20 @@ class TieredShard:
         for t in range(T):
             out = ts.step(X[t], labels[t + 1] if t + 1 < T else None, seeds[t + 1] ...)
             # out.loss, out.row_lse, out.dX belong to step t (valid on the
-            # current stream until step t + 2)
+            # current stream until step t + n_slots)
         ts.finish()          # the bank holds every update
         ts.stale_rows()      # 0 unless a cold row was staged before its write-back
     """
 
     def __init__(self, B, d, C, r, dtype="bf16", class_offset=0, s=64.0, m=0.5,
-                 margin="arcface", lr=0.1, mu=0.9, device="cuda:0", tau=None, master=False):
+                 margin="arcface", lr=0.1, mu=0.9, device="cuda:0", tau=None, master=False,
+                 n_slots=3):
+        if n_slots not in (2, 3):
+            raise ValueError("n_slots must be 2 or 3")
         kw = dict(dtype=dtype, class_offset=class_offset, s=s, m=m, margin=margin, lr=lr, mu=mu,
                   device=device, tau=tau)
-        self.parts = [PfcShard(B, d, C, r, **kw), PfcShard(B, d, C, r, **kw)]
+        self.n = int(n_slots)
+        self.parts = [PfcShard(B, d, C, r, **kw) for _ in range(self.n)]
         p = self.parts[0]
         self.B, self.d, self.C, self.cap, self.device = p.B, p.d, p.C, p.cap, p.device
         dev, cap = self.device, self.cap
@@ -136,7 +151,7 @@ class TieredShard:
         self.row_version = torch.zeros(C, dtype=torch.int32, device=dev)
         self.stale = torch.zeros(1, dtype=torch.int32, device=dev)
         self.slots = []
-        for _ in range(2):
+        for _ in range(self.n):
             sl = {"W": torch.empty((cap, d), dtype=p.tdtype, device=dev),
                   "M": torch.empty((cap, d), dtype=torch.float32, device=dev)}
             if master:
@@ -146,24 +161,26 @@ class TieredShard:
         if master:
             self.banks["P"] = self.P_bank
         self.iota = torch.arange(cap, dtype=torch.int32, device=dev)
-        self.side = torch.cuda.Stream(device=dev)
-        self.ready = [torch.cuda.Event(), torch.cuda.Event()]
-        self.staged = [False, False]
+        self.up = torch.cuda.Stream(device=dev)
+        self.down = torch.cuda.Stream(device=dev)
+        self.ready = [torch.cuda.Event() for _ in range(self.n)]
+        self.written = [None] * self.n      # event: last download of each slot
+        self.staged = [False] * self.n
         self.t = 0
 
     def _row_bytes(self, key):
         return self.d * self.banks[key].element_size()
 
-    def _stage(self, nxt, prv, slot, version):
-        stream = self.side.cuda_stream
+    def _stage(self, nxt, prevs, slot, version):
+        stream = self.up.cuda_stream
+        pv = [(_ptr(q.active), _ptr(q.n_active)) for q in prevs] + [(0, 0)] * (2 - len(prevs))
         for key in ("M", "P", "W"):
             if key not in slot:
                 continue
             ver = key == "W"
             abi.pfc_bank_stage(_ptr(self.banks[key]), self.C, self._row_bytes(key),
-                               _ptr(nxt.active), _ptr(nxt.n_active),
-                               _ptr(prv.active) if prv else 0, _ptr(prv.n_active) if prv else 0,
-                               self.cap, _ptr(slot[key]),
+                               _ptr(nxt.active), _ptr(nxt.n_active), pv[0][0], pv[0][1],
+                               pv[1][0], pv[1][1], self.cap, _ptr(slot[key]),
                                _ptr(self.bank_version) if ver else 0,
                                _ptr(self.row_version) if ver else 0, version,
                                _ptr(self.stale) if ver else 0, stream)
@@ -172,18 +189,21 @@ class TieredShard:
         for key in src:
             abi.pfc_bank_patch(_ptr(src[key]), _ptr(prv.active), _ptr(prv.n_active),
                                _ptr(nxt.active), _ptr(nxt.n_active), self.cap,
-                               self._row_bytes(key), _ptr(dst[key]), self.side.cuda_stream)
+                               self._row_bytes(key), _ptr(dst[key]), self.up.cuda_stream)
 
-    def _writeback(self, part, slot, version):
+    def _writeback(self, part, slot, version, nxt):
         # The W rows go last and stamp the version, so a stamped row's
-        # momentum (and master) rows are already in the bank.
+        # momentum (and master) rows are already in the bank.  Rows the next
+        # step holds are left to its write-back.
+        na, nn = (_ptr(nxt.active), _ptr(nxt.n_active)) if nxt else (0, 0)
         for key in ("M", "P", "W"):
             if key not in slot:
                 continue
-            abi.pfc_bank_writeback(_ptr(slot[key]), _ptr(part.active), _ptr(part.n_active),
-                                   self.cap, self._row_bytes(key), self.C, _ptr(self.banks[key]),
+            abi.pfc_bank_writeback(_ptr(slot[key]), _ptr(part.active), _ptr(part.n_active), na,
+                                   nn, self.cap, self._row_bytes(key), self.C,
+                                   _ptr(self.banks[key]),
                                    _ptr(self.bank_version) if key == "W" else 0, version,
-                                   self.side.cuda_stream)
+                                   self.down.cuda_stream)
 
     def _run_step(self, part, X, slot):
         _require(X, part.tdtype, (self.B, self.d), "X", self.device)
@@ -201,52 +221,75 @@ class TieredShard:
                                 part.lr, part.mu, _ptr(part.dX), _ptr(part.ws), part.ws_bytes,
                                 stream)
 
-    def _side_after_main(self):
+    def _mark_main(self):
         ev = torch.cuda.Event()
         ev.record(torch.cuda.current_stream(self.device))
-        self.side.wait_event(ev)
+        return ev
+
+    def _upload(self, k, prevs, labels, seed, version):
+        """Sample a step into parts[k] and stage its cold rows into slot k."""
+        self.up.wait_event(self._mark_main())          # labels were made on the current stream
+        if self.written[k] is not None:
+            self.up.wait_event(self.written[k])
+        part = self.parts[k]
+        sampled = torch.cuda.Event()
+        with torch.cuda.stream(self.up):
+            part.sample(labels, seed)
+            sampled.record(self.up)
+            self._stage(part, prevs, self.slots[k], version)
+        labels.record_stream(self.up)
+        return sampled
 
     def begin(self, labels, seed):
-        """Samples step 0 and stages all of its rows (side stream)."""
+        """Samples step 0 and stages all of its rows."""
         self.t = 0
-        self._side_after_main()
-        with torch.cuda.stream(self.side):
-            self.parts[0].sample(labels, seed)
-            self._stage(self.parts[0], None, self.slots[0], 1)
-            self.ready[0].record(self.side)
-        self.staged = [True, False]
-        labels.record_stream(self.side)
+        self._upload(0, [], labels, seed, 1)
+        self.ready[0].record(self.up)
+        self.staged = [False] * self.n
+        self.staged[0] = True
 
     def step(self, X, labels_next=None, seed_next=None):
-        """Step t on the current stream; step t+1's staging on the side stream."""
-        t, a = self.t, self.t % 2
-        b = 1 - a
+        """Step t on the current stream; step t+1's rows are staged alongside."""
+        t, n = self.t, self.n
+        a, b, z = t % n, (t + 1) % n, (t - 1) % n
         cur, nxt = self.parts[a], self.parts[b]
         if not self.staged[a]:
             raise RuntimeError("TieredShard.step: no staged rows (call begin(), and pass the "
                                "next step's labels to every step but the last)")
         self.staged[a] = False
+        older = self.parts[z] if (n >= 3 and t >= 1) else None
+        sampled = None
         if labels_next is not None:
-            self._side_after_main()
-            with torch.cuda.stream(self.side):
-                nxt.sample(labels_next, seed_next)
-                self._stage(nxt, cur, self.slots[b], t + 2)
-            labels_next.record_stream(self.side)
+            sampled = self._upload(b, [cur] + ([older] if older else []), labels_next,
+                                   seed_next, t + 2)
+            if older:
+                # Step t-1 is done: the upload stream waited for it before the
+                # previous patch.
+                self._patch(older, self.slots[z], nxt, self.slots[b])
         main = torch.cuda.current_stream(self.device)
         main.wait_event(self.ready[a])
         self._run_step(cur, X, self.slots[a])
-        self._side_after_main()
+        done = self._mark_main()
         if labels_next is not None:
+            self.up.wait_event(done)
             self._patch(cur, self.slots[a], nxt, self.slots[b])
-            self.ready[b].record(self.side)
+            self.ready[b].record(self.up)
             self.staged[b] = True
-        self._writeback(cur, self.slots[a], t + 1)
+        self.down.wait_event(done)
+        if sampled is not None:
+            self.down.wait_event(sampled)
+        self._writeback(cur, self.slots[a], t + 1, nxt if sampled is not None else None)
+        ev = torch.cuda.Event()
+        ev.record(self.down)
+        self.written[a] = ev
         self.t += 1
         return cur
 
     def finish(self):
-        """The current stream waits for the last write-back."""
-        torch.cuda.current_stream(self.device).wait_stream(self.side)
+        """The current stream waits for every staging and write-back."""
+        main = torch.cuda.current_stream(self.device)
+        main.wait_stream(self.up)
+        main.wait_stream(self.down)
 
     def stale_rows(self):
         """Rows staged from the bank before their last update was written back

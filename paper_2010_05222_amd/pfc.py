@@ -60,13 +60,13 @@ _lib.pfc_timing_begin.argtypes = [_int, _int]
 _lib.pfc_timing_begin.restype = _int
 _lib.pfc_timing_end.argtypes = [ctypes.POINTER(_dbl), ctypes.POINTER(_int)]
 _lib.pfc_timing_end.restype = _int
-_lib.pfc_bank_stage.argtypes = [_vp, _i64, _i64, _vp, _vp, _vp, _vp, _i64, _vp, _vp, _vp,
-                                ctypes.c_int32, _vp, _vp]
+_lib.pfc_bank_stage.argtypes = [_vp, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _vp, _vp,
+                                _vp, ctypes.c_int32, _vp, _vp]
 _lib.pfc_bank_stage.restype = _int
 _lib.pfc_bank_patch.argtypes = [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _vp, _vp]
 _lib.pfc_bank_patch.restype = _int
-_lib.pfc_bank_writeback.argtypes = [_vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, ctypes.c_int32,
-                                    _vp]
+_lib.pfc_bank_writeback.argtypes = [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp,
+                                    ctypes.c_int32, _vp]
 _lib.pfc_bank_writeback.restype = _int
 
 
@@ -127,11 +127,11 @@ def pfc_timing_end():
     return ms.value, n.value
 
 
-def pfc_bank_stage(bank, C, row_bytes, next_active, next_n, prev_active, prev_n, active_cap,
-                   slot, bank_version, row_version, version, stale, stream):
+def pfc_bank_stage(bank, C, row_bytes, next_active, next_n, prev_active, prev_n, prev2_active,
+                   prev2_n, active_cap, slot, bank_version, row_version, version, stale, stream):
     _check(_lib.pfc_bank_stage(bank, C, row_bytes, next_active, next_n, prev_active, prev_n,
-                               active_cap, slot, bank_version, row_version, version, stale,
-                               stream), "pfc_bank_stage")
+                               prev2_active, prev2_n, active_cap, slot, bank_version,
+                               row_version, version, stale, stream), "pfc_bank_stage")
 
 
 def pfc_bank_patch(prev_slot, prev_active, prev_n, next_active, next_n, active_cap, row_bytes,
@@ -140,7 +140,8 @@ def pfc_bank_patch(prev_slot, prev_active, prev_n, next_active, next_n, active_c
                                row_bytes, next_slot, stream), "pfc_bank_patch")
 
 
-def pfc_bank_writeback(slot, active, n_active, active_cap, row_bytes, C, bank, bank_version,
-                       version, stream):
-    _check(_lib.pfc_bank_writeback(slot, active, n_active, active_cap, row_bytes, C, bank,
-                                   bank_version, version, stream), "pfc_bank_writeback")
+def pfc_bank_writeback(slot, active, n_active, next_active, next_n, active_cap, row_bytes, C,
+                       bank, bank_version, version, stream):
+    _check(_lib.pfc_bank_writeback(slot, active, n_active, next_active, next_n, active_cap,
+                                   row_bytes, C, bank, bank_version, version, stream),
+           "pfc_bank_writeback")

@@ -158,8 +158,8 @@ def test_backward_rejects_before_launch(kw, status):
 
 def _stage_args(**kw):
     a = dict(bank=FAKE, C=1000, row_bytes=256, next_active=FAKE, next_n=FAKE, prev_active=0,
-             prev_n=0, active_cap=100, slot=FAKE, bank_version=0, row_version=0, version=1,
-             stale=0, stream=0)
+             prev_n=0, prev2_active=0, prev2_n=0, active_cap=100, slot=FAKE, bank_version=0,
+             row_version=0, version=1, stale=0, stream=0)
     a.update(kw)
     return a
 
@@ -169,6 +169,7 @@ def _stage_args(**kw):
     dict(C=0), dict(row_bytes=8), dict(row_bytes=24), dict(row_bytes=1 << 17),
     dict(active_cap=0),
     dict(prev_active=FAKE),                   # a previous list without its count
+    dict(prev2_n=FAKE),
     dict(bank_version=FAKE),                  # versions come in pairs
 ])
 def test_bank_stage_rejects_before_launch(kw):
@@ -192,10 +193,11 @@ def test_bank_patch_rejects_before_launch(kw):
     assert e.value.status == pfc.PFC_ERR_INVALID_ARG
 
 
-@pytest.mark.parametrize("kw", [dict(slot=0), dict(bank=0), dict(C=-1), dict(row_bytes=100)])
+@pytest.mark.parametrize("kw", [dict(slot=0), dict(bank=0), dict(C=-1), dict(row_bytes=100),
+                                dict(next_active=FAKE)])
 def test_bank_writeback_rejects_before_launch(kw):
-    a = dict(slot=FAKE, active=FAKE, n_active=FAKE, active_cap=100, row_bytes=256, C=1000,
-             bank=FAKE, bank_version=0, version=1, stream=0)
+    a = dict(slot=FAKE, active=FAKE, n_active=FAKE, next_active=0, next_n=0, active_cap=100,
+             row_bytes=256, C=1000, bank=FAKE, bank_version=0, version=1, stream=0)
     a.update(kw)
     with pytest.raises(pfc.PfcError) as e:
         pfc.pfc_bank_writeback(**a)

@@ -44,15 +44,17 @@ def _inputs(B, d, C, dtype, T, seed, dev, span):
     return W, M, Xs, Ls
 
 
+@pytest.mark.parametrize("n_slots", [2, 3])
 @pytest.mark.parametrize("dtype,B,d,C,r,margin,m,master", [
     ("f32", 64, 128, 10000, 0.1, "cosface", 0.4, False),
     ("bf16", 200, 256, 30000, 0.1, "arcface", 0.5, True),
     ("f16", 300, 512, 40000, 0.2, "arcface", 0.5, False),
 ])
-def test_tiered_equals_resident(dev, dtype, B, d, C, r, margin, m, master):
+def test_tiered_equals_resident(dev, dtype, B, d, C, r, margin, m, master, n_slots):
     from paper_2010_05222_amd.head import PfcShard, TieredShard
-    T = 5
-    print(f"\ntiered dtype={dtype} B={B} d={d} C={C} r={r} master={master}", flush=True)
+    T = 6
+    print(f"\ntiered dtype={dtype} B={B} d={d} C={C} r={r} master={master} slots={n_slots}",
+          flush=True)
     W, M, Xs, Ls = _inputs(B, d, C, dtype, T, 21, dev, span=C // 8)
     seeds = [100 + t for t in range(T)]
     kw = dict(dtype=dtype, s=64.0, m=m, margin=margin, lr=0.1, mu=0.9, device=dev)
@@ -61,7 +63,7 @@ def test_tiered_equals_resident(dev, dtype, B, d, C, r, margin, m, master):
     Md = torch.from_numpy(M).to(dev)
     Pd = torch.from_numpy(W).to(dev) if master else None
     res = PfcShard(B, d, C, r, **kw)
-    ts = TieredShard(B, d, C, r, master=master, **kw)
+    ts = TieredShard(B, d, C, r, master=master, n_slots=n_slots, **kw)
     ts.W_bank.copy_(Wd.cpu())
     ts.M_bank.copy_(Md.cpu())
     if master:
@@ -128,11 +130,12 @@ def test_tiered_fp32_matches_oracle_over_steps(dev):
     assert np.array_equal(Mb[~touched], M.astype(np.float64)[~touched])
 
 
-def test_versions_and_stale_rows(dev):
+@pytest.mark.parametrize("n_slots", [2, 3])
+def test_versions_and_stale_rows(dev, n_slots):
     from paper_2010_05222_amd.head import TieredShard
     B, d, C, r, T = 128, 128, 20000, 0.1, 4
     W, M, Xs, Ls = _inputs(B, d, C, "bf16", T, 23, dev, span=C // 8)
-    ts = TieredShard(B, d, C, r, dtype="bf16", device=dev)
+    ts = TieredShard(B, d, C, r, dtype="bf16", device=dev, n_slots=n_slots)
     ts.W_bank.copy_(torch.from_numpy(W).to(torch.bfloat16))
     ts.M_bank.copy_(torch.from_numpy(M))
     ts.begin(Ls[0], 0)
@@ -149,21 +152,26 @@ def test_versions_and_stale_rows(dev):
 
     # A row staged while its update is unwritten: raise every row's staged
     # version before step 1's staging of step 2, so that each cold row of
-    # S(2) finds an older version in the bank.
-    ts2 = TieredShard(B, d, C, r, dtype="bf16", device=dev)
+    # S(2) (in no set still held in a slot) finds an older version in the bank.
+    ts2 = TieredShard(B, d, C, r, dtype="bf16", device=dev, n_slots=n_slots)
     ts2.W_bank.copy_(torch.from_numpy(W).to(torch.bfloat16))
     ts2.M_bank.copy_(torch.from_numpy(M))
     ts2.begin(Ls[0], 0)
+    p0 = ts2.parts[0]
+    a0 = None
     ts2.step(Xs[0], Ls[1], 1)
     torch.cuda.synchronize()        # step 1's staging is done before the versions move
+    a0 = p0.active[:int(p0.n_active.item())].cpu().numpy()
     ts2.row_version += 1000
-    s1 = ts2.parts[1]
+    p1, p2 = ts2.parts[1], ts2.parts[2 % n_slots]
     ts2.step(Xs[1], Ls[2], 2)
+    torch.cuda.synchronize()
+    a1 = p1.active[:int(p1.n_active.item())].cpu().numpy()
+    a2 = p2.active[:int(p2.n_active.item())].cpu().numpy()
     ts2.step(Xs[2], None, None)
     n_stale = ts2.stale_rows()
-    a1 = s1.active[:int(s1.n_active.item())].cpu().numpy()
-    a2 = ts2.parts[0].active[:int(ts2.parts[0].n_active.item())].cpu().numpy()
-    assert n_stale == len(np.setdiff1d(a2, a1)) > 0
+    held = a1 if n_slots == 2 else np.union1d(a1, a0)
+    assert n_stale == len(np.setdiff1d(a2, held)) > 0
 
 
 def test_bank_rejects_pageable_memory(dev):
@@ -175,10 +183,10 @@ def test_bank_rejects_pageable_memory(dev):
     n = torch.full((1,), cap, dtype=torch.int32, device=dev)
     with pytest.raises(pfc.PfcError) as e:
         pfc.pfc_bank_stage(pageable.data_ptr(), 1000, d * 4, ids.data_ptr(), n.data_ptr(), 0, 0,
-                           cap, slot.data_ptr(), 0, 0, 1, 0, 0)
+                           0, 0, cap, slot.data_ptr(), 0, 0, 1, 0, 0)
     assert e.value.status == pfc.PFC_ERR_INVALID_ARG
     with pytest.raises(pfc.PfcError) as e:
-        pfc.pfc_bank_writeback(slot.data_ptr(), ids.data_ptr(), n.data_ptr(), cap, d * 4, 1000,
-                               pageable.data_ptr(), 0, 1, 0)
+        pfc.pfc_bank_writeback(slot.data_ptr(), ids.data_ptr(), n.data_ptr(), 0, 0, cap, d * 4,
+                               1000, pageable.data_ptr(), 0, 1, 0)
     assert e.value.status == pfc.PFC_ERR_INVALID_ARG
     torch.cuda.synchronize()
