@@ -251,7 +251,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU's class shard only (asked for --gpus {args.gpus}, "
-              f"WORLD_SIZE {world}); multi-GPU runs are not part of this build.", flush=True)
+              f"WORLD_SIZE {world}); runs over several GPUs are not supported.", flush=True)
         sys.exit(2)
 
     import numpy as np
