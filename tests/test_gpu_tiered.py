@@ -190,3 +190,54 @@ def test_bank_rejects_pageable_memory(dev):
                                1000, pageable.data_ptr(), 0, 1, 0)
     assert e.value.status == pfc.PFC_ERR_INVALID_ARG
     torch.cuda.synchronize()
+
+
+def test_tiered_full_size_equals_resident(dev):
+    """The massive workload (C = 8M, |S| = 800,000, fp16 W, fp32 momentum) with
+    its bank in pinned host memory, three steps, against the same steps on the
+    resident shard: every step's loss, row_lse and dX bit for bit, and sampled
+    bank rows (touched and untouched) against the resident shard afterwards."""
+    import workloads
+    from paper_2010_05222_amd.head import PfcShard, TieredShard
+    cfg = workloads.config("massive")
+    B, d, C, r, T = cfg["B"], cfg["d"], cfg["C"], cfg["r"], 3
+    tdt = torch.float16
+    kw = dict(dtype=cfg["dtype"], class_offset=cfg["a"], s=cfg["s"], m=cfg["m"],
+              margin=cfg["margin"], lr=cfg["lr"], mu=cfg["mu"], device=dev)
+    print(f"\ntiered full size: B={B} d={d} C={C} r={r}", flush=True)
+    W, _ = workloads.make_weights_device(cfg, dev)
+    M = torch.zeros((C, d), dtype=torch.float32, device=dev)
+    ts = TieredShard(B, d, C, r, **kw)
+    ts.W_bank.copy_(W)
+    res = PfcShard(B, d, C, r, **kw)
+    batches = []
+    for t in range(T):
+        X, L = workloads.make_batch(cfg, t)
+        batches.append((torch.from_numpy(X).to(tdt).to(dev), torch.from_numpy(L).to(dev)))
+    torch.cuda.synchronize()
+    print("inputs ready", flush=True)
+    ts.begin(batches[0][1], 0)
+    touched = torch.zeros(C, dtype=torch.bool, device=dev)
+    for t in range(T):
+        out = ts.step(batches[t][0], batches[t + 1][1] if t + 1 < T else None, t + 1)
+        res.step(batches[t][0], batches[t][1], W, M, t)
+        torch.cuda.synchronize()
+        K = int(res.n_active.item())
+        assert int(out.n_active.item()) == K
+        assert torch.equal(out.active[:K], res.active[:K])
+        assert torch.equal(out.loss, res.loss), (t, out.loss.item(), res.loss.item())
+        assert torch.equal(out.row_lse, res.row_lse)
+        assert torch.equal(out.dX, res.dX)
+        touched[res.active[:K].long()] = True
+        print(f"step {t}: |S|={K} loss={out.loss.item():.4f} equal", flush=True)
+    assert ts.stale_rows() == 0
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(5)
+    t_ids = torch.nonzero(touched).flatten().cpu().numpy()
+    u_ids = torch.nonzero(~touched).flatten().cpu().numpy()
+    pick = np.concatenate([rng.choice(t_ids, 20000, replace=False),
+                           rng.choice(u_ids, 5000, replace=False)])
+    pick_t = torch.from_numpy(pick)
+    assert torch.equal(ts.W_bank[pick_t], W[pick_t.to(dev)].cpu())
+    assert torch.equal(ts.M_bank[pick_t], M[pick_t.to(dev)].cpu())
+    print(f"bank rows equal: {len(pick)} sampled of {len(t_ids)} touched", flush=True)
