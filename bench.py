@@ -232,6 +232,41 @@ def run_tiered(args, cfg):
     }), flush=True)
 
 
+def measured_ceilings(dev, dtype):
+    """What plain library work reaches on this GPU, next to the published
+    peaks: a large 16-bit GEMM (torch.matmul, 8192^3, the library's own MFMA
+    kernel) and a 1 GiB device-to-device copy."""
+    import torch
+    tdt = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}[dtype]
+    n = 8192
+    a = torch.randn((n, n), device=dev).to(tdt).contiguous()
+    b = torch.randn((n, n), device=dev).to(tdt).contiguous()
+    for _ in range(3):
+        torch.matmul(a, b)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 20
+    e0.record()
+    for _ in range(reps):
+        torch.matmul(a, b)
+    e1.record()
+    torch.cuda.synchronize()
+    gemm_tflops = 2.0 * n ** 3 * reps / (e0.elapsed_time(e1) * 1e-3) / 1e12
+    del a, b
+    src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    copy_gbps = 2.0 * (1 << 30) * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"gemm_8192_tflops": gemm_tflops, "copy_1GiB_GBps": copy_gbps,
+            "gemm_dtype": dtype}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -355,6 +390,18 @@ def main():
         if fl or nb:
             stage_roofs[name] = roofline_entry(name, cfg, K, ms, None)["frac"]
 
+    ceil = measured_ceilings(dev, cfg["dtype"] if cfg["dtype"] != "f32" else "bf16")
+    log(f"[bench] measured ceilings: {ceil['gemm_8192_tflops']:.0f} TFLOP/s "
+        f"({ceil['gemm_dtype']} GEMM 8192^3), {ceil['copy_1GiB_GBps']:.0f} GB/s (1 GiB copy)")
+    dw_bytes = cm.update_bytes(K, d, cfg["dtype"], cfg["master"])
+    vs_ceil = {
+        "fwd_gemm": cm.contraction_flops(B, d, K) / (stage_ms["fwd_gemm"] * 1e-3) / 1e12
+        / ceil["gemm_8192_tflops"],
+        "dx_gemm": cm.contraction_flops(B, d, K) / (stage_ms["dx_gemm"] * 1e-3) / 1e12
+        / ceil["gemm_8192_tflops"],
+        "dw_update": dw_bytes / (stage_ms["dw_update"] * 1e-3) / 1e9 / ceil["copy_1GiB_GBps"],
+    }
+
     cpu = None
     if not args.no_cpu_baseline:
         log(f"[bench] CPU oracle on a bounded sample ({args.cpu_rows} rows)...")
@@ -385,6 +432,8 @@ def main():
         "cpu_baseline": cpu,
         "stage_ms": stage_ms,
         "stage_roofline_frac": stage_roofs,
+        "measured_ceilings": ceil,
+        "stage_frac_of_measured_ceiling": vs_ceil,
         "step_mfma_frac": step_fl / (ms_per_step * 1e-3) / (cm.PEAK_TFLOPS[cfg["dtype"]] * 1e12),
         "update_hbm_frac": upd_b / (stage_ms["dw_update"] * 1e-3) / (cm.PEAK_HBM_GBPS * 1e9),
         "last_loss": loss,
