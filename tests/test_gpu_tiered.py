@@ -98,6 +98,55 @@ def test_tiered_equals_resident(dev, dtype, B, d, C, r, margin, m, master, n_slo
         assert torch.equal(ts.P_bank, Pd.cpu())
 
 
+@pytest.mark.parametrize("case", ["pfc_star", "offset_unowned"])
+def test_tiered_filter_and_offset(dev, case):
+    """The PFC* filter (tau = 0.3) and a shard at class offset 5,000 whose
+    batch also holds labels of other shards, tiered against resident."""
+    from paper_2010_05222_amd.head import PfcShard, TieredShard
+    B, d, C, r, T, dtype = 160, 256, 12000, 0.1, 5, "bf16"
+    a = 5000 if case == "offset_unowned" else 0
+    tau = 0.3 if case == "pfc_star" else None
+    rng = np.random.default_rng(24)
+    W = (0.01 * rng.standard_normal((C, d))).astype(np.float32)
+    M = (1e-3 * rng.standard_normal((C, d))).astype(np.float32)
+    Xs, Ls = [], []
+    for t in range(T):
+        X = rng.standard_normal((B, d)).astype(np.float32)
+        lo, hi = (a - 2000, a + C // 6) if case == "offset_unowned" else (0, C // 6)
+        L = rng.integers(lo, hi, size=B).astype(np.int64)
+        if case == "pfc_star":
+            # Rows near a centre of another row's class: negatives above tau.
+            for n in range(0, B, 4):
+                k = int(L[(n + 1) % B])
+                if k != L[n]:
+                    X[n] = (W[k] / np.linalg.norm(W[k]) * np.sqrt(d)
+                            + 0.5 * rng.standard_normal(d)).astype(np.float32)
+        Xs.append(torch.from_numpy(X).to(torch.bfloat16).to(dev))
+        Ls.append(torch.from_numpy(L).to(dev))
+    kw = dict(dtype=dtype, class_offset=a, s=64.0, m=0.5, margin="arcface", lr=0.1, mu=0.9,
+              device=dev, tau=tau)
+    Wd = torch.from_numpy(W).to(torch.bfloat16).to(dev)
+    Md = torch.from_numpy(M).to(dev)
+    res = PfcShard(B, d, C, r, **kw)
+    ts = TieredShard(B, d, C, r, **kw)
+    ts.W_bank.copy_(Wd.cpu())
+    ts.M_bank.copy_(Md.cpu())
+    ts.begin(Ls[0], 0)
+    for t in range(T):
+        res.step(Xs[t], Ls[t], Wd, Md, t)
+        out = ts.step(Xs[t], Ls[t + 1] if t + 1 < T else None, t + 1)
+        torch.cuda.synchronize()
+        assert torch.equal(out.labels_mapped, res.labels_mapped)
+        assert torch.equal(out.loss, res.loss), (t, out.loss.item(), res.loss.item())
+        assert torch.equal(out.dX, res.dX)
+        if case == "offset_unowned":
+            assert int((out.labels_mapped < 0).sum().item()) > 0
+    assert ts.stale_rows() == 0
+    torch.cuda.synchronize()
+    assert torch.equal(ts.W_bank, Wd.cpu())
+    assert torch.equal(ts.M_bank, Md.cpu())
+
+
 def test_tiered_fp32_matches_oracle_over_steps(dev):
     """Three fp32 steps on the bank against the oracle's three lazy steps."""
     from paper_2010_05222_amd.head import TieredShard
