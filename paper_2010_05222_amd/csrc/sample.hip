@@ -279,24 +279,46 @@ __global__ void __launch_bounds__(1024) k_select_top(const uint32_t* hist, int t
   }
 }
 
-// Collect the non-positive classes whose key's top bits equal the bucket,
-// with their full keys: kCompactPer classes per thread, one slot reservation
-// per wave.
-__global__ void __launch_bounds__(256) k_collect(const uint16_t* digits, const uint32_t* bitmap,
-                                                 int64_t C, uint64_t seed, int64_t a,
-                                                 SampleState* st, uint32_t* cand,
-                                                 uint64_t* cand_key) {
-  if (st->mode != kSelectKeys) return;
+// One workgroup per compaction group (kCompactClasses classes, kCompactPer per
+// thread).  Counts the group's classes that the top-bit digit already selects
+// (positives, and non-positives below the threshold's bucket; every class when
+// all are taken, the positives when no negative is), and collects the
+// non-positive classes of the bucket with their full keys (one slot
+// reservation per wave).  The bucket's classes are added to their groups'
+// counts once the threshold is known (k_refine).
+__global__ void __launch_bounds__(kCompactThreads) k_collect(
+    const uint16_t* digits, const uint32_t* bitmap, int64_t C, uint64_t seed, int64_t a,
+    SampleState* st, uint32_t* cand, uint64_t* cand_key, uint32_t* grp_sure, uint32_t* grp_tie) {
+  __shared__ uint32_t smem[kCompactThreads / 64];
+  const uint32_t mode = st->mode;
   const uint32_t digit = st->top_digit;
   const int64_t c0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * kCompactPer;
-  uint32_t take = 0;
+  uint32_t take = 0, base_bits = 0;
   if (c0 < C) {
     const uint32_t pos = (bitmap[c0 >> 5] >> (c0 & 31)) & 0xFFFFu;
-    uint32_t w[8];
-    load_digits16(digits, c0, w);
+    const uint32_t live = C - c0 >= kCompactPer ? 0xFFFFu : (1u << (C - c0)) - 1u;
+    if (mode == kSelectAll) {
+      base_bits = live;
+    } else if (mode == kSelectNone) {
+      base_bits = pos & live;
+    } else {
+      uint32_t w[8];
+      load_digits16(digits, c0, w);
 #pragma unroll
-    for (int i = 0; i < kCompactPer; ++i)
-      if (c0 + i < C && digit_of(w, i) == digit && !((pos >> i) & 1u)) take |= 1u << i;
+      for (int i = 0; i < kCompactPer; ++i) {
+        const uint32_t dg = digit_of(w, i);
+        if (dg < digit) base_bits |= 1u << i;
+        else if (dg == digit) take |= 1u << i;
+      }
+      base_bits = (base_bits | pos) & live;
+      take &= ~pos & live;
+    }
+  }
+  uint32_t tot;
+  block_exclusive_scan((uint32_t)__popc(base_bits), smem, &tot);
+  if (threadIdx.x == 0) {
+    grp_sure[blockIdx.x] = tot;
+    grp_tie[blockIdx.x] = 0u;
   }
   const uint32_t n = (uint32_t)__popc(take);
   if (__ballot(n != 0) == 0) return;
@@ -321,8 +343,9 @@ __global__ void __launch_bounds__(256) k_collect(const uint16_t* digits, const u
 
 // One workgroup: resolve the remaining 64 - top_bits bits of the threshold
 // among the collected candidates, 11 bits per round.
-__global__ void __launch_bounds__(1024) k_refine(const uint64_t* cand_key, int top_bits,
-                                                 SampleState* st) {
+__global__ void __launch_bounds__(1024) k_refine(const uint32_t* cand, const uint64_t* cand_key,
+                                                 int top_bits, SampleState* st,
+                                                 uint32_t* grp_sure, uint32_t* grp_tie) {
   if (st->mode != kSelectKeys) return;
   constexpr int kBits = 11;
   __shared__ uint32_t lh[1 << kBits];
@@ -352,6 +375,14 @@ __global__ void __launch_bounds__(1024) k_refine(const uint64_t* cand_key, int t
   if (threadIdx.x == 0) {
     st->thresh = prefix;
     st->k_rem = k;
+  }
+  // The bucket's classes join their groups' counts: below the threshold they
+  // are selected, equal to it they are ties (taken in class order).
+  for (uint32_t i = threadIdx.x; i < n; i += blockDim.x) {
+    const uint64_t key = cand_key[i];
+    const uint32_t g = cand[i] / (uint32_t)kCompactClasses;
+    if (key < prefix) atomicAdd(&grp_sure[g], 1u);
+    else if (key == prefix) atomicAdd(&grp_tie[g], 1u);
   }
 }
 
@@ -400,22 +431,6 @@ __device__ __forceinline__ void class_flags(const uint16_t* digits, const uint32
   }
   *sure = s;
   *tie = t;
-}
-
-__global__ void __launch_bounds__(kCompactThreads) k_compact_count(
-    const uint16_t* digits, const uint32_t* bitmap, int64_t C, uint64_t seed, int64_t a,
-    const SampleState* st, uint32_t* grp_sure, uint32_t* grp_tie) {
-  __shared__ uint32_t smem[kCompactThreads / 64];
-  const int64_t c0 = ((int64_t)blockIdx.x * kCompactThreads + threadIdx.x) * kCompactPer;
-  uint32_t s, t;
-  class_flags(digits, bitmap, C, seed, a, st, c0, &s, &t);
-  uint32_t tot_s, tot_t;
-  block_exclusive_scan((uint32_t)__popc(s), smem, &tot_s);
-  block_exclusive_scan((uint32_t)__popc(t), smem, &tot_t);
-  if (threadIdx.x == 0) {
-    grp_sure[blockIdx.x] = tot_s;
-    grp_tie[blockIdx.x] = tot_t;
-  }
 }
 
 // One workgroup of 1024 threads: per-group tie offsets, selected counts and
@@ -546,11 +561,11 @@ hipError_t launch_sample(const int64_t* labels, int64_t B, int64_t C, int64_t a,
   hipLaunchKernelGGL(k_keys_hist, dim3((unsigned)(hist_wgs < 512 ? hist_wgs : 512)), dim3(256), 0,
                      stream, seed, a, C, top_bits, w.bitmap, w.digits, w.hist, w.state);
   hipLaunchKernelGGL(k_select_top, dim3(1), dim3(1024), 0, stream, w.hist, top_bits, w.state);
-  hipLaunchKernelGGL(k_collect, dim3((unsigned)ceil_div(C, 256 * kCompactPer)), dim3(256), 0, stream,
-                     w.digits, w.bitmap, C, seed, a, w.state, w.cand, w.cand_key);
-  hipLaunchKernelGGL(k_refine, dim3(1), dim3(1024), 0, stream, w.cand_key, top_bits, w.state);
-  hipLaunchKernelGGL(k_compact_count, dim3((unsigned)n_groups), dim3(kCompactThreads), 0, stream,
-                     w.digits, w.bitmap, C, seed, a, w.state, w.grp_sure, w.grp_tie);
+  hipLaunchKernelGGL(k_collect, dim3((unsigned)n_groups), dim3(kCompactThreads), 0, stream,
+                     w.digits, w.bitmap, C, seed, a, w.state, w.cand, w.cand_key, w.grp_sure,
+                     w.grp_tie);
+  hipLaunchKernelGGL(k_refine, dim3(1), dim3(1024), 0, stream, w.cand, w.cand_key, top_bits,
+                     w.state, w.grp_sure, w.grp_tie);
   hipLaunchKernelGGL(k_compact_scan, dim3(1), dim3(1024), 0, stream, w.grp_sure, w.grp_tie,
                      n_groups, w.state, cap, w.grp_out, w.grp_tie_off, n_active);
   hipLaunchKernelGGL(k_compact_write, dim3((unsigned)n_groups), dim3(kCompactThreads), 0, stream,
