@@ -351,6 +351,7 @@ __global__ void __launch_bounds__(1024) k_refine(const uint32_t* cand, const uin
   __shared__ uint32_t lh[1 << kBits];
   __shared__ uint64_t scan_smem[16];
   __shared__ int64_t found[3];
+  __shared__ uint64_t sole;
   const uint32_t n = st->cand_count;
   uint64_t prefix = st->top_digit;
   int known = top_bits;
@@ -370,6 +371,16 @@ __global__ void __launch_bounds__(1024) k_refine(const uint32_t* cand, const uin
     prefix = (prefix << bits) | (uint64_t)found[0];
     k -= found[1];
     known += bits;
+    if (found[2] == 1 && known < 64) {
+      // The bin holds a single key (k is then 1): that key is the threshold.
+      for (uint32_t i = threadIdx.x; i < n; i += blockDim.x) {
+        const uint64_t key = cand_key[i];
+        if ((key >> (64 - known)) == prefix) sole = key;
+      }
+      __syncthreads();
+      prefix = sole;
+      known = 64;
+    }
     __syncthreads();
   }
   if (threadIdx.x == 0) {
