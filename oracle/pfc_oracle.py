@@ -70,7 +70,7 @@ def sample_active(labels, C, a, r, seed):
     S = P  union  Sample([0, C) minus P, max(b - |P|, 0)), sorted ascending;
     labels_mapped = searchsorted(S, y_local) for owned rows, else -1.
 
-    "Sample without replacement" is unspecified in the paper.  Reading: each
+    The paper does not say how the draw without replacement is made.  Reading: each
     class c gets the 64-bit key of its global id a + c (see philox.class_keys)
     and the negatives are the max(b - |P|, 0) non-positive classes with the
     smallest (key, c) pairs in lexicographic order.  That is a uniformly random
