@@ -3,7 +3,7 @@
 // for the step (Sec. 3.3.3, the paragraph on asynchronous hierarchical class
 // storage, and Fig. async_pipeline).
 //
-// Three copies, each a row per wave at a time, 16 bytes per lane:
+// Three row copies, 16 bytes per lane, eight rows per wave at a time:
 //  - stage:     cold rows of S(t+1) - those in neither of the (up to two)
 //               previous active sets still held in slots - from the bank
 //               into the next slot, with a check of the per-row versions
@@ -16,11 +16,12 @@
 //               their newer values).
 // The host side of each copy goes over the host link with ordinary vector
 // loads and stores on the mapped pinned pages; the device side is HBM.
-// Membership in S(t) is a binary search over its sorted id list.  The copies
-// run on a fixed grid of 2048 waves that walks the rows, eight rows per wave
-// at a time with all eight loads issued before the stores: they wait on the
-// host link most of the time, and a grid of one wave per row would hold the
-// CUs and starve the step's kernels running beside them on other streams.
+// Membership in S(t) is a binary search over its sorted id list.  The two
+// host-link copies run on a fixed grid of 2048 waves that walks the rows, with
+// all eight loads of a group issued before its stores: they wait on the host
+// link most of the time, and a grid of one wave per row would hold the CUs
+// and starve the step's kernels running beside them on other streams.  The
+// patch, a device-to-device copy, takes one wave per group of rows.
 #include "pfc_device.h"
 #include "pfc.h"
 
