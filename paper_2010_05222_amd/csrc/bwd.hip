@@ -841,10 +841,18 @@ __global__ void __launch_bounds__(512) k_dw16(
       bt.mv[k][h] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
       if constexpr (MASTER) bt.pv[k][h] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
       if (lane_on) {
-        bt.wv[k][h] = *reinterpret_cast<const uint2*>(reinterpret_cast<const char*>(W + rb) + 2 * o);
-        bt.mv[k][h] = *reinterpret_cast<const float4*>(reinterpret_cast<const char*>(M + rb) + 4 * o);
-        if constexpr (MASTER)
-          bt.pv[k][h] = *reinterpret_cast<const float4*>(reinterpret_cast<const char*>(W_master + rb) + 4 * o);
+        // Non-temporal: each row is read once here and written back once.
+        const u32x2_t w2 = __builtin_nontemporal_load(
+            reinterpret_cast<const u32x2_t*>(reinterpret_cast<const char*>(W + rb) + 2 * o));
+        const f32x4_t m4 = __builtin_nontemporal_load(
+            reinterpret_cast<const f32x4_t*>(reinterpret_cast<const char*>(M + rb) + 4 * o));
+        bt.wv[k][h] = make_uint2(w2.x, w2.y);
+        bt.mv[k][h] = make_float4(m4.x, m4.y, m4.z, m4.w);
+        if constexpr (MASTER) {
+          const f32x4_t p4 = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(
+              reinterpret_cast<const char*>(W_master + rb) + 4 * o));
+          bt.pv[k][h] = make_float4(p4.x, p4.y, p4.z, p4.w);
+        }
       }
     }
   };
