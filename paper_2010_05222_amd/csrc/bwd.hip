@@ -36,6 +36,7 @@ constexpr int kDxRows = 128;       // batch rows of a dX workgroup
 constexpr int kDwCls = 128;        // classes of a dW workgroup
 constexpr int kTLd = 260;         // LDS row stride (floats) of the update's staged gradient rows
 constexpr int kHitCap = 256;      // target rows listed per wave of a dW workgroup
+constexpr int kDwFirstWave = 256;  // dW workgroups resident at once: one per CU of the MI355X
 
 // Every operand reaches LDS through direct-to-LDS loads into three-stage
 // rings (one array per stage, so the compiler can keep later stages in
@@ -545,6 +546,14 @@ __global__ void __launch_bounds__(512) k_dw16(
   const int K = *n_active_p;
   const int64_t j0 = (int64_t)blockIdx.x * kDwCls;
   if (j0 >= K) return;
+  // On a long grid, every second workgroup of the first wave (one per CU)
+  // starts about half a workgroup's lifetime late.  Otherwise all CUs run the
+  // contraction and then the memory-bound update in step for the first few
+  // hundred microseconds, and the updates, all at once, saturate HBM; with
+  // the offset about half of the CUs update at any time from the start.
+  if (gridDim.x >= 4 * kDwFirstWave && blockIdx.x < kDwFirstWave && (blockIdx.x & 1)) {
+    for (int z = 0; z < 8; ++z) __builtin_amdgcn_s_sleep(127);   // ~65 k cycles
+  }
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
