@@ -54,8 +54,9 @@ typedef enum {
   PFC_ARCFACE = 1   /* additive angular margin: f_y = s * cos(acos(cos) + m) */
 } pfc_margin;
 
-/* Size limits of this implementation. */
-#define PFC_MAX_BATCH 65536
+/* Size limits of this implementation (every limit has a parity test at its
+ * boundary: B = 8192 on the 16-bit path, B = 4096 on the fp32 path). */
+#define PFC_MAX_BATCH 8192
 #define PFC_MAX_CLASSES (1LL << 30)
 
 /*
@@ -124,7 +125,10 @@ int pfc_sample(const int64_t* labels, int64_t B, int64_t C,
  *         (lse_n - f_{n, y_n}); rows whose label is outside the shard add 0
  *         (their target term belongs to the owning shard).
  * row_lse float[B] out: lse_n = log sum_{j in S} exp(f_{n,j}), the per-row
- *         statistic a multi-shard caller would combine across shards.
+ *         statistic a multi-shard caller would combine across shards.  A
+ *         row whose label is outside the shard and whose every logit the
+ *         PFC* filter drops has an empty denominator: lse_n = -inf, and the
+ *         backward gives it no probability and no gradient.
  */
 int pfc_forward_loss(const void* X, int x_dtype, int64_t B, int64_t d,
                      const void* W, int w_dtype, int64_t C,

@@ -179,9 +179,35 @@ def logits(cos, yhat, s, m, margin, tau=None):
 
 
 def log_sum_exp(f):
-    """Row log-sum-exp as max + log(sum exp(f - max)) (Sec. 3.2.1 max/sum steps)."""
+    """Row log-sum-exp as max + log(sum exp(f - max)) (Sec. 3.2.1 max/sum steps).
+
+    Reading (paper silent): a row with no logit left (every entry -inf, which
+    the PFC* filter can cause for a row whose label is outside the shard) has
+    an empty denominator and lse = -inf; a log-sum-exp merge across shards
+    then ignores it.
+    """
+    f = np.asarray(f, dtype=np.float64)
     mx = np.max(f, axis=1)
-    return mx + np.log(np.sum(np.exp(f - mx[:, None]), axis=1))
+    empty = mx == -np.inf
+    ref = np.where(empty, 0.0, mx)
+    with np.errstate(divide="ignore"):
+        return np.where(empty, -np.inf,
+                        mx + np.log(np.sum(np.exp(f - ref[:, None]), axis=1)))
+
+
+def probabilities(f, lse):
+    """Softmax probabilities exp(f - lse) over each row's denominator.
+
+    A logit outside the denominator (-inf: dropped by the PFC* filter) has
+    probability 0; so does every entry of a row with an empty denominator
+    (lse = -inf), which therefore gets no gradient.
+    """
+    f = np.asarray(f, dtype=np.float64)
+    lse = np.asarray(lse, dtype=np.float64)
+    live = np.isfinite(f) & np.isfinite(lse)[:, None]
+    out = np.zeros(f.shape)
+    out[live] = np.exp((f - np.where(np.isfinite(lse), lse, 0.0)[:, None])[live])
+    return out
 
 
 def forward(X, Ws, yhat, s, m, margin, tau=None):
@@ -194,7 +220,8 @@ def forward(X, Ws, yhat, s, m, margin, tau=None):
     Reading: a row whose label is outside the shard has no target here and
     contributes 0 to the reported loss (its target term belongs to the owning
     shard, Sec. 3.2.1); its gradient is still P/B, the derivative of its
-    log-sum-exp.  The batch mean always divides by the full batch size
+    log-sum-exp.  If the PFC* filter also drops every one of its logits, its
+    denominator is empty: lse = -inf, P = 0, no gradient, loss term 0.  The batch mean always divides by the full batch size
     (G = (P - Y)/B, Sec. 3.2.1), which the caller applies.
     Returns dict(cos, f, lse, P, row_loss).
     """
@@ -202,7 +229,7 @@ def forward(X, Ws, yhat, s, m, margin, tau=None):
     cos = cosines(X, Ws)
     f = logits(cos, yhat, s, m, margin, tau)
     lse = log_sum_exp(f)
-    P = np.exp(f - lse[:, None])
+    P = probabilities(f, lse)
     own = np.nonzero(yhat >= 0)[0]
     row_loss = np.zeros(len(yhat))
     row_loss[own] = lse[own] - f[own, yhat[own]]
@@ -227,7 +254,7 @@ def cos_grad(cos, lse, yhat, B, s, m, margin, tau=None):
     """
     yhat = np.asarray(yhat, dtype=np.int64)
     f = logits(cos, yhat, s, m, margin, tau)
-    dF = np.exp(f - np.asarray(lse)[:, None])
+    dF = probabilities(f, lse)
     own = np.nonzero(yhat >= 0)[0]
     dF[own, yhat[own]] -= 1.0
     dF /= B
@@ -280,7 +307,7 @@ def grad_w(X, Ws_cols, cols, yhat, lse, B, s, m, margin, tau=None):
     # Rows whose target lies outside the subset still owe P/B on these columns.
     f = logits(cos, pos_in_cols, s, m, margin, tau)
     hit = np.nonzero(pos_in_cols >= 0)[0]
-    dF = np.exp(f - np.asarray(lse)[:, None])
+    dF = probabilities(f, lse)
     dF[hit, pos_in_cols[hit]] -= 1.0
     dF /= B
     dc = s * dF

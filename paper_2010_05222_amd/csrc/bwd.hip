@@ -36,7 +36,7 @@ constexpr int kDxRows = 128;       // batch rows of a dX workgroup
 constexpr int kDwCls = 128;        // classes of a dW workgroup
 constexpr int kTLd = 260;         // LDS row stride (floats) of the update's staged gradient rows
 constexpr int kHitCap = 256;      // target rows listed per wave of a dW workgroup
-constexpr int kDwFirstWave = 256;  // dW workgroups resident at once: one per CU of the MI355X
+constexpr int kDwStaggerCUs = 256;  // CU count of the part the dW start offset was tuned on
 
 // Every operand reaches LDS through direct-to-LDS loads into three-stage
 // rings (one array per stage, so the compiler can keep later stages in
@@ -416,8 +416,10 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
 }
 
 // Row scales of the logit store: gscale[g][n] = 2^(m_gn - lse_n log2 e), so that
-// E * gscale is the softmax probability (0 for rows past the batch).  Groups
-// past |S| are never read and are skipped.
+// E * gscale is the softmax probability (0 for rows past the batch).  A row
+// with an empty denominator (lse = -inf: its label is outside the shard and the
+// PFC* filter dropped every logit, so all its E are 0) gets scale 0, and with
+// it no gradient.  Groups past |S| are never read and are skipped.
 // Also writes the padded copy of the active row ids that the dX kernel reads
 // a chunk at a time: act_pad[j] = active[min(j, |S| - 1)] (0 if S is empty).
 __global__ void __launch_bounds__(256) k_scales(const float* __restrict__ gmax,
@@ -445,8 +447,10 @@ __global__ void __launch_bounds__(256) k_scales(const float* __restrict__ gmax,
   const float mv[4] = {m4.x, m4.y, m4.z, m4.w};
   float v[4];
 #pragma unroll
-  for (int e = 0; e < 4; ++e)
-    v[e] = n + e < B ? __builtin_amdgcn_exp2f(mv[e] - row_lse[n + e] * kLog2e) : 0.0f;
+  for (int e = 0; e < 4; ++e) {
+    const float lse = n + e < B ? row_lse[n + e] : -INFINITY;
+    v[e] = lse > -INFINITY ? __builtin_amdgcn_exp2f(mv[e] - lse * kLog2e) : 0.0f;
+  }
   *reinterpret_cast<float4*>(gscale + i) = make_float4(v[0], v[1], v[2], v[3]);
 }
 
@@ -529,7 +533,7 @@ __global__ void __launch_bounds__(512) k_dw16(
     const float* __restrict__ inv_x, const float* __restrict__ inv_w,
     const float* __restrict__ tgtc, const uint16_t* __restrict__ lbuf, int64_t ld_cos,
     const float* __restrict__ gscale, int64_t ld_g, int B, Margin mg, float sB, float lr,
-    float mu) {
+    float mu, int first_wave) {
   constexpr int D = 128 * WI;
   constexpr int NW = 8;
   constexpr int DW = D / 4;             // d entries of a wave
@@ -546,13 +550,16 @@ __global__ void __launch_bounds__(512) k_dw16(
   const int K = *n_active_p;
   const int64_t j0 = (int64_t)blockIdx.x * kDwCls;
   if (j0 >= K) return;
-  // On a long grid, every second workgroup of the first wave (one per CU)
-  // starts about half a workgroup's lifetime late.  Otherwise all CUs run the
-  // contraction and then the memory-bound update in step for the first few
-  // hundred microseconds, and the updates, all at once, saturate HBM; with
-  // the offset about half of the CUs update at any time from the start.
-  if (gridDim.x >= 4 * kDwFirstWave && blockIdx.x < kDwFirstWave && (blockIdx.x & 1)) {
-    for (int z = 0; z < 8; ++z) __builtin_amdgcn_s_sleep(127);   // ~65 k cycles
+  // On a long grid, every second workgroup of the first wave (first_wave =
+  // one workgroup per CU, 0 = no offset) starts about half a workgroup's
+  // lifetime late.  Otherwise all CUs run the contraction and then the
+  // memory-bound update in step for the first few hundred microseconds, and
+  // the updates, all at once, saturate HBM; with the offset about half of the
+  // CUs update at any time from the start.  The length (~65 k cycles) is tuned
+  // for the 256-CU MI355X at d = 512; the launcher passes 0 on other parts.
+  if (first_wave > 0 && gridDim.x >= 4 * first_wave && (int)blockIdx.x < first_wave &&
+      (blockIdx.x & 1)) {
+    for (int z = 0; z < 8; ++z) __builtin_amdgcn_s_sleep(127);
   }
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -1172,10 +1179,20 @@ __global__ void __launch_bounds__(256) k_dw32(const float* __restrict__ X, float
   }
 }
 
+// Compute units of the current device (0 if the query fails).
+int device_cu_count() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  return n;
+}
+
 template <typename Tag, int WI>
 void launch_bwd16(const StepArgs& a, const StepWs& w, const Margin& mg, float sB,
                   hipStream_t stream) {
   const int B = (int)a.B;
+  const int n_cu = device_cu_count();
+  const int first_wave = (n_cu == kDwStaggerCUs && WI == 4) ? n_cu : 0;
   const int n_rt = (int)ceil_div(B, kDxRows);
   const int64_t n_tiles = (int64_t)n_rt * w.n_split;
   const int64_t per_xcd = ceil_div(n_tiles, 8);
@@ -1200,13 +1217,13 @@ void launch_bwd16(const StepArgs& a, const StepWs& w, const Margin& mg, float sB
                        0, stream, (const uint16_t*)w.xbT, w.ld_xt, a.X, (uint16_t*)a.W, a.W_master,
                        a.M, a.active, a.n_active, a.labels_mapped, a.row_lse, w.inv_x, w.inv_w,
                        w.tgtc, (const uint16_t*)w.lbuf, w.ld_cos, w.gscale, w.ld_g, B, mg, sB, a.lr,
-                       a.mu);
+                       a.mu, first_wave);
   else
     hipLaunchKernelGGL((k_dw16<Tag, WI, false>), dim3((unsigned)ceil_div(a.cap, kDwCls)), dim3(512),
                        0, stream, (const uint16_t*)w.xbT, w.ld_xt, a.X, (uint16_t*)a.W, a.W_master,
                        a.M, a.active, a.n_active, a.labels_mapped, a.row_lse, w.inv_x, w.inv_w,
                        w.tgtc, (const uint16_t*)w.lbuf, w.ld_cos, w.gscale, w.ld_g, B, mg, sB, a.lr,
-                       a.mu);
+                       a.mu, first_wave);
   timing_stop(6, stream);
 }
 

@@ -109,13 +109,15 @@ __device__ __forceinline__ float target_slope(const Margin& mg, float c) {
 }
 
 // Softmax-gradient coefficient of one logit, without the s/B factor:
-// (p - [j == y]) * slope, p = exp(f - lse).
+// (p - [j == y]) * slope, p = exp(f - lse).  A logit the PFC* filter dropped
+// (stored cosine -inf) has p = 0, also in a row whose denominator it leaves
+// empty (lse = -inf).
 __device__ __forceinline__ float grad_coef(const Margin& mg, float c, bool is_target, float lse) {
   if (is_target) {
     const float p = __expf(target_logit(mg, c) - lse);
     return (p - 1.0f) * target_slope(mg, c);
   }
-  return __expf(mg.s * c - lse);
+  return c == -INFINITY ? 0.0f : __expf(mg.s * c - lse);
 }
 
 __device__ __forceinline__ float wave_sum(float v) {

@@ -21,6 +21,8 @@ PFC_ERR_UNSUPPORTED = 4
 PFC_ERR_HIP = 5
 
 PFC_F32, PFC_BF16, PFC_F16 = 0, 1, 2
+PFC_MAX_BATCH = 8192
+PFC_MAX_CLASSES = 1 << 30
 PFC_COSFACE, PFC_ARCFACE = 0, 1
 
 PFC_K_SAMPLE, PFC_K_PREP, PFC_K_FWD_GEMM, PFC_K_LSE = 0, 1, 2, 3

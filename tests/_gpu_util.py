@@ -60,11 +60,14 @@ def make_problem(B, d, C, dtype, seed, class_offset=0, label_span=None, random_m
     return Xd, Wd, Md, Pd, Ld
 
 
-def run_and_compare(shard, Xd, Wd, Md, Pd, Ld, seed, margin_name, check_sampler_only=False):
+def run_and_compare(shard, Xd, Wd, Md, Pd, Ld, seed, margin_name, check_sampler_only=False,
+                    abs_scaled=False):
     """One step on the GPU and the oracle on the same (rounded) inputs.
 
     Returns a dict of the error figures; asserts the stated bar and the
-    derived bounds."""
+    derived bounds.  The max-abs gradient bar is the stated one unless
+    `abs_scaled`, which multiplies it by max(1, max |ref|) for a case whose
+    gradients are far larger than any workload's (see the single-row test)."""
     dt = shard.dtype_name
     X64 = Xd.double().cpu().numpy()
     W0 = Wd.double().cpu().numpy()
@@ -113,7 +116,12 @@ def run_and_compare(shard, Xd, Wd, Md, Pd, Ld, seed, margin_name, check_sampler_
     g_gpu = M1[active_ref] - mom_ref
 
     out["loss_rel"] = abs(loss - loss_ref) / max(abs(loss_ref), 1e-30)
-    out["lse_abs"] = float(np.max(np.abs(lse - fw["lse"])))
+    # A row with an empty denominator has lse = -inf on both sides.
+    empty = np.isneginf(fw["lse"])
+    assert np.array_equal(np.isneginf(lse), empty), (np.nonzero(np.isneginf(lse))[0],
+                                                     np.nonzero(empty)[0])
+    out["n_empty_rows"] = int(np.sum(empty))
+    out["lse_abs"] = float(np.max(np.abs(lse[~empty] - fw["lse"][~empty]), initial=0.0))
     out["dx_abs"] = float(np.max(np.abs(dx - dx_ref)))
     out["dx_row_rel"] = float(np.max(row_rel_err(dx, dx_ref)))
     out["g_abs"] = float(np.max(np.abs(g_gpu - g_ref)))
@@ -126,10 +134,10 @@ def run_and_compare(shard, Xd, Wd, Md, Pd, Ld, seed, margin_name, check_sampler_
 
     assert out["loss_rel"] <= 1e-3, out
     assert out["lse_abs"] <= (1e-4 if dt == "f32" else 5e-3), out
-    # The absolute bar is stated for gradients of the workloads' scale (|ref| <= 1);
-    # a tiny batch (B = 1 gives s/B = 64) scales it by the reference magnitude.
-    assert out["dx_abs"] <= MAX_ABS[dt] * max(1.0, np.max(np.abs(dx_ref))), out
-    assert out["g_abs"] <= MAX_ABS[dt] * max(1.0, np.max(np.abs(g_ref))), out
+    bar_dx = MAX_ABS[dt] * (max(1.0, np.max(np.abs(dx_ref))) if abs_scaled else 1.0)
+    bar_g = MAX_ABS[dt] * (max(1.0, np.max(np.abs(g_ref))) if abs_scaled else 1.0)
+    assert out["dx_abs"] <= bar_dx, out
+    assert out["g_abs"] <= bar_g, out
     assert out["dx_row_rel"] <= REL_ROW[dt], out
     assert out["g_row_rel"] <= REL_ROW[dt], out
 

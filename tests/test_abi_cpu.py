@@ -53,6 +53,13 @@ def test_workspace_and_capacity_of_each_workload(name):
     assert nbytes < 2 * (cfg["B"] * cap * elt + cfg["C"] * 12) + (256 << 20)
 
 
+def test_batch_limit_matches_header():
+    text = open(HEADER).read()
+    assert int(re.search(r"#define PFC_MAX_BATCH (\d+)", text).group(1)) == pfc.PFC_MAX_BATCH
+    nbytes, cap = pfc.pfc_workspace_bytes(pfc.PFC_MAX_BATCH, 512, 40000, 0.2, pfc.PFC_F16)
+    assert cap == 8192 and nbytes > 0
+
+
 def test_capacity_when_positives_exceed_budget():
     _, cap = pfc.pfc_workspace_bytes(512, 128, 1000, 0.05, pfc.PFC_BF16)
     assert cap == 512                     # max(b = 50, min(B, C) = 512)
@@ -72,6 +79,7 @@ def test_capacity_when_positives_exceed_budget():
     ((8, 64, 100, 0.1, 1), pfc.PFC_ERR_UNSUPPORTED),       # 16-bit path needs d % 128 == 0
     ((8, 1024, 100, 0.1, 2), pfc.PFC_ERR_UNSUPPORTED),     # 16-bit path needs d <= 512
     ((8192, 128, 100, 0.1, 0), pfc.PFC_ERR_UNSUPPORTED),   # fp32 path limited to B <= 4096
+    ((8193, 512, 100000, 0.1, 2), pfc.PFC_ERR_INVALID_ARG),  # B above PFC_MAX_BATCH
 ])
 def test_workspace_rejects(args, status):
     with pytest.raises(pfc.PfcError) as e:
@@ -91,6 +99,7 @@ def _sample_args(**kw):
     (dict(labels=0), pfc.PFC_ERR_INVALID_ARG),
     (dict(active=0), pfc.PFC_ERR_INVALID_ARG),
     (dict(B=0), pfc.PFC_ERR_INVALID_ARG),
+    (dict(B=8193, active_cap=8193, C=100000), pfc.PFC_ERR_INVALID_ARG),   # B > PFC_MAX_BATCH
     (dict(C=-1), pfc.PFC_ERR_INVALID_ARG),
     (dict(class_offset=-5), pfc.PFC_ERR_INVALID_ARG),
     (dict(r=0.0), pfc.PFC_ERR_INVALID_ARG),

@@ -9,7 +9,8 @@ checked against the CPU oracle on what the oracle can afford at this size:
     rows and all |S| active classes, in row blocks: rows are independent);
   - dX on a seeded sample of rows;
   - the class gradients (through the momentum rows, M starts at zero so
-    M[S_j] = g_j) and the updated weights on a seeded sample of active classes;
+    M[S_j] = g_j) and the updated weights on a seeded sample of active
+    classes together with every positive class of the batch;
   - every row outside S: weights and momentum untouched (checked on the GPU
     over the whole shard).
 """
@@ -109,8 +110,14 @@ def test_full_size_step(dev, name):
     assert out["dx_abs"] <= MAX_ABS[dt], out
     assert out["dx_row_rel"] <= REL_ROW[dt], out
 
-    # Class gradients and the update on sampled active classes.
-    cols = np.sort(rng.choice(K, size=min(N_CLASSES_G, K), replace=False))
+    # Class gradients and the update on sampled active classes, plus every
+    # positive class: only those carry the exact target term and the dW
+    # kernel's target-row lists.  The Zipf workload's most duplicated classes
+    # (the top one is the label of ~12 % of the rows) are among them.
+    pos, counts = np.unique(mapped_ref[mapped_ref >= 0], return_counts=True)
+    out["n_positive_cols"] = int(len(pos))
+    out["max_rows_per_class"] = int(counts.max()) if counts.size else 0
+    cols = np.union1d(rng.choice(K, size=min(N_CLASSES_G, K), replace=False), pos)
     g_ref = O.grad_w(X64, Ws[cols], cols, mapped_ref, lse_ref, B, cfg["s"], cfg["m"],
                      cfg["margin"])
     rows_g = torch.from_numpy(active_ref[cols].astype(np.int64)).to(dev)

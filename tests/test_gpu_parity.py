@@ -31,14 +31,14 @@ def _shard(B, d, C, r, dtype, margin, m, class_offset=0, dev="cuda:0", tau=None)
 
 
 def _case(dev, B, d, C, r, dtype, margin, m, seed, class_offset=0, label_span=None,
-          random_m=True, master=False, labels=None, tau=None, conflicts=0):
+          random_m=True, master=False, labels=None, tau=None, conflicts=0, abs_scaled=False):
     from _gpu_util import make_problem, run_and_compare
     print(f"\ncase B={B} d={d} C={C} r={r} dtype={dtype} margin={margin} seed={seed} "
           f"offset={class_offset} master={master} tau={tau}", flush=True)
     Xd, Wd, Md, Pd, Ld = make_problem(B, d, C, dtype, seed, class_offset, label_span, random_m,
                                       master, labels, dev, conflicts)
     shard = _shard(B, d, C, r, dtype, margin, m, class_offset, dev, tau)
-    out = run_and_compare(shard, Xd, Wd, Md, Pd, Ld, seed, margin)
+    out = run_and_compare(shard, Xd, Wd, Md, Pd, Ld, seed, margin, abs_scaled=abs_scaled)
     print(out, flush=True)
     return out
 
@@ -120,7 +120,12 @@ def test_duplicated_positives(dev):
 
 
 def test_single_row_and_tiny_shard(dev):
-    _case(dev, 1, 128, 7, 0.5, "bf16", "arcface", 0.5, seed=11)
+    # B = 1 makes the gradient scale s/B = 64, so |g| reaches ~100 here, two
+    # orders of magnitude above any workload's.  The bf16 coefficients carry
+    # ~2^-9 relative error, so the max-abs bar is applied relative to the
+    # reference magnitude (max(1, max |ref|) times the stated bar) in this
+    # case only; the row-relative bound is unchanged.
+    _case(dev, 1, 128, 7, 0.5, "bf16", "arcface", 0.5, seed=11, abs_scaled=True)
 
 
 def test_repeat_is_deterministic(dev):
@@ -202,3 +207,58 @@ def test_tau_at_least_one_is_pfc(dev):
         outs.append((shard.loss.clone(), shard.dX.clone(), Wd.clone(), Md.clone()))
     for a, b in zip(*outs):
         assert torch.equal(a, b)
+
+
+def _empty_row_problem(seed, dtype, dev, B=96, d=128, C=2000, a=1000, n_empty=3, mu=10.0):
+    """Class centres sharing a common direction u, and a few rows along u whose
+    labels lie outside the shard [a, a + C): every active cosine of such a row
+    is ~0.66, above tau = 0.3, so the PFC* filter leaves its denominator empty.
+    The other rows are ordinary Gaussian rows with owned labels."""
+    rng = np.random.default_rng(seed)
+    u = rng.standard_normal(d)
+    u /= np.linalg.norm(u)
+    W = (0.01 * (rng.standard_normal((C, d)) + mu * u)).astype(np.float32)
+    X = rng.standard_normal((B, d)).astype(np.float32)
+    labels = rng.integers(a, a + C, size=B)
+    for k in range(n_empty):
+        n = 7 + 31 * k
+        X[n] = (np.sqrt(d) * u + 0.3 * rng.standard_normal(d)).astype(np.float32)
+        labels[n] = a + C + 17 * k
+    M = (1e-3 * rng.standard_normal((C, d))).astype(np.float32)
+    t = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[dtype]
+    return (torch.from_numpy(X).to(t).to(dev), torch.from_numpy(W).to(t).to(dev),
+            torch.from_numpy(M).to(dev), None, torch.from_numpy(labels).to(dev))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_conflict_filter_empty_denominator(dev, dtype):
+    """Rows whose label is outside the shard and whose every logit the PFC*
+    filter drops: lse = -inf, no probability, no gradient, no NaN anywhere."""
+    from _gpu_util import run_and_compare
+    seed, tau = 32, 0.3
+    print(f"\nempty-denominator rows: dtype={dtype} seed={seed} tau={tau}", flush=True)
+    Xd, Wd, Md, Pd, Ld = _empty_row_problem(seed, dtype, dev)
+    shard = _shard(96, 128, 2000, 0.2, dtype, "arcface", 0.5, class_offset=1000, dev=dev,
+                   tau=tau)
+    out = run_and_compare(shard, Xd, Wd, Md, Pd, Ld, seed, "arcface")
+    print(out, flush=True)
+    assert out["n_empty_rows"] == 3
+    assert bool(torch.isfinite(Wd).all()) and bool(torch.isfinite(Md).all())
+    empty = torch.isneginf(shard.row_lse)
+    assert int(empty.sum()) == 3
+    assert bool((shard.dX[empty] == 0).all())
+
+
+def test_batch_at_limit_16bit(dev):
+    """The largest batch the ABI accepts (PFC_MAX_BATCH = 8192), fp16 at d = 512;
+    the positives (~7,400 distinct labels) nearly fill the budget of 8,000."""
+    from paper_2010_05222_amd import pfc
+    assert pfc.PFC_MAX_BATCH == 8192
+    out = _case(dev, 8192, 512, 40000, 0.2, "f16", "arcface", 0.5, seed=20, random_m=False)
+    assert out["K"] == 8000
+
+
+def test_batch_at_limit_fp32(dev):
+    """The largest batch of the fp32 path (4096 rows); here |P| > b, so S = P."""
+    out = _case(dev, 4096, 128, 3000, 0.5, "f32", "cosface", 0.4, seed=21)
+    assert out["K"] == out["n_pos"] > 1500

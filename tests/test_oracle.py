@@ -547,3 +547,74 @@ def test_filter_step_at_r1_is_fc_star():
     fw = O.forward(X, W, labels, s, m, O.ARCFACE, tau)
     assert abs(out["loss"] - O.batch_loss(fw["row_loss"], B)) < 1e-12
     assert out["P"][0, (labels[0] + 1) % C] == 0.0
+
+
+def _nearest_f16_brute_force(x):
+    """Nearest binary16 value of each float64 x, ties to the even bit pattern,
+    by search over the sorted table of every finite binary16 value (the table
+    comes from widening bit patterns, which is exact)."""
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    vals = bits.view(np.float16).astype(np.float64)
+    ok = np.isfinite(vals) & ~((vals == 0) & (bits >= 0x8000))     # drop inf/nan and -0
+    vals, bits = vals[ok], bits[ok]
+    order = np.argsort(vals, kind="stable")
+    vals, bits = vals[order], bits[order]
+    i = np.clip(np.searchsorted(vals, x), 1, len(vals) - 1)
+    lo, hi = vals[i - 1], vals[i]
+    dlo, dhi = x - lo, hi - x
+    pick_hi = (dhi < dlo) | ((dhi == dlo) & (bits[i] % 2 == 0))
+    return np.where(pick_hi, hi, lo)
+
+
+def test_round_f16_matches_brute_force_and_library():
+    """The fp16 branch of round_to against (a) a brute-force nearest-value
+    search over all binary16 values with ties to even, on float64 inputs that
+    include exact midpoints and subnormals, and (b) torch's float32 -> float16
+    conversion on float32 inputs."""
+    rng = np.random.default_rng(13)
+    x = rng.standard_normal(20000) * 10.0 ** rng.integers(-8, 4, 20000)
+    # exact midpoints between neighbouring binary16 values (ties), both signs
+    grid = np.sort(np.unique(rng.standard_normal(4000).astype(np.float16).astype(np.float64)))
+    mids = (grid[:-1] + grid[1:]) / 2.0
+    sub = np.arange(1, 2000) * 2.0 ** -25            # around the subnormal spacing 2^-24
+    x = np.concatenate([x, mids, -mids, sub, -sub])
+    x = x[np.abs(x) < 65504.0]
+    assert np.array_equal(O.round_to(x, "f16"), _nearest_f16_brute_force(x))
+    x32 = (rng.standard_normal(20000) * 10.0 ** rng.integers(-6, 4, 20000)).astype(np.float32)
+    x32 = x32[np.abs(x32) < 65504.0]
+    ref = torch.from_numpy(x32).to(torch.float16).to(torch.float64).numpy()
+    assert np.array_equal(O.round_to(x32.astype(np.float64), "f16"), ref)
+
+
+def test_empty_denominator_row_contributes_nothing():
+    """A row whose label is outside the shard and whose every logit the PFC*
+    filter drops has an empty denominator (reading of Eq. noise_filtering):
+    lse = -inf, probability 0 everywhere, no gradient, loss term 0.  Pinned
+    against the same batch without that row (same batch size in the mean):
+    every other row's lse, dx and every class gradient are unchanged."""
+    rng = np.random.default_rng(25)
+    B, d, K, tau, s, m = 6, 12, 9, 0.3, 32.0, 0.5
+    u = rng.standard_normal(d)
+    u /= np.linalg.norm(u)
+    Ws = rng.standard_normal((K, d)) + 6.0 * u           # every centre leans along u
+    X = rng.standard_normal((B, d))
+    y = rng.integers(0, K, size=B)
+    X[2] = 4.0 * u + 0.05 * rng.standard_normal(d)
+    y[2] = -1                                           # label outside the shard
+    for margin in (O.COSFACE, O.ARCFACE):
+        fw = O.forward(X, Ws, y, s, m, margin, tau)
+        assert np.all(fw["cos"][2] > tau)               # every logit of row 2 is dropped
+        assert fw["lse"][2] == -np.inf and np.all(fw["P"][2] == 0.0)
+        assert fw["row_loss"][2] == 0.0
+        dx = O.grad_x(X, Ws, y, fw["lse"], B, s, m, margin, tau)
+        g = O.grad_w(X, Ws, np.arange(K), y, fw["lse"], B, s, m, margin, tau)
+        assert np.all(np.isfinite(dx)) and np.all(np.isfinite(g))
+        assert np.all(dx[2] == 0.0)
+        keep = np.array([n for n in range(B) if n != 2])
+        fk = O.forward(X[keep], Ws, y[keep], s, m, margin, tau)
+        assert np.array_equal(fw["lse"][keep], fk["lse"])
+        assert O.batch_loss(fw["row_loss"], B) == O.batch_loss(fk["row_loss"], B)
+        assert np.allclose(dx[keep], O.grad_x(X[keep], Ws, y[keep], fk["lse"], B, s, m, margin,
+                                              tau), rtol=1e-13, atol=1e-15)
+        assert np.allclose(g, O.grad_w(X[keep], Ws, np.arange(K), y[keep], fk["lse"], B, s, m,
+                                       margin, tau), rtol=1e-13, atol=1e-15)
