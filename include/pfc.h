@@ -42,7 +42,8 @@ typedef enum {
   PFC_ERR_CAPACITY = 2,     /* active_cap smaller than the largest possible |S| */
   PFC_ERR_WORKSPACE = 3,    /* ws is NULL or smaller than required */
   PFC_ERR_UNSUPPORTED = 4,  /* dtype combination not implemented */
-  PFC_ERR_HIP = 5           /* a HIP launch failed */
+  PFC_ERR_HIP = 5,          /* a HIP launch failed */
+  PFC_ERR_SCRATCH = 6       /* larger than the static scratch of pfc_sample_noalloc */
 } pfc_status;
 
 typedef enum { PFC_F32 = 0, PFC_BF16 = 1, PFC_F16 = 2 } pfc_dtype;
@@ -103,6 +104,28 @@ int pfc_sample(const int64_t* labels, int64_t B, int64_t C,
                int64_t class_offset, double r, uint64_t seed, int32_t* active,
                int64_t active_cap, int32_t* n_active, int32_t* labels_mapped,
                void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * pfc_sample without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Same arguments, outputs and selection rule as
+ * pfc_sample, minus ws / ws_bytes: the sampler's scratch is a file-scope
+ * device array of the library, about 30 MiB on every device the library runs
+ * on, held until the process ends.  Its address is looked up on the first
+ * call on each device (that call must run with the device current).
+ *
+ * C above PFC_NOALLOC_MAX_CLASSES is PFC_ERR_SCRATCH (checked before any
+ * launch; use pfc_sample with a workspace instead).  The call allocates
+ * nothing and enqueues the same kernels as pfc_sample; the scratch keeps the
+ * last call's contents and every call clears what must start at zero.  All
+ * calls on one device share the one scratch: calls that overlap on a device
+ * (concurrent streams, or host threads) race and give undefined results.
+ */
+#define PFC_NOALLOC_MAX_CLASSES (1LL << 21)
+int pfc_sample_noalloc(const int64_t* labels, int64_t B, int64_t C,
+                       int64_t class_offset, double r, uint64_t seed,
+                       int32_t* active, int64_t active_cap, int32_t* n_active,
+                       int32_t* labels_mapped, void* stream);
 
 /*
  * Stages 3-5: normalise the rows of X and the active rows of W, the cosine

@@ -19,21 +19,6 @@ int ceil_log2(int64_t x) {
   return b;
 }
 
-// Activation budget of a shard (Eq. local_sampling): r*C when it is an
-// integer within 1e-9 relative, else ceil(r*C).
-int64_t budget_of(double r, int64_t C) {
-  const double t = r * (double)C;
-  const double rt = nearbyint(t);
-  if (fabs(t - rt) <= 1e-9 * fmax(1.0, t)) return (int64_t)rt;
-  return (int64_t)ceil(t);
-}
-
-int64_t cap_of(int64_t B, int64_t C, double r) {
-  const int64_t b = budget_of(r, C);
-  const int64_t p = B < C ? B : C;
-  return b > p ? b : p;
-}
-
 bool dtype_ok(int t) { return t == PFC_F32 || t == PFC_BF16 || t == PFC_F16; }
 
 bool finite_pos(double v) { return isfinite(v) && v > 0.0; }
@@ -59,6 +44,21 @@ int check_hparams(float s, float m, int margin) {
 }
 
 }  // namespace
+
+// Activation budget of a shard (Eq. local_sampling): r*C when it is an
+// integer within 1e-9 relative, else ceil(r*C).
+int64_t budget_of(double r, int64_t C) {
+  const double t = r * (double)C;
+  const double rt = nearbyint(t);
+  if (fabs(t - rt) <= 1e-9 * fmax(1.0, t)) return (int64_t)rt;
+  return (int64_t)ceil(t);
+}
+
+int64_t cap_of(int64_t B, int64_t C, double r) {
+  const int64_t b = budget_of(r, C);
+  const int64_t p = B < C ? B : C;
+  return b > p ? b : p;
+}
 
 WsLayout ws_layout(int64_t B, int64_t d, int64_t C, int64_t cap, int compute) {
   WsLayout L{};
@@ -286,6 +286,7 @@ const char* pfc_status_string(int status) {
     case PFC_ERR_WORKSPACE: return "workspace missing or too small";
     case PFC_ERR_UNSUPPORTED: return "unsupported dtype or shape";
     case PFC_ERR_HIP: return "HIP launch failed";
+    case PFC_ERR_SCRATCH: return "problem larger than the static scratch of the no-allocation entry point";
     default: return "unknown status";
   }
 }

@@ -93,6 +93,10 @@ struct WsLayout {
   int top_bits;
 };
 
+// Activation budget b of a shard and the capacity max(b, min(B, C)) of S.
+int64_t budget_of(double r, int64_t C);
+int64_t cap_of(int64_t B, int64_t C, double r);
+
 WsLayout ws_layout(int64_t B, int64_t d, int64_t C, int64_t cap, int compute);
 SampleWs sample_ws(void* ws, const WsLayout& L);
 StepWs step_ws(void* ws, const WsLayout& L);

@@ -19,10 +19,12 @@ PFC_ERR_CAPACITY = 2
 PFC_ERR_WORKSPACE = 3
 PFC_ERR_UNSUPPORTED = 4
 PFC_ERR_HIP = 5
+PFC_ERR_SCRATCH = 6
 
 PFC_F32, PFC_BF16, PFC_F16 = 0, 1, 2
 PFC_MAX_BATCH = 8192
 PFC_MAX_CLASSES = 1 << 30
+PFC_NOALLOC_MAX_CLASSES = 1 << 21
 PFC_COSFACE, PFC_ARCFACE = 0, 1
 
 PFC_K_SAMPLE, PFC_K_PREP, PFC_K_FWD_GEMM, PFC_K_LSE = 0, 1, 2, 3
@@ -31,7 +33,7 @@ KERNEL_NAMES = {PFC_K_SAMPLE: "sample", PFC_K_PREP: "prep", PFC_K_FWD_GEMM: "fwd
                 PFC_K_LSE: "lse", PFC_K_DX_GEMM: "dx_gemm", PFC_K_DX_FINAL: "dx_final",
                 PFC_K_DW_UPDATE: "dw_update"}
 
-EXPORTS = ("pfc_workspace_bytes", "pfc_sample", "pfc_forward_loss",
+EXPORTS = ("pfc_workspace_bytes", "pfc_sample", "pfc_sample_noalloc", "pfc_forward_loss",
            "pfc_backward_update", "pfc_status_string", "pfc_timing_begin", "pfc_timing_end",
            "pfc_bank_stage", "pfc_bank_patch", "pfc_bank_writeback")
 
@@ -49,6 +51,8 @@ _lib.pfc_workspace_bytes.argtypes = [_i64, _i64, _i64, _dbl, _int,
 _lib.pfc_workspace_bytes.restype = _int
 _lib.pfc_sample.argtypes = [_vp, _i64, _i64, _i64, _dbl, _u64, _vp, _i64, _vp, _vp, _vp, _sz, _vp]
 _lib.pfc_sample.restype = _int
+_lib.pfc_sample_noalloc.argtypes = [_vp, _i64, _i64, _i64, _dbl, _u64, _vp, _i64, _vp, _vp, _vp]
+_lib.pfc_sample_noalloc.restype = _int
 _lib.pfc_forward_loss.argtypes = [_vp, _int, _i64, _i64, _vp, _int, _i64, _vp, _vp, _i64, _vp,
                                   _int, _flt, _flt, _int, _flt, _vp, _vp, _vp, _sz, _vp]
 _lib.pfc_forward_loss.restype = _int
@@ -99,6 +103,12 @@ def pfc_sample(labels, B, C, class_offset, r, seed, active, active_cap, n_active
                labels_mapped, ws, ws_bytes, stream):
     _check(_lib.pfc_sample(labels, B, C, class_offset, r, seed, active, active_cap, n_active,
                            labels_mapped, ws, ws_bytes, stream), "pfc_sample")
+
+
+def pfc_sample_noalloc(labels, B, C, class_offset, r, seed, active, active_cap, n_active,
+                       labels_mapped, stream):
+    _check(_lib.pfc_sample_noalloc(labels, B, C, class_offset, r, seed, active, active_cap,
+                                   n_active, labels_mapped, stream), "pfc_sample_noalloc")
 
 
 def pfc_forward_loss(X, x_dtype, B, d, W, w_dtype, C, active, n_active, active_cap,

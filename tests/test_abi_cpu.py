@@ -35,7 +35,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_status_strings():
-    for st in range(6):
+    for st in range(7):
         assert pfc.pfc_status_string(st) not in ("", "unknown status")
     assert pfc.pfc_status_string(99) == "unknown status"
 
@@ -225,4 +225,39 @@ def test_no_device_reports_hip_error():
     """With no HIP device the launch fails and the ABI reports PFC_ERR_HIP."""
     with pytest.raises(pfc.PfcError) as e:
         pfc.pfc_sample(**_sample_args())
+    assert e.value.status == pfc.PFC_ERR_HIP
+
+
+def _noalloc_args(**kw):
+    a = dict(labels=FAKE, B=16, C=1000, class_offset=0, r=0.1, seed=0, active=FAKE,
+             active_cap=100, n_active=FAKE, labels_mapped=FAKE, stream=0)
+    a.update(kw)
+    return a
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(labels=0), pfc.PFC_ERR_INVALID_ARG),
+    (dict(n_active=0), pfc.PFC_ERR_INVALID_ARG),
+    (dict(B=0), pfc.PFC_ERR_INVALID_ARG),
+    (dict(B=8193, active_cap=8193, C=100000), pfc.PFC_ERR_INVALID_ARG),
+    (dict(r=1.5), pfc.PFC_ERR_INVALID_ARG),
+    (dict(active_cap=99), pfc.PFC_ERR_CAPACITY),
+    (dict(C=(1 << 21) + 1, active_cap=1 << 21), pfc.PFC_ERR_SCRATCH),   # beyond the static scratch
+])
+def test_sample_noalloc_rejects_before_launch(kw, status):
+    with pytest.raises(pfc.PfcError) as e:
+        pfc.pfc_sample_noalloc(**_noalloc_args(**kw))
+    assert e.value.status == status
+
+
+def test_noalloc_limit_matches_header():
+    text = open(HEADER).read()
+    assert "(1LL << 21)" in re.search(r"#define PFC_NOALLOC_MAX_CLASSES (.*)", text).group(1)
+    assert pfc.PFC_NOALLOC_MAX_CLASSES == 1 << 21
+
+
+@pytest.mark.skipif(torch.cuda.device_count() > 0, reason="only meaningful without a GPU")
+def test_noalloc_without_device_reports_hip_error():
+    with pytest.raises(pfc.PfcError) as e:
+        pfc.pfc_sample_noalloc(**_noalloc_args())
     assert e.value.status == pfc.PFC_ERR_HIP
