@@ -12,7 +12,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(PKG, "libpfc.so")
 
-SOURCES = ["abi.hip", "sample.hip", "sample_noalloc.hip", "prep.hip", "fwd.hip", "fwdx.hip", "bwd.hip",
+SOURCES = ["abi.hip", "sample.hip", "sample_noalloc.hip", "prep.hip", "fwd.hip", "bwd.hip",
            "timing.hip", "bank.hip"]
 ARCH = "gfx950"
 

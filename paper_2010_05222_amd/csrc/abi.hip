@@ -84,26 +84,29 @@ WsLayout ws_layout(int64_t B, int64_t d, int64_t C, int64_t cap, int compute) {
   L.sample_bytes = off;
 
   L.ld_cos = round_up(cap, 256);
+  L.n_ctiles = ceil_div(cap, kFwdClassTile);
   L.ld_xt = round_up(B, 32);
   L.ld_g = round_up(B, 128);
   L.n_lgroups = L.ld_cos / kLogitGroup;
   if (compute == PFC_F32) {
     L.n_split = 1;
   } else {
-    // Class slices of the fused forward: ~256 workgroups of 64 batch rows,
-    // one per CU; a slice is a whole number of 128-class groups.
-    const int64_t n_rt = ceil_div(B, kFwdRows);
-    const int64_t groups = ceil_div(cap, kLogitGroup);
+    // Split-K of the feature-gradient contraction: ~256 workgroups of
+    // 128 batch rows, one per CU.
+    const int64_t n_rt = ceil_div(B, 128);
+    const int64_t chunks = ceil_div(cap, 32);
     int64_t ns = ceil_div(256, n_rt);
-    ns = ns > groups ? groups : ns;
+    ns = ns > chunks ? chunks : ns;
     L.n_split = (int)(ns < 1 ? 1 : ns);
   }
   const size_t cos_elt = compute == PFC_F32 ? 4 : 2;
   L.off_inv_x = take((size_t)B * 4);
   L.off_xb = take(compute == PFC_F32 ? 0 : (size_t)L.ld_xt * d * 2);
+  L.off_xblk = take(compute == PFC_F32 ? 0 : (size_t)L.ld_xt * d * 2);
+  L.off_wmax = take(4);
   L.off_inv_w = take((size_t)L.ld_cos * 4);
   L.off_cos = take((size_t)B * L.ld_cos * cos_elt);
-  L.off_stats = take((size_t)B * L.n_split * 8);
+  L.off_stats = take((size_t)B * L.n_ctiles * 8);
   L.off_tgt = take((size_t)B * 4);
   L.off_dx = take((size_t)L.n_split * B * d * 4);
   L.off_loss = take((size_t)B * 4);
@@ -137,11 +140,14 @@ StepWs step_ws(void* ws, const WsLayout& L) {
   StepWs w;
   w.inv_x = (float*)(b + L.off_inv_x);
   w.xbT = b + L.off_xb;
+  w.xblk = b + L.off_xblk;
   w.ld_xt = L.ld_xt;
+  w.inv_w_max = (float*)(b + L.off_wmax);
   w.inv_w = (float*)(b + L.off_inv_w);
   w.lbuf = b + L.off_cos;
   w.ld_cos = L.ld_cos;
   w.stats = (float2*)(b + L.off_stats);
+  w.n_ctiles = L.n_ctiles;
   w.tgt = (float*)(b + L.off_tgt);
   w.dx_part = (float*)(b + L.off_dx);
   w.n_split = L.n_split;

@@ -11,37 +11,49 @@
 // single target term of each row, (p_t - 1) * slope_t, is added exactly in
 // fp32 outside the MFMA loops.
 //
-// dX: the contraction over classes, dX_hat = sum_j p_nj W[S_j] / ||w_j||,
-//   runs inside the fused forward kernel, against a running per-row reference
-//   m per class slice (fwdx.hip).  k_dx_final scales each slice's partial by
-//   2^(m - lse log2 e) (lse as given to the backward), sums the slices in a
-//   fixed order, adds the exact target terms and applies the normalisation
-//   backward of x.
+// dX (k_dx16): split-K MFMA contraction over classes, dX_hat^T[i][n] =
+//   sum_j W[S_j][i] * p_{nj} / ||w_j||.  A workgroup owns 128 batch rows x all
+//   of d and a slice of the classes.  The gathered W rows go straight from
+//   HBM into a three-stage LDS ring (direct-to-LDS loads) and are read as MFMA
+//   operands with transposing LDS reads, so they are never staged in
+//   registers.  k_dx_final sums the split partials in a fixed order, adds the
+//   target terms and applies the normalisation backward of x.
 // dW + update (k_dw16): a workgroup (eight waves, two per SIMD) owns 128
 //   active classes x all of d and reduces over the whole batch, so its
 //   epilogue has complete rows: target terms, tangent projection, momentum,
 //   weight step and the scatter into the persistent W / momentum rows (unique
-//   rows, no atomics).  It runs after the forward, which read the old W.
+//   rows, no atomics).  It runs after the dX kernels, which read the old W.
 #include "pfc_gemm.h"
 
 namespace pfc {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kBwKC = 32;          // reduction chunk of the class-gradient contraction: batch rows
+constexpr int kBwKC = 32;          // reduction chunk: classes (dX) or batch rows (dW)
 constexpr int kRowLd = 528;        // LDS row stride of a DMA'd row of up to 512 (1 KB + 32 B)
 constexpr int kRowStage = kBwKC * kRowLd;
+constexpr int kDxRows = 128;       // batch rows of a dX workgroup
 constexpr int kDwCls = 128;        // classes of a dW workgroup
 constexpr int kTLd = 260;         // LDS row stride (floats) of the update's staged gradient rows
 constexpr int kHitCap = 256;      // target rows listed per wave of a dW workgroup
 constexpr int kDwStaggerCUs = 256;  // CU count of the part the dW start offset was tuned on
 
-// Every operand of the class-gradient contraction reaches LDS through
-// direct-to-LDS loads into three-stage rings (one array per stage, so the
-// compiler can keep later stages in flight while a stage is read); the
-// coefficient producer reads the raw logit-store values from LDS and writes
-// the 16-bit MFMA operand back to LDS.
+// Every operand reaches LDS through direct-to-LDS loads into three-stage
+// rings (one array per stage, so the compiler can keep later stages in
+// flight while a stage is read); the coefficient producer reads the raw
+// logit-store values from LDS and writes the 16-bit MFMA operand back to LDS.
 //
+// dX: W rows, raw logit-store values [128 rows x 32 classes], 1/||w|| of the
+// chunk, the rows' scales, and the coefficient tile (K-major, 64-byte rows).
+__shared__ __attribute__((aligned(1024))) uint16_t xW0[kRowStage], xW1[kRowStage], xW2[kRowStage];
+__shared__ __attribute__((aligned(1024))) int16_t xR0[kDxRows * kBwKC], xR1[kDxRows * kBwKC],
+    xR2[kDxRows * kBwKC];
+__shared__ __attribute__((aligned(16))) float xI0[kBwKC], xI1[kBwKC], xI2[kBwKC];
+__shared__ __attribute__((aligned(16))) float xS0[kDxRows], xS1[kDxRows], xS2[kDxRows];
+__shared__ __attribute__((aligned(1024))) uint16_t xG0[kDxRows * kBwKC], xG1[kDxRows * kBwKC],
+    xG2[kDxRows * kBwKC];
+// dX: active row ids of four chunks (a ring: chunk c in slot c % 4).
+__shared__ __attribute__((aligned(16))) int32_t xIds[4][kBwKC];
 // dW: X^T rows (K-major: d rows of 32 batch rows, bf16), raw logit-store
 // values [32 rows x 128 classes] (16-byte pieces swizzled per row), the rows'
 // scales, and the coefficient tile G^T (K-major: 128 class rows of 32 batch
@@ -61,6 +73,11 @@ __shared__ __attribute__((aligned(1024))) uint16_t wG0[kDwCls * kBwKC], wG1[kDwC
     else if constexpr (S == 1) return a1;        \
     else return a2;                              \
   }
+PFC_STAGE3(dx_w, uint16_t, xW0, xW1, xW2)
+PFC_STAGE3(dx_r, int16_t, xR0, xR1, xR2)
+PFC_STAGE3(dx_i, float, xI0, xI1, xI2)
+PFC_STAGE3(dx_s, float, xS0, xS1, xS2)
+PFC_STAGE3(dx_g, uint16_t, xG0, xG1, xG2)
 PFC_STAGE3(dw_x, uint16_t, wX0, wX1, wX2)
 PFC_STAGE3(dw_r, int16_t, wR0, wR1, wR2)
 PFC_STAGE3(dw_q, float, wQ0, wQ1, wQ2)
@@ -77,6 +94,13 @@ __device__ __forceinline__ float target_coef(const Margin& mg, float c, float ls
   const float p = __expf(target_logit(mg, c) - lse);
   return (p - 1.0f) * target_slope(mg, c);
 }
+
+// Scale of the fp16 coefficient operand of dX: a power of two that keeps
+// p / ||w_j|| * scale inside the fp16 range for every active class (p <= 1).
+__device__ __forceinline__ float dx_operand_scale(F16Tag, float inv_w_max) {
+  return exp2f(floorf(log2f(60000.0f / fmaxf(inv_w_max, 1e-30f))));
+}
+__device__ __forceinline__ float dx_operand_scale(Bf16Tag, float) { return 1.0f; }
 
 // Two floats to a packed pair of 16-bit values, round to nearest even
 // (v_cvt_pk_bf16_f32 / v_cvt_f16_f32 on gfx950).
@@ -105,20 +129,316 @@ __device__ __forceinline__ uint4 pack8(const float (&v)[8]) {
   return o;
 }
 
+// An MFMA operand from the two halves of a transposing read pair.
+__device__ __forceinline__ uint4 frag_of(const u32x2_t& lo, const u32x2_t& hi) {
+  return make_uint4(lo.x, lo.y, hi.x, hi.y);
+}
+__device__ __forceinline__ uint4 as_uint4(const u32x4_t& v) { return make_uint4(v.x, v.y, v.z, v.w); }
+
+template <typename T>
+__device__ __forceinline__ void zero_acc(T (&acc)[4][2]) {
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.0f;
+}
+
+// ------------------------------------------------------------------ dX
+
+// D = 128 * WI; 2 * WI waves: wave (wi, wn) owns d entries [128 wi, +128) and
+// batch rows [64 wn, +64) of the workgroup's 128 (4 x 2 MFMA blocks).
+// Pipeline per chunk c (32 classes): the raw cosines and 1/||w|| of chunk
+// c + 3 and the W rows of chunk c + 2 are requested, the coefficients of
+// chunk c + 1 are produced, and chunk c is contracted.
+template <typename Tag, int WI>
+__global__ void __launch_bounds__(128 * WI) k_dx16(
+    const uint16_t* __restrict__ W, const int32_t* __restrict__ act_pad,
+    const int32_t* __restrict__ n_active_p, const float* __restrict__ inv_w,
+    const float* __restrict__ inv_w_max, const uint16_t* __restrict__ lbuf, int64_t ld_cos,
+    const float* __restrict__ gscale, int64_t ld_g, int B, int n_rt, int n_split,
+    int64_t n_tiles, int64_t per_xcd, float* __restrict__ dx_part) {
+  constexpr int D = 128 * WI;
+  constexpr int NT = 128 * WI;              // threads
+  constexpr int NW = 2 * WI;                // waves
+  constexpr int WROWS = kBwKC / NW;         // W rows DMA'd by each wave per chunk
+  constexpr int RDMA = 8 / NW;              // 1-KB logit-store blocks DMA'd by each wave
+  constexpr int GROUPS = 512 / NT;          // 8-coefficient groups per thread per chunk
+  constexpr int PER_ITER = WROWS + RDMA + 3;  // DMAs a wave issues per chunk
+  const int64_t t = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  if (t >= n_tiles) return;
+  // The batch-row tiles of one split share its class range: they run on one
+  // XCD so the split's W rows are fetched from HBM once.
+  const int split = (int)(t / n_rt);
+  const int n0 = (int)(t % n_rt) * kDxRows;
+  const int K = *n_active_p;
+  const int64_t n_chunks = ceil_div((int64_t)K, (int64_t)kBwKC);
+  const int64_t per = ceil_div(n_chunks, (int64_t)n_split);
+  const int64_t c_begin = split * per;
+  const int64_t c_end = c_begin + per < n_chunks ? c_begin + per : n_chunks;
+  const int64_t c_stop =
+      c_begin + ceil_div(c_end > c_begin ? c_end - c_begin : 0, (int64_t)3) * 3;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wi = wave >> 1, wn = wave & 1;
+  const float scale = dx_operand_scale(Tag{}, *inv_w_max);
+
+  // Coefficient-producer slots of this thread (fixed for the whole kernel):
+  // row prow, classes 8 pchunk .. + 7 of each chunk.
+  int prow[GROUPS], pchunk[GROUPS];
+#pragma unroll
+  for (int u = 0; u < GROUPS; ++u) {
+    const int q = tid + NT * u;
+    prow[u] = q >> 2;
+    pchunk[u] = q & 3;
+  }
+  // Logit-store DMA of this lane: block b holds rows 16 b .. 16 b + 15.
+  int64_t rsrc[RDMA];
+#pragma unroll
+  for (int v = 0; v < RDMA; ++v) {
+    const int r = 16 * (wave * RDMA + v) + (lane >> 2);
+    const int n = n0 + r < B ? n0 + r : B - 1;
+    rsrc[v] = (int64_t)n * ld_cos + 8 * (lane & 3);
+  }
+
+  auto dma_raw = [&](auto st, int64_t c) {
+    constexpr int S = decltype(st)::value;
+    const int64_t jb = (c < n_chunks ? c : n_chunks - 1) * kBwKC;
+#pragma unroll
+    for (int v = 0; v < RDMA; ++v)
+      dma16(lbuf + rsrc[v] + jb, dx_r<S>() + 512 * (wave * RDMA + v));
+    // 1/||w|| of the chunk's 32 classes: 8 / NW 16-byte pieces per wave.
+    if (lane < 8 / NW) dma16(inv_w + jb + 4 * (wave * (8 / NW) + lane), dx_i<S>() + 4 * wave * (8 / NW));
+    // Row scales of the chunk's 128-class group for the 128 rows: 32 / NW pieces per wave.
+    const float* gs = gscale + (jb / kLogitGroup) * ld_g + n0;
+    if (lane < 32 / NW) dma16(gs + 4 * (wave * (32 / NW) + lane), dx_s<S>() + 4 * wave * (32 / NW));
+  };
+  // Active-set indices of the W rows this wave DMAs for a chunk.  The first
+  // two chunks' come from scalar loads; later chunks' travel with the loads,
+  // four chunks ahead, into the index ring (their wait is then the chunk's
+  // load wait, not a scalar-load round trip inside the loop).  The padded copy
+  // holds a valid row id at every index of a chunk.
+  int32_t rows_pf[WROWS];
+  auto load_rows = [&](int64_t c) {
+    const int64_t jb = (c < n_chunks ? c : n_chunks - 1) * kBwKC;
+#pragma unroll
+    for (int v = 0; v < WROWS; ++v)
+      rows_pf[v] = act_pad[__builtin_amdgcn_readfirstlane((int)(jb + wave * WROWS + v))];
+  };
+  auto dma_ids = [&](int64_t c) {
+    const int64_t jb = (c < n_chunks ? c : n_chunks - 1) * kBwKC;
+    if (lane < WROWS / 4) dma16(act_pad + jb + wave * WROWS + 4 * lane, &xIds[c & 3][wave * WROWS]);
+  };
+  auto read_ids = [&](int64_t c, u32x4_t (&iv)[WROWS / 4]) {
+#pragma unroll
+    for (int q = 0; q < WROWS / 4; ++q)
+      ds_read_128<0>(iv[q], lds_addr(&xIds[c & 3][wave * WROWS + 4 * q]));
+  };
+  auto rows_of = [&](u32x4_t (&iv)[WROWS / 4]) {
+#pragma unroll
+    for (int q = 0; q < WROWS / 4; ++q) {
+      rows_pf[4 * q + 0] = __builtin_amdgcn_readfirstlane((int)iv[q].x);
+      rows_pf[4 * q + 1] = __builtin_amdgcn_readfirstlane((int)iv[q].y);
+      rows_pf[4 * q + 2] = __builtin_amdgcn_readfirstlane((int)iv[q].z);
+      rows_pf[4 * q + 3] = __builtin_amdgcn_readfirstlane((int)iv[q].w);
+    }
+  };
+  auto dma_w = [&](auto st) {
+    constexpr int S = decltype(st)::value;
+#pragma unroll
+    for (int v = 0; v < WROWS; ++v) {
+      const int r = wave * WROWS + v;
+      if (lane < D / 8) dma16(W + (int64_t)rows_pf[v] * D + 8 * lane, dx_w<S>() + r * kRowLd);
+    }
+  };
+  // Coefficients of chunk c (K-major, rows of 32 classes): the LDS reads are
+  // issued first (produce_load) and consumed later (produce_store), after an
+  // lgkm wait that covers them.
+  // Coefficient of (row, class): p / ||w_j|| * scale = E * gscale_row * scale * (1/||w_j||);
+  // E is 0 at the row's target and past |S|, gscale 0 past the batch, so only
+  // chunks past the split's end need masking.
+  struct ProdIn {
+    u32x4_t qv[GROUPS], i0v[GROUPS], i1v[GROUPS];
+    uint32_t sv[GROUPS];
+  };
+  auto produce_load = [&](auto st, ProdIn& in) {
+    constexpr int S = decltype(st)::value;
+#pragma unroll
+    for (int u = 0; u < GROUPS; ++u) {
+      ds_read_128<0>(in.qv[u], lds_addr(dx_r<S>()) + (prow[u] * kBwKC + 8 * pchunk[u]) * 2);
+      ds_read_128<0>(in.i0v[u], lds_addr(dx_i<S>()) + 32 * pchunk[u]);
+      ds_read_128<16>(in.i1v[u], lds_addr(dx_i<S>()) + 32 * pchunk[u]);
+      ds_read_32<0>(in.sv[u], lds_addr(dx_s<S>()) + 4 * prow[u]);
+    }
+  };
+  auto produce_store = [&](auto st, int64_t c, ProdIn& in) {
+    constexpr int S = decltype(st)::value;
+    const bool cvalid = c < c_end;   // wave-uniform
+#pragma unroll
+    for (int u = 0; u < GROUPS; ++u) {
+      pin_reg(in.qv[u]);
+      pin_reg(in.i0v[u]);
+      pin_reg(in.i1v[u]);
+      pin_reg(in.sv[u]);
+      const uint4 q = as_uint4(in.qv[u]);
+      const uint32_t qw[4] = {q.x, q.y, q.z, q.w};
+      const float iw[8] = {__uint_as_float(in.i0v[u].x), __uint_as_float(in.i0v[u].y),
+                           __uint_as_float(in.i0v[u].z), __uint_as_float(in.i0v[u].w),
+                           __uint_as_float(in.i1v[u].x), __uint_as_float(in.i1v[u].y),
+                           __uint_as_float(in.i1v[u].z), __uint_as_float(in.i1v[u].w)};
+      const float sc = cvalid ? __uint_as_float(in.sv[u]) * scale : 0.0f;
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float ev = (e & 1) ? f16_hi(qw[e >> 1]) : f16_lo(qw[e >> 1]);
+        v[e] = ev * (sc * iw[e]);
+      }
+      const uint4 o = pack8<Tag>(v);
+      ds_write_128<0>(lds_addr(dx_g<S>()) + k_major32_offset(prow[u], pchunk[u]) * 2,
+                      u32x4_t{o.x, o.y, o.z, o.w});
+    }
+  };
+
+  // Per-lane byte offsets of the fragment reads (see frag_mn_major and
+  // frag_k_major32): W rows MN-major, coefficients K-major.
+  const int fg = lane >> 4, fsrc = lane & 15;
+  const uint32_t a_lane =
+      ((8 * (fg >> 1) + (fsrc >> 2)) * kRowLd + 16 * (fg & 1) + 4 * (fsrc & 3) + 128 * wi) * 2;
+  const uint32_t b_lane0 = k_major32_offset(64 * wn + (lane & 31), lane >> 5) * 2;
+  const uint32_t b_lane1 = k_major32_offset(64 * wn + (lane & 31), 2 + (lane >> 5)) * 2;
+
+  f32x16_t acc[4][2];
+  zero_acc(acc);
+
+  if (c_begin < c_stop) {
+    using S0 = std::integral_constant<int, 0>;
+    using S1 = std::integral_constant<int, 1>;
+    using S2 = std::integral_constant<int, 2>;
+    // Prologue: raw data of chunks 0..2, W rows of chunks 0, 1; coefficients of chunk 0.
+    load_rows(c_begin);
+    dma_raw(S0{}, c_begin);
+    dma_w(S0{});
+    load_rows(c_begin + 1);
+    dma_raw(S1{}, c_begin + 1);
+    dma_ids(c_begin + 2);
+    dma_ids(c_begin + 3);
+    dma_w(S1{});
+    dma_raw(S2{}, c_begin + 2);
+    wait_vmcnt_lgkm0<2 * (RDMA + 1) + WROWS + 2>();
+    stage_barrier();
+    ProdIn in0;
+    produce_load(S0{}, in0);
+    lgkm_wait<0>();
+    produce_store(S0{}, c_begin, in0);
+    for (int64_t c = c_begin; c < c_stop; c += 3) {
+      static_for<0, 3>([&](auto uu) {
+        constexpr int u = decltype(uu)::value;
+        const int64_t cu = c + u;
+        // Landed: W rows of chunk cu, raw data of chunk cu + 1; this wave's
+        // coefficient writes of the previous iteration are complete.
+        wait_vmcnt_lgkm0<PER_ITER>();
+        stage_barrier();
+        // The row ids of chunk cu + 2 (landed: requested before the W rows of
+        // chunk cu) and the producer's reads of chunk cu + 1 go first
+        // (consumed while the first k-step's MFMAs run), then the fragments of
+        // chunk cu...
+        u32x4_t idv[WROWS / 4];
+        read_ids(cu + 2, idv);
+        ProdIn pin;
+        produce_load(std::integral_constant<int, (u + 1) % 3>{}, pin);
+        const uint32_t wb = lds_addr(dx_w<u>()) + a_lane;
+        const uint32_t gb0 = lds_addr(dx_g<u>()) + b_lane0;
+        const uint32_t gb1 = lds_addr(dx_g<u>()) + b_lane1;
+        u32x2_t alo[2][4], ahi[2][4];
+        u32x4_t bq[2][2];
+        static_for<0, 4>([&](auto mm) {
+          constexpr int mb = decltype(mm)::value;
+          ds_read_tr_b64<(0 * kRowLd + 32 * mb) * 2>(alo[0][mb], wb);
+          ds_read_tr_b64<(4 * kRowLd + 32 * mb) * 2>(ahi[0][mb], wb);
+        });
+        ds_read_128<0>(bq[0][0], gb0);
+        ds_read_128<32 * 64>(bq[0][1], gb0);
+        static_for<0, 4>([&](auto mm) {
+          constexpr int mb = decltype(mm)::value;
+          ds_read_tr_b64<(16 * kRowLd + 32 * mb) * 2>(alo[1][mb], wb);
+          ds_read_tr_b64<(20 * kRowLd + 32 * mb) * 2>(ahi[1][mb], wb);
+        });
+        ds_read_128<0>(bq[1][0], gb1);
+        ds_read_128<32 * 64>(bq[1][1], gb1);
+        // ... then later chunks' loads; the next coefficients are produced
+        // while the first k-step's MFMAs run.
+        dma_raw(std::integral_constant<int, u>{}, cu + 3);
+        dma_ids(cu + 4);
+        static_for<0, 2>([&](auto kq) {
+          constexpr int kk = decltype(kq)::value;
+          if constexpr (kk == 0) {
+            lgkm_wait<10>(alo[0][0], alo[0][1], alo[0][2], alo[0][3], ahi[0][0], ahi[0][1],
+                          ahi[0][2], ahi[0][3], bq[0][0], bq[0][1], idv);
+            // W rows of chunk cu + 2, from the ids read above.
+            rows_of(idv);
+            dma_w(std::integral_constant<int, (u + 2) % 3>{});
+          } else {
+            produce_store(std::integral_constant<int, (u + 1) % 3>{}, cu + 1, pin);
+            lgkm_wait<0>(alo[1][0], alo[1][1], alo[1][2], alo[1][3], ahi[1][0], ahi[1][1],
+                         ahi[1][2], ahi[1][3], bq[1][0], bq[1][1]);
+          }
+#pragma unroll
+          for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+            for (int nb = 0; nb < 2; ++nb)
+              acc[mb][nb] = mfma_32x32x16(frag_of(alo[kk][mb], ahi[kk][mb]), as_uint4(bq[kk][nb]),
+                                          acc[mb][nb], Tag{});
+        });
+      });
+    }
+    wait_vmcnt<0>();
+  }
+
+  const float inv_scale = 1.0f / scale;
+  const int half = lane >> 5, l32 = lane & 31;
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb) {
+    const int n = n0 + 64 * wn + 32 * nb + l32;
+    if (n >= B) continue;
+    float* out = dx_part + ((int64_t)split * B + n) * D;
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int i = 128 * wi + 32 * mb + 8 * g + 4 * half;
+        *reinterpret_cast<float4*>(out + i) =
+            make_float4(acc[mb][nb][4 * g] * inv_scale, acc[mb][nb][4 * g + 1] * inv_scale,
+                        acc[mb][nb][4 * g + 2] * inv_scale, acc[mb][nb][4 * g + 3] * inv_scale);
+      }
+  }
+}
+
 // Row scales of the logit store: gscale[g][n] = 2^(m_gn - lse_n log2 e), so that
 // E * gscale is the softmax probability (0 for rows past the batch).  A row
 // with an empty denominator (lse = -inf: its label is outside the shard and the
 // PFC* filter dropped every logit, so all its E are 0) gets scale 0, and with
 // it no gradient.  Groups past |S| are never read and are skipped.
+// Also writes the padded copy of the active row ids that the dX kernel reads
+// a chunk at a time: act_pad[j] = active[min(j, |S| - 1)] (0 if S is empty).
 __global__ void __launch_bounds__(256) k_scales(const float* __restrict__ gmax,
                                                 const float* __restrict__ row_lse, int B,
                                                 int64_t ld_g, int64_t n_groups,
                                                 const int32_t* __restrict__ n_active_p,
-                                                float* __restrict__ gscale) {
-  // Four consecutive entries per thread (ld_g is a multiple of 4, so the four
-  // rows share one group and the 16-byte accesses are aligned).
+                                                float* __restrict__ gscale,
+                                                const int32_t* __restrict__ active,
+                                                int32_t* __restrict__ act_pad, int64_t n_pad) {
+  // Four consecutive entries per thread (ld_g and n_pad are multiples of 4,
+  // so the four rows share one group and the 16-byte accesses are aligned).
   const int64_t i = 4 * ((int64_t)blockIdx.x * blockDim.x + threadIdx.x);
   const int64_t K = *n_active_p;
+  if (i < n_pad) {
+    int o[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = K > 0 ? active[i + e < K ? i + e : K - 1] : 0;
+    *reinterpret_cast<int4*>(act_pad + i) = make_int4(o[0], o[1], o[2], o[3]);
+  }
   if (i >= n_groups * ld_g) return;
   const int64_t g = i / ld_g;
   const int n = (int)(i - g * ld_g);
@@ -134,37 +454,27 @@ __global__ void __launch_bounds__(256) k_scales(const float* __restrict__ gmax,
   *reinterpret_cast<float4*>(gscale + i) = make_float4(v[0], v[1], v[2], v[3]);
 }
 
-// Sum the class-slice partials of a row, each scaled by 2^(m_s - lse log2 e)
-// (m_s its reference, from the forward's per-slice pairs; 0 for a slice with
-// no live logit or a row whose lse is -inf), in slice order; add the row's
-// target term g_t * W[S_t] / ||w_t||, and apply the normalisation backward:
+// Sum the split partials of a row in split order, add the row's target term
+// g_t * W[S_t] / ||w_t||, and apply the normalisation backward:
 // dx = (dX_hat - x_hat (x_hat . dX_hat)) / ||x||, dX_hat = (s/B) * sum.
 template <typename Tag>
 __global__ void __launch_bounds__(256) k_dx_final(
-    const float* __restrict__ dx_part, const float2* __restrict__ stats, int n_split,
-    const void* __restrict__ X, const void* __restrict__ W, const int32_t* __restrict__ active,
+    const float* __restrict__ dx_part, int n_split, const void* __restrict__ X,
+    const void* __restrict__ W, const int32_t* __restrict__ active,
     const int32_t* __restrict__ yhat, const float* __restrict__ row_lse,
     const float* __restrict__ inv_x, const float* __restrict__ inv_w,
     const float* __restrict__ tgtc, int B, int d, Margin mg, float sB, float* __restrict__ dX) {
   // One workgroup per batch row, thread t owns entries t and t + 256 (d <= 512):
-  // the slice partials are independent loads, summed in slice order.
-  constexpr int kMaxSplit = 256;
+  // the split partials are independent loads, summed in split order.
   __shared__ float red[4];
-  __shared__ float scl[kMaxSplit];
   const int n = blockIdx.x;
   const int t = threadIdx.x, lane = t & 63;
-  const float lse = row_lse[n];
-  for (int s = t; s < n_split; s += 256) {
-    const float m = stats[(int64_t)n * n_split + s].x;
-    scl[s] = (m > -INFINITY && lse > -INFINITY) ? __builtin_amdgcn_exp2f(m - lse * kLog2e) : 0.0f;
-  }
-  __syncthreads();
   const float ix = inv_x[n];
   const int yt = yhat[n];
   float gt = 0.0f;
   int64_t wbase = 0;
   if (yt >= 0) {
-    gt = target_coef(mg, tgtc[n], lse) * inv_w[yt];
+    gt = target_coef(mg, tgtc[n], row_lse[n]) * inv_w[yt];
     wbase = (int64_t)active[yt] * d;
   }
   float v[2] = {0.0f, 0.0f}, xh[2] = {0.0f, 0.0f};
@@ -182,9 +492,9 @@ __global__ void __launch_bounds__(256) k_dx_final(
 #pragma unroll
       for (int u = 0; u < 8; ++u) q[u] = p[(int64_t)(s + u) * stride];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) sum = fmaf(q[u], scl[s + u], sum);
+      for (int u = 0; u < 8; ++u) sum += q[u];
     }
-    for (; s < n_split; ++s) sum = fmaf(p[(int64_t)s * stride], scl[s], sum);
+    for (; s < n_split; ++s) sum += p[(int64_t)s * stride];
     if (yt >= 0) sum = fmaf(gt, load16<Tag>(W, wbase + i), sum);
     v[k] = sB * sum;
     xh[k] = load16<Tag>(X, (int64_t)n * d + i) * ix;
@@ -883,14 +1193,22 @@ void launch_bwd16(const StepArgs& a, const StepWs& w, const Margin& mg, float sB
   const int B = (int)a.B;
   const int n_cu = device_cu_count();
   const int first_wave = (n_cu == kDwStaggerCUs && WI == 4) ? n_cu : 0;
+  const int n_rt = (int)ceil_div(B, kDxRows);
+  const int64_t n_tiles = (int64_t)n_rt * w.n_split;
+  const int64_t per_xcd = ceil_div(n_tiles, 8);
   timing_start(4, stream);
   // Row scales of the logit store from the lse the gradient is normalised with.
   hipLaunchKernelGGL(k_scales, dim3((unsigned)ceil_div(w.n_groups * w.ld_g, 4 * 256)), dim3(256), 0,
-                     stream, w.gmax, a.row_lse, B, w.ld_g, w.n_groups, a.n_active, w.gscale);
+                     stream, w.gmax, a.row_lse, B, w.ld_g, w.n_groups, a.n_active, w.gscale,
+                     a.active, w.act_pad, w.n_act_pad);
+  hipLaunchKernelGGL((k_dx16<Tag, WI>), dim3((unsigned)(8 * per_xcd)), dim3(128 * WI), 0, stream,
+                     (const uint16_t*)a.W, w.act_pad, a.n_active, w.inv_w, w.inv_w_max,
+                     (const uint16_t*)w.lbuf, w.ld_cos, w.gscale, w.ld_g, B, n_rt, w.n_split,
+                     n_tiles, per_xcd, w.dx_part);
   timing_stop(4, stream);
   timing_start(5, stream);
   hipLaunchKernelGGL(k_dx_final<Tag>, dim3((unsigned)B), dim3(256), 0, stream,
-                     w.dx_part, w.stats, w.n_split, a.X, a.W, a.active, a.labels_mapped, a.row_lse,
+                     w.dx_part, w.n_split, a.X, a.W, a.active, a.labels_mapped, a.row_lse,
                      w.inv_x, w.inv_w, w.tgtc, B, (int)a.d, mg, sB, a.dX);
   timing_stop(5, stream);
   timing_start(6, stream);

@@ -1,21 +1,472 @@
-// Stages 4-5 (the parts outside the fused contraction kernel of fwdx.hip):
-// the row-wise log-sum-exp and the batch loss (Partial FC Sec. 3.1,
-// Eq. sampled_probability; the max / sum decomposition of Sec. 3.2.1), and
-// the fp32 path of the cosine contraction for small problems.
+// Stages 4-5: the cosine-logit contraction cos = x_hat . w_hat over the
+// active classes (Partial FC Sec. 3.3.3, Eq. mp_gemm: [B x d][d x |S|]), the
+// target margin and the row-wise log-sum-exp cross-entropy over S
+// (Sec. 3.1, Eq. sampled_probability; max / sum decomposition of Sec. 3.2.1).
 //
-// On the 16-bit paths the fused kernel leaves one (m, sum 2^(f - m)) pair per
-// row and class slice; k_lse16 merges a row's pairs into lse_n and its loss
-// term, and k_loss takes the deterministic batch mean.
+// 16-bit path: one MFMA GEMM workgroup per 256 active classes (MFMA M) x 128
+// batch rows (MFMA N), d streamed in 32-wide chunks through a three-stage
+// direct-to-LDS ring; two workgroups share a CU.  Classes sit on the MFMA M
+// axis so that each lane holds one batch row and 64 of its classes: the row
+// max / sum-exp of the epilogue is mostly in-register.  The epilogue scales
+// by 1/||x_n|| and 1/||w_j|| (the class-row norms are summed from the
+// contraction's own class fragments), applies the margin at the target and
+// the optional PFC* conflict filter, and writes each logit once, as its fp16
+// softmax numerator E = 2^(f - m) relative to the maximum m of its row and
+// 128-class group (the tile is assembled in the idle LDS ring and stored as
+// whole rows), with one (max, sum E) pair per (row, class tile).  A small
+// kernel merges the pairs into lse_n and the loss.
 #include "pfc_gemm.h"
 
 namespace pfc {
 namespace {
 
-// Merge the per-slice (m, sum) pairs of a row: lse_n, and the row's loss
-// term.  One workgroup per row: the row maximum M over the slices, then
-// sum_s sum_s * 2^(m_s - M), each a fixed-order reduction.  A row with no
-// live logit (every pair (-inf, 0)) gets lse = -inf.
-__global__ void __launch_bounds__(256) k_lse16(const float2* __restrict__ stats, int n_split,
+constexpr int kFwdBM = 256;       // classes per tile (MFMA M)
+constexpr int kFwdBN = 128;       // batch rows per tile (MFMA N)
+constexpr int kFwdKC = 32;        // slice of d per pipeline stage
+constexpr int kFwdThreads = 256;  // 4 waves: 2 (classes) x 2 (rows), 128 x 64 each
+constexpr int kFwdStageA = kFwdBM * kFwdKC;  // uint16 elements per stage, class operand
+constexpr int kFwdStageB = kFwdBN * kFwdKC;  // uint16 elements per stage, batch operand
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kEpsNormW = 1e-12f;  // ||w|| floor of the normalisation
+
+// Three-stage LDS ring per operand (24 KB per stage; 75 KB in all, so two
+// workgroups share a CU and one's epilogue overlaps the other's MFMA loop).
+// One array per stage, so the compiler can keep the direct-to-LDS loads of
+// later stages in flight while a stage is read.  Row r of a stage holds 32
+// elements (64 B) as four 16-byte chunks; chunk c is stored at position
+// c ^ ((r >> 2) & 3), so the sixteen lanes of a 16-byte LDS read that
+// address sixteen consecutive rows hit distinct banks (64 banks).
+__shared__ __attribute__((aligned(1024))) uint16_t fA0[kFwdStageA], fA1[kFwdStageA],
+    fA2[kFwdStageA];
+__shared__ __attribute__((aligned(1024))) uint16_t fB0[kFwdStageB], fB1[kFwdStageB],
+    fB2[kFwdStageB];
+__shared__ float2 fRed[2][kFwdBN];
+__shared__ __attribute__((aligned(16))) float fIw[kFwdBM];
+__shared__ float fNrm[2][kFwdBM];
+
+template <int S>
+__device__ __forceinline__ uint16_t* fwd_a() {
+  if constexpr (S == 0) return fA0;
+  else if constexpr (S == 1) return fA1;
+  else return fA2;
+}
+template <int S>
+__device__ __forceinline__ uint16_t* fwd_b() {
+  if constexpr (S == 0) return fB0;
+  else if constexpr (S == 1) return fB1;
+  else return fB2;
+}
+
+// Row r (0..127) of the epilogue's cosine tile, rows of 256 elements: rows
+// 0..95 in the class-operand stages (32 each), 96..127 in two batch-operand
+// stages (16 each).
+__device__ __forceinline__ uint16_t* fwd_tile_row(int r) {
+  uint16_t* base;
+  if (r < 32) base = fA0 + r * kFwdBM;
+  else if (r < 64) base = fA1 + (r - 32) * kFwdBM;
+  else if (r < 96) base = fA2 + (r - 64) * kFwdBM;
+  else if (r < 112) base = fB0 + (r - 96) * kFwdBM;
+  else base = fB1 + (r - 112) * kFwdBM;
+  return base;
+}
+
+// DMA of one stage: class operand rows 16 (4 wave + u) + lane / 4 (u < 4),
+// batch operand rows 16 (2 wave + u) + lane / 4 (u < 2).
+template <int S>
+__device__ __forceinline__ void fwd_issue(const uint16_t* const ap[4], const uint16_t* const bp[2],
+                                          int k0, int64_t kb, int wave) {
+#pragma unroll
+  for (int u = 0; u < 4; ++u) dma16(ap[u] + k0, fwd_a<S>() + (4 * wave + u) * 16 * kFwdKC);
+#pragma unroll
+  for (int u = 0; u < 2; ++u) dma16(bp[u] + kb, fwd_b<S>() + (2 * wave + u) * 16 * kFwdKC);
+}
+
+// a0^2 + a1^2 + acc for a packed pair of 16-bit values (v_dot2_f32_*).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ float sumsq2(uint32_t v, float acc, F16Tag) {
+  const f16x2_t h = __builtin_bit_cast(f16x2_t, v);
+  return __builtin_amdgcn_fdot2(h, h, acc, false);
+}
+__device__ __forceinline__ float sumsq2(uint32_t v, float acc, Bf16Tag) {
+  const bf16x2_t h = __builtin_bit_cast(bf16x2_t, v);
+  return __builtin_amdgcn_fdot2_f32_bf16(h, h, acc, false);
+}
+
+// Fragments of both 16-wide k-steps of a stage are requested first, then
+// consumed: lane l reads row 32 q + l % 32 of its operand block, chunk
+// 2 kk + l / 32 (stored at chunk ^ ((row >> 2) & 3)).  The class-operand
+// fragments also feed the class-row norms: the wave with wn == kk adds the
+// squares of its k-step's fragments to wss[mb] (class row 128 wm + 32 mb +
+// l % 32, elements 8 (l / 32) .. + 7 of the k-step).
+template <int S, typename Tag>
+__device__ __forceinline__ void fwd_compute(f32x16_t (&acc)[4][2], int wm, int wn, int lane,
+                                            float (&wss)[4]) {
+  const int r32 = lane & 31;
+  const int sw = (lane >> 2) & 3;
+  const uint32_t arow = lds_addr(fwd_a<S>()) + (128 * wm + r32) * kFwdKC * 2;
+  const uint32_t brow = lds_addr(fwd_b<S>()) + (64 * wn + r32) * kFwdKC * 2;
+  u32x4_t af[2][4], bf[2][2];
+  static_for<0, 2>([&](auto kq) {
+    constexpr int kk = decltype(kq)::value;
+    const uint32_t chunk = (uint32_t)(((2 * kk + (lane >> 5)) ^ sw) * 16);
+    static_for<0, 4>([&](auto mm) {
+      constexpr int mb = decltype(mm)::value;
+      ds_read_128<32 * mb * kFwdKC * 2>(af[kk][mb], arow + chunk);
+    });
+    static_for<0, 2>([&](auto nn) {
+      constexpr int nb = decltype(nn)::value;
+      ds_read_128<32 * nb * kFwdKC * 2>(bf[kk][nb], brow + chunk);
+    });
+  });
+  static_for<0, 2>([&](auto kq) {
+    constexpr int kk = decltype(kq)::value;
+    if constexpr (kk == 0)
+      lgkm_wait<6>(af[0][0], af[0][1], af[0][2], af[0][3], bf[0][0], bf[0][1]);
+    else
+      lgkm_wait<0>(af[1][0], af[1][1], af[1][2], af[1][3], bf[1][0], bf[1][1]);
+    if (wn == kk) {
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb) {
+        wss[mb] = sumsq2(af[kk][mb].x, wss[mb], Tag{});
+        wss[mb] = sumsq2(af[kk][mb].y, wss[mb], Tag{});
+        wss[mb] = sumsq2(af[kk][mb].z, wss[mb], Tag{});
+        wss[mb] = sumsq2(af[kk][mb].w, wss[mb], Tag{});
+      }
+    }
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+        acc[mb][nb] = mfma_32x32x16(make_uint4(af[kk][mb].x, af[kk][mb].y, af[kk][mb].z, af[kk][mb].w),
+                                    make_uint4(bf[kk][nb].x, bf[kk][nb].y, bf[kk][nb].z, bf[kk][nb].w),
+                                    acc[mb][nb], Tag{});
+  });
+}
+
+// Epilogue of one lane for one 32-row block (nb): the lane's row n and its
+// 64 classes j = jb + 32 mb + 8 g + e (jb = first class of the lane's
+// pattern, e < 4); with the partner lane (half ^ 1) they are the row's 128
+// classes of one group.  Computes the base-2 logits f2 = s c log2 e (-inf at
+// the target, whose margined logit is merged separately, past |S|, and with
+// FILT at a negative whose cosine exceeds tau: the PFC* conflict filter,
+// Sec. 3.3.4, Eq. noise_filtering, so E = 0 there and the backward's
+// coefficient too), the
+// group maximum m (the target's margined logit included), and writes
+// E = 2^(f2 - m) as fp16 to the LDS tile row trow (16-byte block b of the row
+// at position b ^ bsw).  Returns the pair's (m, sum of E and the target term).
+template <bool CHECK_J, bool CHECK_T, bool FILT>
+__device__ __forceinline__ void fwd_epilogue_rows(f32x16_t (&acc)[4][2], int nb, float ix,
+                                                  const float* iwp, int K, int64_t jb, int tpos,
+                                                  const Margin& mg, float tau, uint16_t* trow,
+                                                  int bbase, int bsw, int half, float* mx_out,
+                                                  float* sm_out, float* tgt_out, float* tgtc_out) {
+  const float s2 = mg.s * kLog2e;
+  float mx = -INFINITY;
+  float ct = 0.0f;
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int o = 32 * mb + 8 * g;
+      const float4 iw4 = *reinterpret_cast<const float4*>(iwp + o);
+      const float iwv[4] = {iw4.x, iw4.y, iw4.z, iw4.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float c = acc[mb][nb][4 * g + e] * ix * iwv[e];
+        float f2 = c * s2;
+        if (CHECK_J && jb + o + e >= K) f2 = -INFINITY;
+        if (FILT && c > tau) f2 = -INFINITY;   // PFC* drops the negative (not the target: below)
+        if (CHECK_T && tpos == o + e) {
+          ct = c;
+          f2 = -INFINITY;   // the margined target logit is merged below
+        }
+        acc[mb][nb][4 * g + e] = f2;
+        mx = fmaxf(mx, f2);
+      }
+    }
+  }
+  float ft2 = -INFINITY;
+  if (CHECK_T && tgt_out) {
+    const float ft = target_logit(mg, ct);
+    *tgt_out = ft;
+    *tgtc_out = ct;
+    ft2 = ft * kLog2e;
+    mx = fmaxf(mx, ft2);
+  }
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  // A group with no live logit keeps reference 0 (all its E are 0).
+  const float mref = mx == -INFINITY ? 0.0f : mx;
+  float sm = 0.0f;
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int o = 32 * mb + 8 * g;
+      float ev[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        ev[e] = __builtin_amdgcn_exp2f(acc[mb][nb][4 * g + e] - mref);
+        sm += ev[e];
+      }
+      uint2 packed;
+      packed.x = pack_f16x2(ev[0], ev[1]);
+      packed.y = pack_f16x2(ev[2], ev[3]);
+      *reinterpret_cast<uint2*>(trow + 8 * ((bbase + o / 8) ^ bsw) + 4 * half) = packed;
+    }
+  }
+  if (CHECK_T && tgt_out) sm += __builtin_amdgcn_exp2f(ft2 - mref);
+  sm += __shfl_xor(sm, 32, 64);
+  *mx_out = mx;
+  *sm_out = sm;
+}
+
+// The common case of fwd_epilogue_rows: every class of the lane's pattern
+// exists, none is a row's target, no filter.  With q = s log2 e / ||x|| >= 0
+// the group maximum is q max_j u_j over u_j = acc_j / ||w_j||, and
+// E_j = 2^(u_j q - m) takes one fused multiply-add.
+__device__ __forceinline__ void fwd_epilogue_rows_plain(f32x16_t (&acc)[4][2], int nb, float q,
+                                                        const float* iwp, uint16_t* trow,
+                                                        int bbase, int bsw, int half,
+                                                        float* mx_out, float* sm_out) {
+  float mu = -INFINITY;
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const float4 iw4 = *reinterpret_cast<const float4*>(iwp + 32 * mb + 8 * g);
+      const float iwv[4] = {iw4.x, iw4.y, iw4.z, iw4.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float u = acc[mb][nb][4 * g + e] * iwv[e];
+        acc[mb][nb][4 * g + e] = u;
+        mu = fmaxf(mu, u);
+      }
+    }
+  }
+  mu = fmaxf(mu, __shfl_xor(mu, 32, 64));
+  const float mx = mu * q;
+  float sm = 0.0f;
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int o = 32 * mb + 8 * g;
+      float ev[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        ev[e] = __builtin_amdgcn_exp2f(fmaf(acc[mb][nb][4 * g + e], q, -mx));
+        sm += ev[e];
+      }
+      uint2 packed;
+      packed.x = pack_f16x2(ev[0], ev[1]);
+      packed.y = pack_f16x2(ev[2], ev[3]);
+      *reinterpret_cast<uint2*>(trow + 8 * ((bbase + o / 8) ^ bsw) + 4 * half) = packed;
+    }
+  }
+  sm += __shfl_xor(sm, 32, 64);
+  *mx_out = mx;
+  *sm_out = sm;
+}
+
+// Tile: 256 active classes x 128 batch rows, the whole of d (= 32 * NK).
+// Epilogue, per (row, class): c = acc / (||x|| ||w||) and the base-2 logit
+// s c log2 e (the margined logit at the target, which also goes to tgt[n],
+// its cosine to tgtc[n]); per (row, 128-class group) the maximum m, written
+// to gmax, and E = 2^(f - m) in fp16; per (row, class tile) the pair
+// (max, sum E), merged by k_lse16.  The batch operand comes from the
+// column-blocked copy of X (block k = [ld_xb][32]), so a stage's 128 batch
+// rows are one contiguous 8 KB run.
+template <typename Tag, int NK, bool FILT>
+__global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
+    const uint16_t* __restrict__ Xb, int64_t ld_xb, const uint16_t* __restrict__ W,
+    const int32_t* __restrict__ active, const int32_t* __restrict__ n_active_p,
+    const int32_t* __restrict__ yhat, const float* __restrict__ inv_x,
+    float* __restrict__ inv_w, float* __restrict__ inv_w_max, int B, int64_t ld_cos,
+    int64_t n_ctiles, int n_rt, int64_t n_tiles, int64_t per_xcd, Margin mg, float tau,
+    uint16_t* __restrict__ lbuf, float2* __restrict__ stats, float* __restrict__ tgt,
+    float* __restrict__ tgtc, float* __restrict__ gmax, int64_t ld_g) {
+  constexpr int D = NK * kFwdKC;
+  // All batch-row tiles of a class tile run on one XCD: the gathered W rows
+  // come from HBM once and are re-read from that XCD's L2.
+  const int64_t t = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  if (t >= n_tiles) return;
+  const int64_t ct = t / n_rt;
+  const int rt = (int)(t % n_rt);
+  const int K = *n_active_p;
+  const int64_t j0 = ct * kFwdBM;
+  if (j0 >= K) return;
+  const int n0 = rt * kFwdBN;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int half = lane >> 5, l32 = lane & 31;
+
+  // Per-lane source rows of the DMA segments; rows past the end are clamped
+  // to a valid row (their results are masked in the epilogue).
+  const int cidx = (lane & 3) ^ ((lane >> 4) & 3);
+  const uint16_t* ap[4];
+  const uint16_t* bp[2];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int row = 16 * (4 * wave + u) + (lane >> 2);
+    const int64_t jr = j0 + row < K ? j0 + row : K - 1;
+    ap[u] = W + (int64_t)active[jr] * D + 8 * cidx;
+  }
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int row = 16 * (2 * wave + u) + (lane >> 2);
+    const int nr = n0 + row < B ? n0 + row : B - 1;
+    bp[u] = Xb + (int64_t)nr * kFwdKC + 8 * cidx;
+  }
+
+  f32x16_t acc[4][2];
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.0f;
+
+  // Epilogue inputs, requested before the main loop: each lane's row data.
+  float ixr[2];
+  int yhr[2];
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb) {
+    const int n = n0 + 64 * wn + 32 * nb + l32;
+    ixr[nb] = n < B ? inv_x[n] : 0.0f;
+    yhr[nb] = n < B ? yhat[n] : -1;
+  }
+
+  float wss[4] = {0.0f, 0.0f, 0.0f, 0.0f};  // partial ||w||^2 of the lane's class rows
+  constexpr int kPerStage = 6;  // DMAs per thread per stage
+  fwd_issue<0>(ap, bp, 0, 0, wave);
+  if constexpr (NK > 1) fwd_issue<1>(ap, bp, kFwdKC, (int64_t)kFwdKC * ld_xb, wave);
+  static_for<0, NK>([&](auto cc) {
+    constexpr int c = decltype(cc)::value;
+    constexpr int ahead = (NK - 1 - c) < 1 ? (NK - 1 - c) : 1;
+    // This wave's loads of chunk c have landed; after the barrier everyone's
+    // have, and every wave is done with chunk c - 1, whose stage is refilled.
+    wait_vmcnt<kPerStage * ahead>();
+    stage_barrier();
+    if constexpr (c + 2 < NK) fwd_issue<(c + 2) % 3>(ap, bp, (c + 2) * kFwdKC, (int64_t)(c + 2) * kFwdKC * ld_xb, wave);
+    fwd_compute<c % 3, Tag>(acc, wm, wn, lane, wss);
+  });
+
+  // Inverse norms of the tile's class rows (stage 3 of the step, computed from
+  // the rows this kernel streams anyway): the four partial sums of a row
+  // (lane halves, and the two waves wn = 0, 1) meet in LDS; the norms stay in
+  // LDS for the epilogue, and the first batch-row tile of each class tile
+  // also publishes them, and their running maximum, for the backward kernels.
+  {
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) {
+      const float s = wss[mb] + __shfl_xor(wss[mb], 32, 64);
+      if (half == 0) fNrm[wn][128 * wm + 32 * mb + l32] = s;
+    }
+    wait_lgkm0();
+    stage_barrier();
+    const float inv = 1.0f / fmaxf(sqrtf(fNrm[0][tid] + fNrm[1][tid]), kEpsNormW);
+    fIw[tid] = inv;
+    if (rt == 0) {
+      const bool jok = j0 + tid < (int64_t)K;
+      inv_w[j0 + tid] = jok ? inv : 0.0f;
+      const float m = wave_max(jok ? inv : 0.0f);
+      if (lane == 0) atomicMax(reinterpret_cast<int*>(inv_w_max), __float_as_int(m));
+    }
+  }
+
+  // ---- epilogue.  The fp16 256-class x 128-row tile of E values is
+  // assembled in the (now idle) LDS ring (rows of 512 B, 16-byte block b of
+  // row r at position b ^ (r & 15): conflict-free writes from the MFMA layout
+  // and reads along rows), then written out in whole rows.
+  wait_lgkm0();
+  stage_barrier();  // all fragment reads of the ring are done
+  const int64_t jlo = j0 + 128 * wm;
+  const bool full = jlo + 128 <= (int64_t)K;   // wave-uniform: no class past |S|
+  const float* iwp = fIw + 128 * wm + 4 * half;
+  // Rows of the lane, and whether the lane's class pattern holds a row's target.
+  int tpos[2];
+  bool has_t[2];
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb) {
+    const int yh = yhr[nb];
+    tpos[nb] = yh - (int)(jlo + 4 * half);   // target's offset in this lane's class pattern
+    has_t[nb] = yh >= jlo && yh < jlo + 128 && ((tpos[nb] & 4) == 0);
+  }
+  auto finish = [&](int nb, float mx, float sm) __attribute__((always_inline)) {
+    const int nl = 64 * wn + 32 * nb + l32;
+    const int n = n0 + nl;
+    if (half == 0) {
+      fRed[wm][nl] = make_float2(mx, sm);
+      // reference of the row's 128-class group 2 ct + wm
+      if (n < B) gmax[(2 * ct + wm) * ld_g + n] = mx == -INFINITY ? 0.0f : mx;
+    }
+  };
+  // Two separate paths over both row blocks, so that the masking work of
+  // the checked one (classes past |S|, targets) stays out of the common one.
+  if (full && !__any(has_t[0] || has_t[1])) {
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      const int nl = 64 * wn + 32 * nb + l32;
+      float mx, sm;
+      if constexpr (FILT)
+        fwd_epilogue_rows<false, false, true>(acc, nb, ixr[nb], iwp, K, jlo + 4 * half, tpos[nb],
+                                              mg, tau, fwd_tile_row(nl), 16 * wm, nl & 15, half,
+                                              &mx, &sm, nullptr, nullptr);
+      else
+        fwd_epilogue_rows_plain(acc, nb, ixr[nb] * (mg.s * kLog2e), iwp, fwd_tile_row(nl),
+                                16 * wm, nl & 15, half, &mx, &sm);
+      finish(nb, mx, sm);
+    }
+  } else {
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      const int nl = 64 * wn + 32 * nb + l32;
+      const int n = n0 + nl;
+      float mx, sm;
+      fwd_epilogue_rows<true, true, FILT>(acc, nb, ixr[nb], iwp, K, jlo + 4 * half, tpos[nb], mg,
+                                          tau, fwd_tile_row(nl), 16 * wm, nl & 15, half, &mx,
+                                          &sm, has_t[nb] ? tgt + n : nullptr,
+                                          has_t[nb] ? tgtc + n : nullptr);
+      finish(nb, mx, sm);
+    }
+  }
+  wait_lgkm0();
+  stage_barrier();
+  // Wave w writes rows 32 w .. 32 w + 31, two rows (2 x 512 B) per store;
+  // all of its LDS reads are issued before the first store.  The stores are
+  // non-temporal: the logit store is read back only by later kernels, after
+  // gigabytes of other traffic, so it should not take L2 space from the
+  // operands this kernel re-reads.
+  {
+    const int b = lane & 31;
+    u32x4_t v[16];
+    static_for<0, 16>([&](auto ii) {
+      constexpr int i = decltype(ii)::value;
+      const int r = 32 * wave + 2 * i + (lane >> 5);
+      ds_read_128<0>(v[i], lds_addr(fwd_tile_row(r) + 8 * (b ^ (r & 15))));
+    });
+    lgkm_wait<0>(v);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int r = 32 * wave + 2 * i + (lane >> 5);
+      const int n = n0 + r;
+      if (n < B)
+        __builtin_nontemporal_store(
+            v[i], reinterpret_cast<u32x4_t*>(lbuf + (int64_t)n * ld_cos + j0 + 8 * b));
+    }
+  }
+  if (tid < kFwdBN) {
+    const int n = n0 + tid;
+    if (n < B) stats[(int64_t)n * n_ctiles + ct] = lse_merge2(fRed[0][tid], fRed[1][tid]);
+  }
+}
+
+// Merge the per-tile (max, sum) pairs of a row: lse_n, and the row's loss
+// term.  One workgroup per row: the row maximum M over the tiles, then
+// sum_tiles sum_t * 2^(max_t - M), each a fixed-order reduction.
+__global__ void __launch_bounds__(256) k_lse16(const float2* __restrict__ stats, int64_t n_ctiles,
+                                               const int32_t* __restrict__ n_active_p,
                                                const int32_t* __restrict__ yhat,
                                                const float* __restrict__ tgt, int B,
                                                float* __restrict__ row_lse,
@@ -23,8 +474,8 @@ __global__ void __launch_bounds__(256) k_lse16(const float2* __restrict__ stats,
   __shared__ float red[4];
   const int n = blockIdx.x;
   const int t = threadIdx.x, lane = t & 63;
-  const int64_t nct = n_split;
-  const float2* row = stats + (int64_t)n * n_split;
+  const int64_t nct = ceil_div((int64_t)*n_active_p, (int64_t)kFwdBM);
+  const float2* row = stats + (int64_t)n * n_ctiles;
   float mx = -INFINITY;
   for (int64_t c = t; c < nct; c += 256) mx = fmaxf(mx, row[c].x);
   mx = wave_max(mx);
@@ -122,6 +573,33 @@ __global__ void __launch_bounds__(1024) k_loss(const float* __restrict__ loss_pa
   }
 }
 
+template <typename Tag, int NK>
+void launch_fwd16_nk(unsigned grid, hipStream_t stream, const StepArgs& a, const StepWs& w, int B,
+                     int n_rt, int64_t n_tiles, int64_t per_xcd, const Margin& mg) {
+  if (a.tau < 1.0f)
+    hipLaunchKernelGGL((k_fwd16<Tag, NK, true>), dim3(grid), dim3(kFwdThreads), 0, stream,
+                       (const uint16_t*)w.xblk, w.ld_xt, (const uint16_t*)a.W, a.active, a.n_active,
+                       a.labels_mapped, w.inv_x, w.inv_w, w.inv_w_max, B, w.ld_cos, w.n_ctiles,
+                       n_rt, n_tiles, per_xcd, mg, a.tau, (uint16_t*)w.lbuf, w.stats, w.tgt,
+                       w.tgtc, w.gmax, w.ld_g);
+  else
+    hipLaunchKernelGGL((k_fwd16<Tag, NK, false>), dim3(grid), dim3(kFwdThreads), 0, stream,
+                       (const uint16_t*)w.xblk, w.ld_xt, (const uint16_t*)a.W, a.active, a.n_active,
+                       a.labels_mapped, w.inv_x, w.inv_w, w.inv_w_max, B, w.ld_cos, w.n_ctiles,
+                       n_rt, n_tiles, per_xcd, mg, a.tau, (uint16_t*)w.lbuf, w.stats, w.tgt,
+                       w.tgtc, w.gmax, w.ld_g);
+}
+
+template <typename Tag>
+void launch_fwd16(int d, unsigned grid, hipStream_t stream, const StepArgs& a, const StepWs& w,
+                  int B, int n_rt, int64_t n_tiles, int64_t per_xcd, const Margin& mg) {
+  switch (d) {
+    case 128: launch_fwd16_nk<Tag, 4>(grid, stream, a, w, B, n_rt, n_tiles, per_xcd, mg); break;
+    case 256: launch_fwd16_nk<Tag, 8>(grid, stream, a, w, B, n_rt, n_tiles, per_xcd, mg); break;
+    default: launch_fwd16_nk<Tag, 16>(grid, stream, a, w, B, n_rt, n_tiles, per_xcd, mg); break;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_forward(const StepArgs& a, const StepWs& w, hipStream_t stream) {
@@ -141,12 +619,20 @@ hipError_t launch_forward(const StepArgs& a, const StepWs& w, hipStream_t stream
                        (const float*)w.lbuf, w.ld_cos, a.n_active, a.labels_mapped, B, mg,
                        a.row_lse_out, w.loss_part);
   } else {
+    const int n_rt = (int)ceil_div(B, kFwdBN);
+    const int64_t n_tiles = w.n_ctiles * n_rt;
+    const int64_t per_xcd = ceil_div(n_tiles, 8);
+    const unsigned grid = (unsigned)(8 * per_xcd);
     timing_start(2, stream);
-    launch_fwdx16(a, w, mg, stream);
+    if (a.dtype == 1)
+      launch_fwd16<Bf16Tag>(d, grid, stream, a, w, B, n_rt, n_tiles, per_xcd, mg);
+    else
+      launch_fwd16<F16Tag>(d, grid, stream, a, w, B, n_rt, n_tiles, per_xcd, mg);
     timing_stop(2, stream);
     timing_start(3, stream);
-    hipLaunchKernelGGL(k_lse16, dim3((unsigned)B), dim3(256), 0, stream, w.stats, w.n_split,
-                       a.labels_mapped, w.tgt, B, a.row_lse_out, w.loss_part);
+    hipLaunchKernelGGL(k_lse16, dim3((unsigned)B), dim3(256), 0, stream, w.stats,
+                       w.n_ctiles, a.n_active, a.labels_mapped, w.tgt, B, a.row_lse_out,
+                       w.loss_part);
   }
   hipLaunchKernelGGL(k_loss, dim3(1), dim3(1024), 0, stream, w.loss_part, B, a.loss);
   timing_stop(3, stream);

@@ -44,9 +44,8 @@ struct SampleWs {
 
 // ----------------------------------------------------------------- step
 
-// Batch rows of a workgroup of the fused forward (16-bit paths); its class
-// slices are whole groups of the logit store.
-constexpr int kFwdRows = 64;
+// Class tile of the forward contraction (one softmax-statistics pair per row and tile).
+constexpr int kFwdClassTile = 256;
 // Class group of the logit store: the forward keeps one base-2 reference per
 // (row, group of 128 active classes).
 constexpr int kLogitGroup = 128;
@@ -56,26 +55,28 @@ struct StepWs {
   void* xbT;             // [ld_xt / 32][d][32] x_hat (normalised rows) transposed in blocks of
                          // 32 rows, bf16, zero past B (the class-gradient operand)
   int64_t ld_xt;         // B rounded up to 32
-  float* inv_w;          // [ld_cos] 1/max(||W[S_j]||, eps), 0 past |S| within the last chunk
+  void* xblk;            // [d / 32][ld_xt][32] the raw 16-bit batch rows in 32-wide column
+                         // blocks, zero past B (the forward's batch operand: one block is
+                         // a contiguous run of whole rows)
+  float* inv_w_max;      // [1] max_j 1/||W[S_j]|| (scale of the fp16 feature-gradient operand)
+  float* inv_w;          // [ld_cos] 1/max(||W[S_j]||, eps), 0 past |S| within the last tile
   void* lbuf;            // [B x ld_cos] logit store.  16-bit paths: fp16 E = 2^(f log2 e - m)
                          // with m the row's reference for the class's 128-class group (E = 0
                          // at the target and past |S|); fp32 path: fp32 cosines
   int64_t ld_cos;        // row stride of lbuf: cap rounded up to 256
-  float2* stats;         // [B x n_split] per (row, class slice): (m, sum 2^(f log2 e - m)),
-                         // base 2 (16-bit paths)
+  float2* stats;         // [B x n_ctiles] per class tile: (max, sum 2^(f log2 e - max)), base 2
+  int64_t n_ctiles;      // class tiles of the forward contraction
   float* tgt;            // [B] margined target logit
   float* tgtc;           // [B] unmargined target cosine
   float* gmax;           // [n_groups x ld_g] reference m of each (group, row)
   float* gscale;         // [n_groups x ld_g] 2^(m - lse log2 e), so p = E * gscale (0 past B)
   int64_t ld_g;          // B rounded up to 128
   int64_t n_groups;      // ld_cos / 128
-  float* dx_part;        // [n_split x B x d] per class slice: sum_j 2^(f log2 e - m) w_j / ||w_j||
-                         // with m that (row, slice)'s reference (16-bit paths; fp32 path:
-                         // one slice, the finished sum of the probabilities)
-  int n_split;           // class slices of the forward (16-bit paths), 1 on the fp32 path
+  float* dx_part;        // [n_split x B x d] split-K partial sums of dX_hat
+  int n_split;
   float* loss_part;      // [B] per-row loss terms
   int32_t* act_pad;      // [n_act_pad] the active row ids, padded with the last one
-                         // (read a whole 32-class chunk at a time by the fused forward)
+                         // (read a whole 32-class chunk at a time by the dX kernel)
   int64_t n_act_pad;     // cap rounded up to 32
 };
 
@@ -85,9 +86,9 @@ struct WsLayout {
   size_t sample_bytes;   // prefix used by the sampler
   size_t off_bitmap, off_hist, off_state, off_digits, off_cand, off_cand_key;
   size_t off_grp_sure, off_grp_tie, off_grp_out, off_grp_tie_off;
-  size_t off_inv_x, off_xb, off_inv_w, off_cos, off_stats, off_tgt, off_tgtc, off_gmax,
-      off_gscale, off_dx, off_loss, off_act_pad;
-  int64_t ld_cos, n_groups, ld_xt, ld_g, n_lgroups, n_act_pad;
+  size_t off_inv_x, off_xb, off_xblk, off_wmax, off_inv_w, off_cos, off_stats, off_tgt, off_tgtc,
+      off_gmax, off_gscale, off_dx, off_loss, off_act_pad;
+  int64_t ld_cos, n_ctiles, n_groups, ld_xt, ld_g, n_lgroups, n_act_pad;
   int n_split;
   int top_bits;
 };
@@ -127,8 +128,6 @@ struct StepArgs {
 };
 
 hipError_t launch_prep(const StepArgs& a, const StepWs& w, hipStream_t stream);
-struct Margin;
-void launch_fwdx16(const StepArgs& a, const StepWs& w, const Margin& mg, hipStream_t stream);
 hipError_t launch_forward(const StepArgs& a, const StepWs& w, hipStream_t stream);
 hipError_t launch_backward(const StepArgs& a, const StepWs& w, hipStream_t stream);
 

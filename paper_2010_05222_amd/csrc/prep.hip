@@ -5,10 +5,9 @@
 // The normalised rows are never materialised: the contractions use the raw
 // 16-bit rows (exact products in fp32) and apply 1/||x_n|| and 1/||w_j|| as
 // row / column scales.  On the 16-bit paths the class-row norms come out of
-// the fused forward kernel, which streams every active row through LDS
-// anyway; this file holds the batch side (norms, the transposed bf16 copy
-// used by the class-gradient contraction), the padded copy of the active ids
-// the fused forward reads a chunk at a time, and the fp32 path.
+// the forward contraction kernel, which streams every active row through
+// LDS anyway; this file holds the batch side (norms, the transposed bf16
+// copy used by the class-gradient contraction) and the fp32 path.
 #include "pfc_device.h"
 
 namespace pfc {
@@ -28,18 +27,24 @@ __device__ __forceinline__ float sumsq8(const uint4& v) {
   return acc;
 }
 
-// inv_x[n], and a transposed bf16 copy of the normalised batch x_hat in
-// blocks of 32 rows (block c = [d][32]: entry (i, r) = x_hat[32 c + r][i]),
-// the K-major operand of the class-gradient contraction, which a workgroup
-// transposes through LDS.  Rows n in [B, ld_xt) are zero.
+// inv_x[n]; a transposed bf16 copy of the normalised batch x_hat in blocks
+// of 32 rows (block c = [d][32]: entry (i, r) = x_hat[32 c + r][i]), the
+// K-major operand of the class-gradient contraction, which a workgroup
+// transposes through LDS; and the raw rows in 32-wide column blocks (block k
+// = [ld_xt][32]: entry (n, e) = X[n][32 k + e]), the forward's operand, whose
+// k-th chunk of a run of rows is then contiguous.  Rows n in [B, ld_xt) are
+// zero in both.  Also clears the running max of 1/||w_j||.
 constexpr int kPrepRows = 32;
 template <typename Tag>
 __global__ void __launch_bounds__(256) k_prep_x16(const uint16_t* __restrict__ X, int B, int d,
-                                                  float* __restrict__ inv_x,
-                                                  uint16_t* __restrict__ xbT) {
+                                                  int64_t ld_xt, float* __restrict__ inv_x,
+                                                  uint16_t* __restrict__ xbT,
+                                                  uint16_t* __restrict__ xblk,
+                                                  float* __restrict__ inv_w_max) {
   __shared__ uint16_t tile[kPrepRows][512 + 8];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n0 = blockIdx.x * kPrepRows;
+  if (blockIdx.x == 0 && threadIdx.x == 0) *inv_w_max = 0.0f;
   for (int r = wave; r < kPrepRows; r += 4) {
     const int n = n0 + r;
     const bool c_ok = lane < d / 8;   // d <= 512: one 16-byte piece per lane
@@ -49,6 +54,7 @@ __global__ void __launch_bounds__(256) k_prep_x16(const uint16_t* __restrict__ X
     const float ix = 1.0f / fmaxf(sqrtf(ss), kEpsNorm);
     if (lane == 0 && n < B) inv_x[n] = ix;
     if (c_ok) {
+      *reinterpret_cast<uint4*>(xblk + ((int64_t)(lane >> 2) * ld_xt + n) * 32 + 8 * (lane & 3)) = v;
       const uint16_t* h = reinterpret_cast<const uint16_t*>(&v);
       uint16_t o[8];
 #pragma unroll
@@ -71,20 +77,6 @@ __global__ void __launch_bounds__(256) k_prep_x16(const uint16_t* __restrict__ X
     __builtin_memcpy(&ov, o, 16);
     *reinterpret_cast<uint4*>(blk + i * kPrepRows + r0) = ov;
   }
-}
-
-// The padded copy of the active ids: act_pad[j] = active[min(j, |S| - 1)]
-// (0 if S is empty), four entries per thread (n_pad is a multiple of 32).
-__global__ void __launch_bounds__(256) k_pad_active(const int32_t* __restrict__ active,
-                                                    const int32_t* __restrict__ n_active_p,
-                                                    int32_t* __restrict__ act_pad, int64_t n_pad) {
-  const int64_t i = 4 * ((int64_t)blockIdx.x * blockDim.x + threadIdx.x);
-  if (i >= n_pad) return;
-  const int64_t K = *n_active_p;
-  int o[4];
-#pragma unroll
-  for (int e = 0; e < 4; ++e) o[e] = K > 0 ? active[i + e < K ? i + e : K - 1] : 0;
-  *reinterpret_cast<int4*>(act_pad + i) = make_int4(o[0], o[1], o[2], o[3]);
 }
 
 __global__ void __launch_bounds__(256) k_prep_x32(const float* __restrict__ X, int B, int d,
@@ -128,15 +120,14 @@ hipError_t launch_prep(const StepArgs& a, const StepWs& w, hipStream_t stream) {
                        (const float*)a.X, B, d, w.inv_x);
     hipLaunchKernelGGL(k_norm_w32, dim3(wblocks), dim3(256), 0, stream, (const float*)a.W, d,
                        a.active, a.n_active, a.cap, w.inv_w);
+  } else if (a.dtype == 1) {
+    hipLaunchKernelGGL(k_prep_x16<Bf16Tag>, dim3((unsigned)(w.ld_xt / kPrepRows)), dim3(256), 0,
+                       stream, (const uint16_t*)a.X, B, d, w.ld_xt, w.inv_x, (uint16_t*)w.xbT,
+                       (uint16_t*)w.xblk, w.inv_w_max);
   } else {
-    if (a.dtype == 1)
-      hipLaunchKernelGGL(k_prep_x16<Bf16Tag>, dim3((unsigned)(w.ld_xt / kPrepRows)), dim3(256), 0,
-                         stream, (const uint16_t*)a.X, B, d, w.inv_x, (uint16_t*)w.xbT);
-    else
-      hipLaunchKernelGGL(k_prep_x16<F16Tag>, dim3((unsigned)(w.ld_xt / kPrepRows)), dim3(256), 0,
-                         stream, (const uint16_t*)a.X, B, d, w.inv_x, (uint16_t*)w.xbT);
-    hipLaunchKernelGGL(k_pad_active, dim3((unsigned)ceil_div(w.n_act_pad, 4 * 256)), dim3(256), 0,
-                       stream, a.active, a.n_active, w.act_pad, w.n_act_pad);
+    hipLaunchKernelGGL(k_prep_x16<F16Tag>, dim3((unsigned)(w.ld_xt / kPrepRows)), dim3(256), 0,
+                       stream, (const uint16_t*)a.X, B, d, w.ld_xt, w.inv_x, (uint16_t*)w.xbT,
+                       (uint16_t*)w.xblk, w.inv_w_max);
   }
   timing_stop(1, stream);
   return hipGetLastError();
