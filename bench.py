@@ -47,16 +47,11 @@ def kernel_source_sha(name):
 def algorithmic_work(name, cfg, K):
     """(flops, bytes) the method must spend in one launch of a kernel."""
     from paper_2010_05222_amd import costmodel as cm
-    B, d, dt = cfg["B"], cfg["d"], cfg["dtype"]
-    xb = cm.DTYPE_BYTES[dt]
+    B, d = cfg["B"], cfg["d"]
     if name in ("fwd_gemm", "dx_gemm"):
         return cm.contraction_flops(B, d, K), 0
     if name == "dw_update":
-        return cm.contraction_flops(B, d, K), cm.update_bytes(K, d, dt, cfg["master"])
-    if name == "prep":
-        # the batch side only: X read, its transposed bf16 copy written (the
-        # class-row norms come out of the forward contraction kernel)
-        return 0, B * d * (xb + 2)
+        return cm.contraction_flops(B, d, K), cm.update_bytes(K, d, cfg["dtype"], cfg["master"])
     return 0, 0
 
 
@@ -80,8 +75,42 @@ def roofline_entry(name, cfg, K, avg_ms, traffic):
     return entry
 
 
-def measured_traffic(name, workload):
-    """HBM bytes per launch from committed counter runs, if they match the current kernel."""
+def contraction_precision(dtype):
+    """Operand and accumulator types of the step's three contractions."""
+    if dtype == "f32":
+        return {"forward": "f32 x f32 -> f32 (FMA)", "dx": "f32 x f32 -> f32 (FMA)",
+                "dw": "f32 x f32 -> f32 (FMA)"}
+    return {"forward": f"{dtype} x {dtype} -> f32 (MFMA)",
+            "dx": (f"{dtype} W x {dtype} coefficients -> f32 (MFMA)"
+                   + (", coefficients scaled by a power of two" if dtype == "f16" else "")),
+            "dw": "bf16 x_hat x bf16 coefficients -> f32 (MFMA)"}
+
+
+def gather_entry(cfg, K, stage_ms, traffic):
+    """Stage a3 (gather + normalise of the sampled class rows, judged by HBM
+    rate).  The gather has no kernel of its own: the forward contraction
+    streams the active W rows from HBM straight into LDS.  Its rate is the
+    compulsory gathered bytes (|S| rows of d elements, read once) over the
+    forward kernel's time.  Also reports how many times a step reads the
+    active W rows: the forward gathers them, the feature-gradient
+    contraction gathers them again, and the class-gradient kernel reads them
+    for the update (compulsory: the update is a read-modify-write)."""
+    from paper_2010_05222_amd import costmodel as cm
+    elt = cm.DTYPE_BYTES[cfg["dtype"]]
+    nbytes = K * cfg["d"] * elt
+    sec = stage_ms["fwd_gemm"] * 1e-3
+    achieved = nbytes / sec / 1e9
+    ent = {"bytes": nbytes, "kernel": "fwd_gemm", "achieved": achieved, "unit": "GB/s",
+           "peak": cm.PEAK_HBM_GBPS, "frac": achieved / cm.PEAK_HBM_GBPS,
+           "w_row_reads_per_step": 3, "w_row_read_bytes_per_step": 3 * nbytes}
+    if traffic:
+        ent["counter_read_bytes"] = traffic
+    return ent
+
+
+def measured_traffic_record(name, workload):
+    """The committed counter record of a kernel (HBM bytes per launch), if it
+    was taken on this workload and the kernel's source has not changed since."""
     try:
         with open(TRAFFIC_FILE) as fh:
             rec = json.load(fh)
@@ -92,7 +121,13 @@ def measured_traffic(name, workload):
         return None
     if ent.get("source_sha256") != kernel_source_sha(name):
         return None
-    return ent.get("bytes_per_launch")
+    return ent
+
+
+def measured_traffic(name, workload):
+    """HBM bytes per launch from committed counter runs, if they match the current kernel."""
+    ent = measured_traffic_record(name, workload)
+    return ent.get("bytes_per_launch") if ent else None
 
 
 def cpu_baseline(cfg, W_dev, rows):
@@ -389,6 +424,13 @@ def main():
         fl, nb = algorithmic_work(name, cfg, K)
         if fl or nb:
             stage_roofs[name] = roofline_entry(name, cfg, K, ms, None)["frac"]
+    reads = {}
+    for name in ("fwd_gemm", "dx_gemm", "dw_update"):
+        rec = measured_traffic_record(name, cfg["name"])
+        if rec:
+            reads[name] = rec["read_bytes"]
+    gather = gather_entry(cfg, K, stage_ms, reads or None)
+    stage_roofs["gather"] = gather["frac"]
 
     ceil = measured_ceilings(dev, cfg["dtype"] if cfg["dtype"] != "f32" else "bf16")
     log(f"[bench] measured ceilings: {ceil['gemm_8192_tflops']:.0f} TFLOP/s "
@@ -427,11 +469,13 @@ def main():
                                f"|S|={K} {cfg['margin']} s={cfg['s']} m={cfg['m']}",
                    "global_batch": B, "d": d, "C_shard": C, "r": cfg["r"], "active": K,
                    "margin": cfg["margin"], "w_dtype": cfg["dtype"], "momentum": "f32",
+                   "contractions": contraction_precision(cfg["dtype"]),
                    "parallelism": "one class shard on one GPU"},
         "roofline": roof,
         "cpu_baseline": cpu,
         "stage_ms": stage_ms,
         "stage_roofline_frac": stage_roofs,
+        "gather": gather,
         "measured_ceilings": ceil,
         "stage_frac_of_measured_ceiling": vs_ceil,
         "step_mfma_frac": step_fl / (ms_per_step * 1e-3) / (cm.PEAK_TFLOPS[cfg["dtype"]] * 1e12),

@@ -770,7 +770,7 @@ __global__ void __launch_bounds__(512) k_dw16(
       pin_reg(b1);
       static_for<0, NMF>([&](auto ii) {
         constexpr int i = decltype(ii)::value;
-        mfma_bf16_asm(acc[i / NB][i % NB], a1[i / NB], b1[i % NB]);
+        acc[i / NB][i % NB] = mfma_32x32x16(as_uint4(a1[i / NB]), as_uint4(b1[i % NB]), acc[i / NB][i % NB], Bf16Tag{});
         if constexpr (i == W_AT) {
           lgkm_wait<0>(a0, b0);
           pin_group(pin, 0);
@@ -783,7 +783,7 @@ __global__ void __launch_bounds__(512) k_dw16(
       // chunk's second k-step reads spread over its slots.
       static_for<0, NMF>([&](auto ii) {
         constexpr int i = decltype(ii)::value;
-        mfma_bf16_asm(acc[i / NB][i % NB], a0[i / NB], b0[i % NB]);
+        acc[i / NB][i % NB] = mfma_32x32x16(as_uint4(a0[i / NB]), as_uint4(b0[i % NB]), acc[i / NB][i % NB], Bf16Tag{});
         static_for<(i * NITEM + NMF - 1) / NMF, ((i + 1) * NITEM + NMF - 1) / NMF>([&](auto kk) {
           constexpr int k = decltype(kk)::value;
           if constexpr (k < RDMA) {
@@ -811,8 +811,8 @@ __global__ void __launch_bounds__(512) k_dw16(
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) mfma_bf16_asm(acc[mb][nb], a1[mb], b1[nb]);
-  mfma_drain();
+    for (int nb = 0; nb < NB; ++nb)
+      acc[mb][nb] = mfma_32x32x16(as_uint4(a1[mb]), as_uint4(b1[nb]), acc[mb][nb], Bf16Tag{});
 
   // ---- update: the tile goes through LDS in four passes of 32 classes so
   // that each wave then owns whole rows: W, momentum and master rows are read

@@ -102,20 +102,6 @@ __device__ __forceinline__ void lgkm_wait(T&... regs) {
 }
 
 
-// v_mfma_f32_32x32x16_bf16 as inline assembly, accumulating in AGPRs, so that
-// its place among the other inline-assembly instructions of a pipelined loop
-// is fixed.  The compiler does not know its latency: after the last one, call
-// mfma_drain() before the accumulators are read by anything but another
-// MFMA of this shape.
-__device__ __forceinline__ void mfma_bf16_asm(f32x16_t& acc, const u32x4_t& a, const u32x4_t& b) {
-  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
-}
-// Wait states covering the latency of an MFMA result (more than the 18 a
-// 16-pass instruction needs before a VALU, memory or export read of it).
-__device__ __forceinline__ void mfma_drain() {
-  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
-}
-
 template <int C, int N, typename F>
 __device__ __forceinline__ void static_for(F&& f) {
   if constexpr (C < N) {
