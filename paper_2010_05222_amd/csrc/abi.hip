@@ -115,6 +115,7 @@ WsLayout ws_layout(int64_t B, int64_t d, int64_t C, int64_t cap, int compute) {
   L.off_gscale = take(compute == PFC_F32 ? 0 : (size_t)L.n_lgroups * L.ld_g * 4);
   L.n_act_pad = round_up(cap, 32);
   L.off_act_pad = take(compute == PFC_F32 ? 0 : (size_t)L.n_act_pad * 4);
+  L.off_dw_gate = take(compute == PFC_F32 ? 0 : (size_t)kDwGates * 4);
   L.bytes = off;
   return L;
 }
@@ -159,6 +160,7 @@ StepWs step_ws(void* ws, const WsLayout& L) {
   w.n_groups = L.n_lgroups;
   w.act_pad = (int32_t*)(b + L.off_act_pad);
   w.n_act_pad = L.n_act_pad;
+  w.dw_gate = (int32_t*)(b + L.off_dw_gate);
   return w;
 }
 

@@ -23,6 +23,8 @@
 //   epilogue has complete rows: target terms, tangent projection, momentum,
 //   weight step and the scatter into the persistent W / momentum rows (unique
 //   rows, no atomics).  It runs after the dX kernels, which read the old W.
+#include <atomic>
+
 #include "pfc_gemm.h"
 
 namespace pfc {
@@ -36,7 +38,7 @@ constexpr int kDxRows = 128;       // batch rows of a dX workgroup
 constexpr int kDwCls = 128;        // classes of a dW workgroup
 constexpr int kTLd = 260;         // LDS row stride (floats) of the update's staged gradient rows
 constexpr int kHitCap = 256;      // target rows listed per wave of a dW workgroup
-constexpr int kDwStaggerCUs = 256;  // CU count of the part the dW start offset was tuned on
+constexpr int kGateSpins = 512;   // polls of a dW start gate before the workgroup goes ahead anyway
 
 // Every operand reaches LDS through direct-to-LDS loads into three-stage
 // rings (one array per stage, so the compiler can keep later stages in
@@ -533,7 +535,7 @@ __global__ void __launch_bounds__(512) k_dw16(
     const float* __restrict__ inv_x, const float* __restrict__ inv_w,
     const float* __restrict__ tgtc, const uint16_t* __restrict__ lbuf, int64_t ld_cos,
     const float* __restrict__ gscale, int64_t ld_g, int B, Margin mg, float sB, float lr,
-    float mu, int first_wave) {
+    float mu, int32_t* __restrict__ gate, int n_gate, int epoch) {
   constexpr int D = 128 * WI;
   constexpr int NW = 8;
   constexpr int DW = D / 4;             // d entries of a wave
@@ -550,16 +552,25 @@ __global__ void __launch_bounds__(512) k_dw16(
   const int K = *n_active_p;
   const int64_t j0 = (int64_t)blockIdx.x * kDwCls;
   if (j0 >= K) return;
-  // On a long grid, every second workgroup of the first wave (first_wave =
-  // one workgroup per CU, 0 = no offset) starts about half a workgroup's
-  // lifetime late.  Otherwise all CUs run the contraction and then the
-  // memory-bound update in step for the first few hundred microseconds, and
-  // the updates, all at once, saturate HBM; with the offset about half of the
-  // CUs update at any time from the start.  The length (~65 k cycles) is tuned
-  // for the 256-CU MI355X at d = 512; the launcher passes 0 on other parts.
-  if (first_wave > 0 && gridDim.x >= 4 * first_wave && (int)blockIdx.x < first_wave &&
-      (blockIdx.x & 1)) {
-    for (int z = 0; z < 8; ++z) __builtin_amdgcn_s_sleep(127);
+  // Start gates (n_gate > 0 on a long grid, one workgroup per CU): workgroup
+  // 2 i + 1 of the first wave starts once workgroup 2 i has finished its
+  // contraction, which it signals by writing this launch's number to gate[i].
+  // Otherwise all CUs run the contraction and then the memory-bound update in
+  // step for the first few hundred microseconds, and the updates, all at
+  // once, saturate HBM; with the gates about half of the CUs update at any
+  // time from the start.  The wait is bounded (kGateSpins polls), and the
+  // results never depend on it: a gate that is never opened, or holds the
+  // number by chance, only changes when the workgroup starts.
+  const bool gated = (int)blockIdx.x < 2 * n_gate;
+  if (gated && (blockIdx.x & 1)) {
+    if (threadIdx.x == 0) {
+      const int32_t* g = gate + blockIdx.x / 2;
+      for (int it = 0; it < kGateSpins; ++it) {
+        if (__hip_atomic_load(g, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == epoch) break;
+        __builtin_amdgcn_s_sleep(8);
+      }
+    }
+    __syncthreads();
   }
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -813,6 +824,8 @@ __global__ void __launch_bounds__(512) k_dw16(
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
       acc[mb][nb] = mfma_32x32x16(as_uint4(a1[mb]), as_uint4(b1[nb]), acc[mb][nb], Bf16Tag{});
+  if (gated && !(blockIdx.x & 1) && threadIdx.x == 0)
+    __hip_atomic_store(gate + blockIdx.x / 2, epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 
   // ---- update: the tile goes through LDS in four passes of 32 classes so
   // that each wave then owns whole rows: W, momentum and master rows are read
@@ -1191,8 +1204,13 @@ template <typename Tag, int WI>
 void launch_bwd16(const StepArgs& a, const StepWs& w, const Margin& mg, float sB,
                   hipStream_t stream) {
   const int B = (int)a.B;
+  // Start gates on grids of at least four waves of one workgroup per CU; each
+  // launch writes a number of its own to the gates it opens.
+  static std::atomic<int> launches{0};
   const int n_cu = device_cu_count();
-  const int first_wave = (n_cu == kDwStaggerCUs && WI == 4) ? n_cu : 0;
+  const int64_t dw_grid = ceil_div(a.cap, kDwCls);
+  const int n_gate = (n_cu > 0 && dw_grid >= 4LL * n_cu) ? (n_cu / 2 < kDwGates ? n_cu / 2 : kDwGates) : 0;
+  const int epoch = 1 + (launches.fetch_add(1, std::memory_order_relaxed) & 0x3FFFFFFF);
   const int n_rt = (int)ceil_div(B, kDxRows);
   const int64_t n_tiles = (int64_t)n_rt * w.n_split;
   const int64_t per_xcd = ceil_div(n_tiles, 8);
@@ -1213,17 +1231,17 @@ void launch_bwd16(const StepArgs& a, const StepWs& w, const Margin& mg, float sB
   timing_stop(5, stream);
   timing_start(6, stream);
   if (a.W_master)
-    hipLaunchKernelGGL((k_dw16<Tag, WI, true>), dim3((unsigned)ceil_div(a.cap, kDwCls)), dim3(512),
+    hipLaunchKernelGGL((k_dw16<Tag, WI, true>), dim3((unsigned)dw_grid), dim3(512),
                        0, stream, (const uint16_t*)w.xbT, w.ld_xt, a.X, (uint16_t*)a.W, a.W_master,
                        a.M, a.active, a.n_active, a.labels_mapped, a.row_lse, w.inv_x, w.inv_w,
                        w.tgtc, (const uint16_t*)w.lbuf, w.ld_cos, w.gscale, w.ld_g, B, mg, sB, a.lr,
-                       a.mu, first_wave);
+                       a.mu, w.dw_gate, n_gate, epoch);
   else
-    hipLaunchKernelGGL((k_dw16<Tag, WI, false>), dim3((unsigned)ceil_div(a.cap, kDwCls)), dim3(512),
+    hipLaunchKernelGGL((k_dw16<Tag, WI, false>), dim3((unsigned)dw_grid), dim3(512),
                        0, stream, (const uint16_t*)w.xbT, w.ld_xt, a.X, (uint16_t*)a.W, a.W_master,
                        a.M, a.active, a.n_active, a.labels_mapped, a.row_lse, w.inv_x, w.inv_w,
                        w.tgtc, (const uint16_t*)w.lbuf, w.ld_cos, w.gscale, w.ld_g, B, mg, sB, a.lr,
-                       a.mu, first_wave);
+                       a.mu, w.dw_gate, n_gate, epoch);
   timing_stop(6, stream);
 }
 

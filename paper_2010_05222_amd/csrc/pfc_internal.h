@@ -78,7 +78,12 @@ struct StepWs {
   int32_t* act_pad;      // [n_act_pad] the active row ids, padded with the last one
                          // (read a whole 32-class chunk at a time by the dX kernel)
   int64_t n_act_pad;     // cap rounded up to 32
+  int32_t* dw_gate;      // [kDwGates] start gates of the class-gradient kernel: entry i holds
+                         // the launch number once workgroup 2 i has finished its contraction
 };
+
+// Start gates of the class-gradient kernel (pairs of first-wave workgroups).
+constexpr int kDwGates = 512;
 
 // Layout of the whole workspace (offsets in bytes from its base).
 struct WsLayout {
@@ -87,7 +92,7 @@ struct WsLayout {
   size_t off_bitmap, off_hist, off_state, off_digits, off_cand, off_cand_key;
   size_t off_grp_sure, off_grp_tie, off_grp_out, off_grp_tie_off;
   size_t off_inv_x, off_xb, off_xblk, off_wmax, off_inv_w, off_cos, off_stats, off_tgt, off_tgtc,
-      off_gmax, off_gscale, off_dx, off_loss, off_act_pad;
+      off_gmax, off_gscale, off_dx, off_loss, off_act_pad, off_dw_gate;
   int64_t ld_cos, n_ctiles, n_groups, ld_xt, ld_g, n_lgroups, n_act_pad;
   int n_split;
   int top_bits;
