@@ -243,48 +243,59 @@ int pfc_timing_end(double* total_ms /*host*/, int* launches /*host*/);
  *              that step writes them back with newer values, and the next
  *              stages take them from its slot; the slot is free for reuse
  *              after the write-back.
- * Each copy is a byte copy of `row_bytes` per row (a multiple of 16, at most
- * 65536): d * 2 for 16-bit W, d * 4 for momentum and the master; one call per
- * array.  active / next_active / prev_active are sorted ascending id lists of
- * active_cap entries (pfc_sample's output) with their device counts n (a list
- * and its count are given together or both NULL);
+ * Each call copies the rows of n_arrays arrays (1 to PFC_BANK_MAX_ARRAYS: W,
+ * momentum and the master if any) at once: array a is a byte copy of
+ * row_bytes[a] per row (a multiple of 16, at most 65536; d * 2 for 16-bit W,
+ * d * 4 for momentum and the master) between banks[a] and slots[a] (or
+ * prev_slots[a] and next_slots[a]); the three pointer / size arrays are host
+ * arrays of n_arrays entries, each pointer non-NULL, a source never equal to
+ * its destination.  active / next_active / prev_active are sorted ascending
+ * id lists of active_cap entries (pfc_sample's output) with their device
+ * counts n (a list and its count are given together or both NULL);
  * entries past the count are ignored, and counts are clamped to [0, cap].
  * Slots are [active_cap x row] device buffers.  Bank pointers (and
  * bank_version) must be host memory allocated pinned and mapped (hipHostMalloc,
  * or torch's pin_memory) or device memory; anything else - pageable host memory
  * in particular - is PFC_ERR_INVALID_ARG, checked before any launch.
  *
- * Versions (optional, pass both or neither, on one of a step's stage calls):
+ * Versions (optional, pass both or neither):
  * bank_version int32[C] (host, pinned) holds the version of each bank row's
  * last write-back; row_version int32[C] (device) the version of each row's
  * last staging, starting from all zeros on both sides.  stage stamps
  * row_version[c] = version for every c in S(t+1), and a cold row whose
  * bank_version differs from its row_version (an update of it not yet written
  * back) adds 1 to stale[0]; writeback stamps bank_version[c] = version after
- * the row's data.  Ids outside [0, C) are not copied and also add 1 to stale.
+ * the row's data in every array has reached the bank.  Ids outside [0, C)
+ * are not copied and also add 1 to stale.
  * stale (device int32[1]) may be NULL.  A caller uses version = t + 1 for the
  * rows of step t.
  */
-int pfc_bank_stage(const void* bank, int64_t C, int64_t row_bytes,
+#define PFC_BANK_MAX_ARRAYS 3
+int pfc_bank_stage(int n_arrays, const void* const* banks /*host array*/,
+                   void* const* slots /*host array*/,
+                   const int64_t* row_bytes /*host array*/, int64_t C,
                    const int32_t* next_active, const int32_t* next_n,
                    const int32_t* prev_active /*or NULL*/,
                    const int32_t* prev_n /*or NULL*/,
                    const int32_t* prev2_active /*or NULL*/,
                    const int32_t* prev2_n /*or NULL*/, int64_t active_cap,
-                   void* slot, const int32_t* bank_version /*host, or NULL*/,
+                   const int32_t* bank_version /*host, or NULL*/,
                    int32_t* row_version /*or NULL*/, int32_t version,
                    int32_t* stale /*or NULL*/, void* stream);
-int pfc_bank_patch(const void* prev_slot, const int32_t* prev_active,
-                   const int32_t* prev_n, const int32_t* next_active,
-                   const int32_t* next_n, int64_t active_cap, int64_t row_bytes,
-                   void* next_slot, void* stream);
-int pfc_bank_writeback(const void* slot, const int32_t* active,
-                       const int32_t* n_active,
+int pfc_bank_patch(int n_arrays, const void* const* prev_slots /*host array*/,
+                   void* const* next_slots /*host array*/,
+                   const int64_t* row_bytes /*host array*/,
+                   const int32_t* prev_active, const int32_t* prev_n,
+                   const int32_t* next_active, const int32_t* next_n,
+                   int64_t active_cap, void* stream);
+int pfc_bank_writeback(int n_arrays, const void* const* slots /*host array*/,
+                       void* const* banks /*host array*/,
+                       const int64_t* row_bytes /*host array*/,
+                       const int32_t* active, const int32_t* n_active,
                        const int32_t* next_active /*or NULL*/,
                        const int32_t* next_n /*or NULL*/, int64_t active_cap,
-                       int64_t row_bytes, int64_t C, void* bank,
-                       int32_t* bank_version /*host, or NULL*/, int32_t version,
-                       void* stream);
+                       int64_t C, int32_t* bank_version /*host, or NULL*/,
+                       int32_t version, void* stream);
 
 #ifdef __cplusplus
 }

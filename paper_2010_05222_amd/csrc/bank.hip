@@ -3,7 +3,8 @@
 // for the step (Sec. 3.3.3, the paragraph on asynchronous hierarchical class
 // storage, and Fig. async_pipeline).
 //
-// Three row copies, 16 bytes per lane, eight rows per wave at a time:
+// Three row copies, each moving every array of the bank (W, momentum, the
+// master if any) for its rows in one launch, 16 bytes per lane:
 //  - stage:     cold rows of S(t+1) - those in neither of the (up to two)
 //               previous active sets still held in slots - from the bank
 //               into the next slot, with a check of the per-row versions
@@ -15,13 +16,19 @@
 //               except rows the next step also holds (its write-back carries
 //               their newer values).
 // The host side of each copy goes over the host link with ordinary vector
-// loads and stores on the mapped pinned pages; the device side is HBM.
-// Membership in S(t) is a binary search over its sorted id list.  The two
-// host-link copies run on a fixed grid of 2048 waves that walks the rows, with
-// all eight loads of a group issued before its stores: they wait on the host
-// link most of the time, and a grid of one wave per row would hold the CUs
-// and starve the step's kernels running beside them on other streams.  The
-// patch, a device-to-device copy, takes one wave per group of rows.
+// loads and stores on the mapped pinned pages; the device side is HBM.  One
+// launch per row set and direction, rather than one per array, keeps rows of
+// every size on both directions of the link at once: a 1 KB-row write-back
+// beside a 2 KB-row stage measured well below the two together.
+// Membership in S(t) is a binary search over its sorted id list, one row per
+// lane: a wave settles 64 rows in one search's worth of dependent loads, then
+// copies them eight at a time (a row per lane, and a search per row, made
+// each wave spend most of its time in dependent loads rather than on the
+// link).  The two host-link copies run on a fixed grid of 2048 waves that
+// walks the rows: they wait on the host link most of the time, and a grid of
+// one wave per 64 rows would hold the CUs and starve the step's kernels
+// running beside them on other streams.  The patch, a device-to-device copy,
+// takes one wave per 64 rows.
 #include "pfc_device.h"
 #include "pfc.h"
 
@@ -32,16 +39,21 @@ constexpr int kBankWaves = 4;     // waves per workgroup
 constexpr int kBankGrid = 512;    // workgroups of a copy
 constexpr int64_t kMaxRowBytes = 1 << 16;
 
-// Index of v in the ascending a[0, n), or -1.
+// Index of v in the ascending a[0, n), or -1; each lane looks up its own v.
+// The number of steps depends on n only (a branch-free lower bound), so the
+// lanes of a wave run their searches side by side: a wave settles the rows
+// of 64 lanes in one search's worth of dependent loads.
 __device__ __forceinline__ int64_t find_sorted(const int32_t* __restrict__ a, int64_t n,
                                                int32_t v) {
-  int64_t lo = 0, hi = n;
-  while (lo < hi) {
-    const int64_t mid = (lo + hi) >> 1;
-    if (a[mid] < v) lo = mid + 1;
-    else hi = mid;
+  if (n <= 0) return -1;
+  int64_t base = 0, len = n;
+  while (len > 1) {
+    const int64_t half = len >> 1;   // base + half < base + len <= n
+    base = a[base + half] < v ? base + half : base;
+    len -= half;
   }
-  return (lo < n && a[lo] == v) ? lo : -1;
+  const int64_t i = base + (a[base] < v ? 1 : 0);
+  return (i < n && a[i] == v) ? i : -1;
 }
 
 __device__ __forceinline__ int64_t rows_of(const int32_t* n_p, int64_t cap) {
@@ -54,124 +66,116 @@ __device__ __forceinline__ int64_t wave_index() {
 }
 __device__ __forceinline__ int64_t wave_count() { return (int64_t)gridDim.x * kBankWaves; }
 
-// A wave copies kGroup rows at a time: all their loads are issued before the
-// first store, so a wave keeps kGroup x 1 KB in flight on the host link.
+// A wave settles the rows of its 64 lanes (lane l: row j0 + l of the list
+// it walks) and then copies them kGroup at a time, array after array: all
+// loads of a pass over kGroup rows are issued before the first store, so a
+// wave keeps kGroup x 1 KB in flight on the host link.
 constexpr int kGroup = 8;
 
-struct RowGroup {
-  const uint4* src[kGroup];
-  uint4* dst[kGroup];
-  bool ok[kGroup];
+// The arrays a call copies (W, momentum, master: up to kMaxArrays), each with
+// rows of row16[a] 16-byte pieces.  One launch moves every array of a row
+// set, so both directions of the host link carry all row sizes at once.
+constexpr int kMaxArrays = PFC_BANK_MAX_ARRAYS;
+struct Arrays {
+  const uint4* src[kMaxArrays];
+  uint4* dst[kMaxArrays];
+  int row16[kMaxArrays];
+  int n;
 };
 
-__device__ __forceinline__ void copy_group(const RowGroup& g, int row16, int lane) {
-  for (int i = lane; i < row16; i += 64) {
-    uint4 v[kGroup];
+__device__ __forceinline__ int64_t lane_value(int64_t v, int l) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)v >> 32), l);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// Copies the rows the lanes hold: lane l's row, when bit l of ok is set, goes
+// from source row srow to destination row drow (both held by lane l).
+__device__ __forceinline__ void copy_rows(const Arrays& ar, uint64_t ok, int64_t srow,
+                                          int64_t drow, int lane) {
+#pragma unroll 1
+  for (int s0 = 0; s0 < 64; s0 += kGroup) {
+    const uint32_t m = (uint32_t)(ok >> s0) & ((1u << kGroup) - 1);
+    if (m == 0) continue;
+    int64_t sr[kGroup], dr[kGroup];
 #pragma unroll
-    for (int k = 0; k < kGroup; ++k)
-      if (g.ok[k]) v[k] = g.src[k][i];
+    for (int k = 0; k < kGroup; ++k) {
+      sr[k] = lane_value(srow, s0 + k);
+      dr[k] = lane_value(drow, s0 + k);
+    }
+    for (int a = 0; a < ar.n; ++a) {
+      const int row16 = ar.row16[a];
+      const uint4* __restrict__ src = ar.src[a];
+      uint4* __restrict__ dst = ar.dst[a];
+      for (int i = lane; i < row16; i += 64) {
+        uint4 v[kGroup];
 #pragma unroll
-    for (int k = 0; k < kGroup; ++k)
-      if (g.ok[k]) g.dst[k][i] = v[k];
+        for (int k = 0; k < kGroup; ++k)
+          if ((m >> k) & 1) v[k] = src[sr[k] * row16 + i];
+#pragma unroll
+        for (int k = 0; k < kGroup; ++k)
+          if ((m >> k) & 1) dst[dr[k] * row16 + i] = v[k];
+      }
+    }
   }
 }
 
 __global__ void __launch_bounds__(64 * kBankWaves) k_bank_stage(
-    const uint4* __restrict__ bank, int64_t C, int row16, const int32_t* __restrict__ next_active,
+    Arrays ar, int64_t C, const int32_t* __restrict__ next_active,
     const int32_t* __restrict__ next_n, const int32_t* __restrict__ prev_active,
     const int32_t* __restrict__ prev_n, const int32_t* __restrict__ prev2_active,
-    const int32_t* __restrict__ prev2_n, int64_t cap, uint4* __restrict__ slot,
+    const int32_t* __restrict__ prev2_n, int64_t cap,
     const int32_t* __restrict__ bank_version, int32_t* __restrict__ row_version,
     int32_t version, int32_t* __restrict__ stale) {
   const int lane = threadIdx.x & 63;
   const int64_t n = rows_of(next_n, cap);
   const int64_t np = prev_active ? rows_of(prev_n, cap) : 0;
   const int64_t np2 = prev2_active ? rows_of(prev2_n, cap) : 0;
-  for (int64_t j0 = wave_index() * kGroup; j0 < n; j0 += wave_count() * kGroup) {
-    RowGroup g;
-    int32_t cls[kGroup];
-#pragma unroll
-    for (int k = 0; k < kGroup; ++k) {
-      const int64_t j = j0 + k;
-      cls[k] = -1;
-      g.ok[k] = false;
-      g.src[k] = bank;
-      g.dst[k] = slot;
-      if (j >= n) continue;
-      const int32_t c = next_active[j];
-      if (c < 0 || c >= C) {   // not a row of the bank: nothing is copied
-        if (lane == 0 && stale) atomicAdd(stale, 1);
-        continue;
-      }
-      cls[k] = c;
-      const bool overlap = (np > 0 && find_sorted(prev_active, np, c) >= 0) ||
-                           (np2 > 0 && find_sorted(prev2_active, np2, c) >= 0);
-      if (overlap) continue;
-      if (row_version && lane == 0 && bank_version[c] != row_version[c] && stale)
-        atomicAdd(stale, 1);
-      g.ok[k] = true;
-      g.src[k] = bank + (int64_t)c * row16;
-      g.dst[k] = slot + j * row16;
-    }
-    copy_group(g, row16, lane);
-    if (row_version && lane == 0) {
-#pragma unroll
-      for (int k = 0; k < kGroup; ++k)
-        if (cls[k] >= 0) row_version[cls[k]] = version;
-    }
+  for (int64_t j0 = wave_index() * 64; j0 < n; j0 += wave_count() * 64) {
+    const int64_t j = j0 + lane;
+    const int32_t c = j < n ? next_active[j] : -1;
+    const bool in_bank = c >= 0 && c < C;
+    const bool bad = j < n && !in_bank;   // not a row of the bank: nothing is copied
+    const bool overlap = find_sorted(prev_active, np, c) >= 0 || find_sorted(prev2_active, np2, c) >= 0;
+    const bool cold = in_bank && !overlap;
+    bool behind = false;
+    if (row_version && cold) behind = bank_version[c] != row_version[c];
+    const uint64_t ok = __ballot(cold);
+    const int n_stale = __popcll(__ballot(bad)) + __popcll(__ballot(behind));
+    if (stale && lane == 0 && n_stale > 0) atomicAdd(stale, n_stale);
+    copy_rows(ar, ok, cold ? c : 0, j, lane);
+    if (row_version && in_bank) row_version[c] = version;
   }
 }
 
 __global__ void __launch_bounds__(64 * kBankWaves) k_bank_patch(
-    const uint4* __restrict__ prev_slot, const int32_t* __restrict__ prev_active,
-    const int32_t* __restrict__ prev_n, const int32_t* __restrict__ next_active,
-    const int32_t* __restrict__ next_n, int64_t cap, int row16, uint4* __restrict__ next_slot) {
+    Arrays ar, const int32_t* __restrict__ prev_active, const int32_t* __restrict__ prev_n,
+    const int32_t* __restrict__ next_active, const int32_t* __restrict__ next_n, int64_t cap) {
   const int lane = threadIdx.x & 63;
   const int64_t n = rows_of(next_n, cap), np = rows_of(prev_n, cap);
-  for (int64_t j0 = wave_index() * kGroup; j0 < n; j0 += wave_count() * kGroup) {
-    RowGroup g;
-#pragma unroll
-    for (int k = 0; k < kGroup; ++k) {
-      const int64_t j = j0 + k;
-      const int64_t i = j < n ? find_sorted(prev_active, np, next_active[j]) : -1;
-      g.ok[k] = i >= 0;
-      g.src[k] = i >= 0 ? prev_slot + i * row16 : prev_slot;
-      g.dst[k] = i >= 0 ? next_slot + j * row16 : next_slot;
-    }
-    copy_group(g, row16, lane);
+  for (int64_t j0 = wave_index() * 64; j0 < n; j0 += wave_count() * 64) {
+    const int64_t j = j0 + lane;
+    const int64_t i = find_sorted(prev_active, np, j < n ? next_active[j] : -1);
+    copy_rows(ar, __ballot(j < n && i >= 0), i >= 0 ? i : 0, j, lane);
   }
 }
 
 __global__ void __launch_bounds__(64 * kBankWaves) k_bank_writeback(
-    const uint4* __restrict__ slot, const int32_t* __restrict__ active,
-    const int32_t* __restrict__ n_active, const int32_t* __restrict__ next_active,
-    const int32_t* __restrict__ next_n, int64_t cap, int row16, int64_t C,
-    uint4* __restrict__ bank, int32_t* __restrict__ bank_version, int32_t version) {
+    Arrays ar, const int32_t* __restrict__ active, const int32_t* __restrict__ n_active,
+    const int32_t* __restrict__ next_active, const int32_t* __restrict__ next_n, int64_t cap,
+    int64_t C, int32_t* __restrict__ bank_version, int32_t version) {
   const int lane = threadIdx.x & 63;
   const int64_t n = rows_of(n_active, cap);
   const int64_t nn = next_active ? rows_of(next_n, cap) : 0;
-  for (int64_t j0 = wave_index() * kGroup; j0 < n; j0 += wave_count() * kGroup) {
-    RowGroup g;
-    int32_t cls[kGroup];
-#pragma unroll
-    for (int k = 0; k < kGroup; ++k) {
-      const int64_t j = j0 + k;
-      const int32_t c = j < n ? active[j] : -1;
-      const bool ok = c >= 0 && c < C && !(nn > 0 && find_sorted(next_active, nn, c) >= 0);
-      cls[k] = ok ? c : -1;
-      g.ok[k] = ok;
-      g.src[k] = ok ? slot + j * row16 : slot;
-      g.dst[k] = ok ? bank + (int64_t)c * row16 : bank;
-    }
-    copy_group(g, row16, lane);
+  for (int64_t j0 = wave_index() * 64; j0 < n; j0 += wave_count() * 64) {
+    const int64_t j = j0 + lane;
+    const int32_t c = j < n ? active[j] : -1;
+    const bool ok = c >= 0 && c < C && find_sorted(next_active, nn, c) < 0;
+    copy_rows(ar, __ballot(ok), j, ok ? c : 0, lane);
     if (bank_version) {
-      // The rows' data reach system scope before their versions do.
+      // Every array's row reaches system scope before the row's version does.
       __threadfence_system();
-      if (lane == 0) {
-#pragma unroll
-        for (int k = 0; k < kGroup; ++k)
-          if (cls[k] >= 0) bank_version[cls[k]] = version;
-      }
+      if (ok) bank_version[c] = version;
     }
   }
 }
@@ -189,9 +193,32 @@ bool device_accessible(const void* p) {
   return false;
 }
 
-int common_checks(int64_t row_bytes, int64_t active_cap) {
-  if (row_bytes < 16 || row_bytes > kMaxRowBytes || row_bytes % 16 != 0) return PFC_ERR_INVALID_ARG;
+int common_checks(int64_t active_cap) {
   if (active_cap < 1 || active_cap > PFC_MAX_CLASSES) return PFC_ERR_INVALID_ARG;
+  return PFC_OK;
+}
+
+// The arrays of a call: n in [1, PFC_BANK_MAX_ARRAYS], every pointer given and
+// reachable from the device, row sizes multiples of 16 up to kMaxRowBytes.
+int take_arrays(int n, const void* const* src, void* const* dst, const int64_t* row_bytes,
+                Arrays* ar) {
+  if (n < 1 || n > kMaxArrays || !src || !dst || !row_bytes) return PFC_ERR_INVALID_ARG;
+  *ar = Arrays{};
+  ar->n = n;
+  for (int a = 0; a < n; ++a) {
+    const int64_t rb = row_bytes[a];
+    if (!src[a] || !dst[a] || src[a] == dst[a]) return PFC_ERR_INVALID_ARG;
+    if (rb < 16 || rb > kMaxRowBytes || rb % 16 != 0) return PFC_ERR_INVALID_ARG;
+    ar->src[a] = (const uint4*)src[a];
+    ar->dst[a] = (uint4*)dst[a];
+    ar->row16[a] = (int)(rb / 16);
+  }
+  return PFC_OK;
+}
+
+int arrays_accessible(const Arrays& ar) {
+  for (int a = 0; a < ar.n; ++a)
+    if (!device_accessible(ar.src[a]) || !device_accessible(ar.dst[a])) return PFC_ERR_INVALID_ARG;
   return PFC_OK;
 }
 
@@ -205,7 +232,7 @@ int device_present() {
 }
 
 unsigned grid_of(int64_t cap) {
-  const int64_t g = ceil_div(cap, kBankWaves);
+  const int64_t g = ceil_div(cap, 64 * kBankWaves);
   return (unsigned)(g < kBankGrid ? g : kBankGrid);
 }
 
@@ -216,69 +243,72 @@ using namespace pfc;
 
 extern "C" {
 
-int pfc_bank_stage(const void* bank, int64_t C, int64_t row_bytes, const int32_t* next_active,
+int pfc_bank_stage(int n_arrays, const void* const* banks, void* const* slots,
+                   const int64_t* row_bytes, int64_t C, const int32_t* next_active,
                    const int32_t* next_n, const int32_t* prev_active, const int32_t* prev_n,
                    const int32_t* prev2_active, const int32_t* prev2_n, int64_t active_cap,
-                   void* slot, const int32_t* bank_version, int32_t* row_version,
-                   int32_t version, int32_t* stale, void* stream) {
-  if (!bank || !next_active || !next_n || !slot) return PFC_ERR_INVALID_ARG;
+                   const int32_t* bank_version, int32_t* row_version, int32_t version,
+                   int32_t* stale, void* stream) {
+  if (!next_active || !next_n) return PFC_ERR_INVALID_ARG;
   if (C < 1 || C > PFC_MAX_CLASSES) return PFC_ERR_INVALID_ARG;
   if ((prev_active == nullptr) != (prev_n == nullptr)) return PFC_ERR_INVALID_ARG;
   if ((prev2_active == nullptr) != (prev2_n == nullptr)) return PFC_ERR_INVALID_ARG;
   if ((bank_version == nullptr) != (row_version == nullptr)) return PFC_ERR_INVALID_ARG;
-  const int st = common_checks(row_bytes, active_cap);
+  Arrays ar;
+  int st = take_arrays(n_arrays, banks, slots, row_bytes, &ar);
+  if (st == PFC_OK) st = common_checks(active_cap);
   if (st != PFC_OK) return st;
   const int dv = device_present();
   if (dv != PFC_OK) return dv;
-  if (!device_accessible(bank) || !device_accessible(slot)) return PFC_ERR_INVALID_ARG;
+  if (arrays_accessible(ar) != PFC_OK) return PFC_ERR_INVALID_ARG;
   if (bank_version && !device_accessible(bank_version)) return PFC_ERR_INVALID_ARG;
   (void)hipGetLastError();
   hipLaunchKernelGGL(k_bank_stage, dim3(grid_of(active_cap)), dim3(64 * kBankWaves), 0,
-                     (hipStream_t)stream, (const uint4*)bank, C, (int)(row_bytes / 16),
-                     next_active, next_n, prev_active, prev_n, prev2_active, prev2_n,
-                     active_cap, (uint4*)slot,
-                     bank_version, row_version, version, stale);
+                     (hipStream_t)stream, ar, C, next_active, next_n, prev_active, prev_n,
+                     prev2_active, prev2_n, active_cap, bank_version, row_version, version,
+                     stale);
   return hipGetLastError() == hipSuccess ? PFC_OK : PFC_ERR_HIP;
 }
 
-int pfc_bank_patch(const void* prev_slot, const int32_t* prev_active, const int32_t* prev_n,
+int pfc_bank_patch(int n_arrays, const void* const* prev_slots, void* const* next_slots,
+                   const int64_t* row_bytes, const int32_t* prev_active, const int32_t* prev_n,
                    const int32_t* next_active, const int32_t* next_n, int64_t active_cap,
-                   int64_t row_bytes, void* next_slot, void* stream) {
-  if (!prev_slot || !prev_active || !prev_n || !next_active || !next_n || !next_slot)
-    return PFC_ERR_INVALID_ARG;
-  if (prev_slot == next_slot) return PFC_ERR_INVALID_ARG;
-  const int st = common_checks(row_bytes, active_cap);
+                   void* stream) {
+  if (!prev_active || !prev_n || !next_active || !next_n) return PFC_ERR_INVALID_ARG;
+  Arrays ar;
+  int st = take_arrays(n_arrays, prev_slots, next_slots, row_bytes, &ar);
+  if (st == PFC_OK) st = common_checks(active_cap);
   if (st != PFC_OK) return st;
   const int dv = device_present();
   if (dv != PFC_OK) return dv;
-  if (!device_accessible(prev_slot) || !device_accessible(next_slot)) return PFC_ERR_INVALID_ARG;
+  if (arrays_accessible(ar) != PFC_OK) return PFC_ERR_INVALID_ARG;
   (void)hipGetLastError();
   // A device-to-device copy: enough waves for every group of rows at once.
-  hipLaunchKernelGGL(k_bank_patch, dim3((unsigned)ceil_div(active_cap, kGroup * kBankWaves)),
-                     dim3(64 * kBankWaves), 0,
-                     (hipStream_t)stream, (const uint4*)prev_slot, prev_active, prev_n,
-                     next_active, next_n, active_cap, (int)(row_bytes / 16), (uint4*)next_slot);
+  hipLaunchKernelGGL(k_bank_patch, dim3((unsigned)ceil_div(active_cap, 64 * kBankWaves)),
+                     dim3(64 * kBankWaves), 0, (hipStream_t)stream, ar, prev_active, prev_n,
+                     next_active, next_n, active_cap);
   return hipGetLastError() == hipSuccess ? PFC_OK : PFC_ERR_HIP;
 }
 
-int pfc_bank_writeback(const void* slot, const int32_t* active, const int32_t* n_active,
+int pfc_bank_writeback(int n_arrays, const void* const* slots, void* const* banks,
+                       const int64_t* row_bytes, const int32_t* active, const int32_t* n_active,
                        const int32_t* next_active, const int32_t* next_n, int64_t active_cap,
-                       int64_t row_bytes, int64_t C, void* bank, int32_t* bank_version,
-                       int32_t version, void* stream) {
-  if (!slot || !active || !n_active || !bank) return PFC_ERR_INVALID_ARG;
+                       int64_t C, int32_t* bank_version, int32_t version, void* stream) {
+  if (!active || !n_active) return PFC_ERR_INVALID_ARG;
   if ((next_active == nullptr) != (next_n == nullptr)) return PFC_ERR_INVALID_ARG;
   if (C < 1 || C > PFC_MAX_CLASSES) return PFC_ERR_INVALID_ARG;
-  const int st = common_checks(row_bytes, active_cap);
+  Arrays ar;
+  int st = take_arrays(n_arrays, slots, banks, row_bytes, &ar);
+  if (st == PFC_OK) st = common_checks(active_cap);
   if (st != PFC_OK) return st;
   const int dv = device_present();
   if (dv != PFC_OK) return dv;
-  if (!device_accessible(bank) || !device_accessible(slot)) return PFC_ERR_INVALID_ARG;
+  if (arrays_accessible(ar) != PFC_OK) return PFC_ERR_INVALID_ARG;
   if (bank_version && !device_accessible(bank_version)) return PFC_ERR_INVALID_ARG;
   (void)hipGetLastError();
   hipLaunchKernelGGL(k_bank_writeback, dim3(grid_of(active_cap)), dim3(64 * kBankWaves), 0,
-                     (hipStream_t)stream, (const uint4*)slot, active, n_active, next_active,
-                     next_n, active_cap,
-                     (int)(row_bytes / 16), C, (uint4*)bank, bank_version, version);
+                     (hipStream_t)stream, ar, active, n_active, next_active, next_n, active_cap,
+                     C, bank_version, version);
   return hipGetLastError() == hipSuccess ? PFC_OK : PFC_ERR_HIP;
 }
 

@@ -106,17 +106,18 @@ class TieredShard:
     tensors the caller fills).  Each step runs on a device slot of `cap` rows
     holding only its active rows; `n_slots` slots (2 or 3) are used in turn.
     While step t runs on its slot (current stream), an upload stream samples
-    step t+1 and stages its cold rows into the next slot; rows that S(t+1)
-    shares with S(t) (and, with three slots, with S(t-1)) are patched from
-    those slots once their steps have updated them, and a download stream
-    writes each slot back to the bank after its step.  HIP events order the
-    three streams:
+    step t+1; after step t it stages the cold rows of S(t+1) into the next
+    slot.  Rows that S(t+1) shares with S(t) (and, with three slots, with
+    S(t-1)) are patched from those slots once their steps have updated them,
+    and a download stream writes each slot back to the bank after its step.
+    HIP events order the three streams:
       upload(t+1)   after download(t+1-n_slots)  (the slot and its id lists are
-                    free, and every bank row it may read is current)
-      patch(t-1 -> t+1), then patch(t -> t+1) after step t  (the newest copy wins)
+                    free, and every bank row it may read is current); its
+                    sampling and patch(t-1 -> t+1) beside step t, its stage
+                    and patch(t -> t+1) after step t (the newest copy wins)
       download(t)   after step t and the sampling of step t+1, whose rows it
                     leaves to download(t+1)
-      step t+1      after its patches
+      step t+1      after its stage and patches
     With three slots the upload of step t+1 need not wait for the download of
     step t-1, so the two directions of the host link run at once.  Every copy
     is a libpfc kernel.
@@ -171,39 +172,37 @@ class TieredShard:
     def _row_bytes(self, key):
         return self.d * self.banks[key].element_size()
 
+    def _keys(self, slot):
+        return [k for k in ("M", "P", "W") if k in slot]
+
     def _stage(self, nxt, prevs, slot, version):
-        stream = self.up.cuda_stream
+        # One launch moves the cold rows of every array; it checks and stamps
+        # the versions.
         pv = [(_ptr(q.active), _ptr(q.n_active)) for q in prevs] + [(0, 0)] * (2 - len(prevs))
-        for key in ("M", "P", "W"):
-            if key not in slot:
-                continue
-            ver = key == "W"
-            abi.pfc_bank_stage(_ptr(self.banks[key]), self.C, self._row_bytes(key),
-                               _ptr(nxt.active), _ptr(nxt.n_active), pv[0][0], pv[0][1],
-                               pv[1][0], pv[1][1], self.cap, _ptr(slot[key]),
-                               _ptr(self.bank_version) if ver else 0,
-                               _ptr(self.row_version) if ver else 0, version,
-                               _ptr(self.stale) if ver else 0, stream)
+        keys = self._keys(slot)
+        abi.pfc_bank_stage([_ptr(self.banks[k]) for k in keys], [_ptr(slot[k]) for k in keys],
+                           [self._row_bytes(k) for k in keys], self.C, _ptr(nxt.active),
+                           _ptr(nxt.n_active), pv[0][0], pv[0][1], pv[1][0], pv[1][1], self.cap,
+                           _ptr(self.bank_version), _ptr(self.row_version), version,
+                           _ptr(self.stale), self.up.cuda_stream)
 
     def _patch(self, prv, src, nxt, dst):
-        for key in src:
-            abi.pfc_bank_patch(_ptr(src[key]), _ptr(prv.active), _ptr(prv.n_active),
-                               _ptr(nxt.active), _ptr(nxt.n_active), self.cap,
-                               self._row_bytes(key), _ptr(dst[key]), self.up.cuda_stream)
+        keys = self._keys(src)
+        abi.pfc_bank_patch([_ptr(src[k]) for k in keys], [_ptr(dst[k]) for k in keys],
+                           [self._row_bytes(k) for k in keys], _ptr(prv.active),
+                           _ptr(prv.n_active), _ptr(nxt.active), _ptr(nxt.n_active), self.cap,
+                           self.up.cuda_stream)
 
     def _writeback(self, part, slot, version, nxt):
-        # The W rows go last and stamp the version, so a stamped row's
-        # momentum (and master) rows are already in the bank.  Rows the next
-        # step holds are left to its write-back.
+        # One launch writes every array's rows back; a row's version is
+        # stamped after all of its arrays have reached the bank.  Rows the
+        # next step holds are left to its write-back.
         na, nn = (_ptr(nxt.active), _ptr(nxt.n_active)) if nxt else (0, 0)
-        for key in ("M", "P", "W"):
-            if key not in slot:
-                continue
-            abi.pfc_bank_writeback(_ptr(slot[key]), _ptr(part.active), _ptr(part.n_active), na,
-                                   nn, self.cap, self._row_bytes(key), self.C,
-                                   _ptr(self.banks[key]),
-                                   _ptr(self.bank_version) if key == "W" else 0, version,
-                                   self.down.cuda_stream)
+        keys = self._keys(slot)
+        abi.pfc_bank_writeback([_ptr(slot[k]) for k in keys], [_ptr(self.banks[k]) for k in keys],
+                               [self._row_bytes(k) for k in keys], _ptr(part.active),
+                               _ptr(part.n_active), na, nn, self.cap, self.C,
+                               _ptr(self.bank_version), version, self.down.cuda_stream)
 
     def _run_step(self, part, X, slot):
         _require(X, part.tdtype, (self.B, self.d), "X", self.device)
@@ -226,24 +225,23 @@ class TieredShard:
         ev.record(torch.cuda.current_stream(self.device))
         return ev
 
-    def _upload(self, k, prevs, labels, seed, version):
-        """Sample a step into parts[k] and stage its cold rows into slot k."""
+    def _sample_into(self, k, labels, seed):
+        """Sample a step into parts[k] on the upload stream, once slot k is free."""
         self.up.wait_event(self._mark_main())          # labels were made on the current stream
         if self.written[k] is not None:
             self.up.wait_event(self.written[k])
-        part = self.parts[k]
         sampled = torch.cuda.Event()
         with torch.cuda.stream(self.up):
-            part.sample(labels, seed)
+            self.parts[k].sample(labels, seed)
             sampled.record(self.up)
-            self._stage(part, prevs, self.slots[k], version)
         labels.record_stream(self.up)
         return sampled
 
     def begin(self, labels, seed):
         """Samples step 0 and stages all of its rows."""
         self.t = 0
-        self._upload(0, [], labels, seed, 1)
+        self._sample_into(0, labels, seed)
+        self._stage(self.parts[0], [], self.slots[0], 1)
         self.ready[0].record(self.up)
         self.staged = [False] * self.n
         self.staged[0] = True
@@ -260,8 +258,7 @@ class TieredShard:
         older = self.parts[z] if (n >= 3 and t >= 1) else None
         sampled = None
         if labels_next is not None:
-            sampled = self._upload(b, [cur] + ([older] if older else []), labels_next,
-                                   seed_next, t + 2)
+            sampled = self._sample_into(b, labels_next, seed_next)
             if older:
                 # Step t-1 is done: the upload stream waited for it before the
                 # previous patch.
@@ -271,7 +268,11 @@ class TieredShard:
         self._run_step(cur, X, self.slots[a])
         done = self._mark_main()
         if labels_next is not None:
+            # The cold rows go up after the step: a copy kernel beside the
+            # step's kernels finds few free CUs and moves little, while it
+            # slows them down.
             self.up.wait_event(done)
+            self._stage(nxt, [cur] + ([older] if older else []), self.slots[b], t + 2)
             self._patch(cur, self.slots[a], nxt, self.slots[b])
             self.ready[b].record(self.up)
             self.staged[b] = True

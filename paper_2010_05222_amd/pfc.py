@@ -66,12 +66,12 @@ _lib.pfc_timing_begin.argtypes = [_int, _int]
 _lib.pfc_timing_begin.restype = _int
 _lib.pfc_timing_end.argtypes = [ctypes.POINTER(_dbl), ctypes.POINTER(_int)]
 _lib.pfc_timing_end.restype = _int
-_lib.pfc_bank_stage.argtypes = [_vp, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _vp, _vp,
-                                _vp, ctypes.c_int32, _vp, _vp]
+_lib.pfc_bank_stage.argtypes = [_int, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _i64,
+                                _vp, _vp, ctypes.c_int32, _vp, _vp]
 _lib.pfc_bank_stage.restype = _int
-_lib.pfc_bank_patch.argtypes = [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _vp, _vp]
+_lib.pfc_bank_patch.argtypes = [_int, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _vp]
 _lib.pfc_bank_patch.restype = _int
-_lib.pfc_bank_writeback.argtypes = [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp,
+_lib.pfc_bank_writeback.argtypes = [_int, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _vp,
                                     ctypes.c_int32, _vp]
 _lib.pfc_bank_writeback.restype = _int
 
@@ -139,21 +139,35 @@ def pfc_timing_end():
     return ms.value, n.value
 
 
-def pfc_bank_stage(bank, C, row_bytes, next_active, next_n, prev_active, prev_n, prev2_active,
-                   prev2_n, active_cap, slot, bank_version, row_version, version, stale, stream):
-    _check(_lib.pfc_bank_stage(bank, C, row_bytes, next_active, next_n, prev_active, prev_n,
-                               prev2_active, prev2_n, active_cap, slot, bank_version,
-                               row_version, version, stale, stream), "pfc_bank_stage")
+def _bank_arrays(src, dst, row_bytes):
+    """Host arrays of the per-array pointers and row sizes of a bank copy
+    (equal-length sequences of ints); kept alive by the caller's frame."""
+    n = len(src)
+    if len(dst) != n or len(row_bytes) != n:
+        raise ValueError("bank copy: pointer and row-size lists of different lengths")
+    return (n, (ctypes.c_void_p * max(n, 1))(*src), (ctypes.c_void_p * max(n, 1))(*dst),
+            (ctypes.c_int64 * max(n, 1))(*row_bytes))
 
 
-def pfc_bank_patch(prev_slot, prev_active, prev_n, next_active, next_n, active_cap, row_bytes,
-                   next_slot, stream):
-    _check(_lib.pfc_bank_patch(prev_slot, prev_active, prev_n, next_active, next_n, active_cap,
-                               row_bytes, next_slot, stream), "pfc_bank_patch")
+def pfc_bank_stage(banks, slots, row_bytes, C, next_active, next_n, prev_active, prev_n,
+                   prev2_active, prev2_n, active_cap, bank_version, row_version, version, stale,
+                   stream):
+    n, b, s, rb = _bank_arrays(banks, slots, row_bytes)
+    _check(_lib.pfc_bank_stage(n, b, s, rb, C, next_active, next_n, prev_active, prev_n,
+                               prev2_active, prev2_n, active_cap, bank_version, row_version,
+                               version, stale, stream), "pfc_bank_stage")
 
 
-def pfc_bank_writeback(slot, active, n_active, next_active, next_n, active_cap, row_bytes, C,
-                       bank, bank_version, version, stream):
-    _check(_lib.pfc_bank_writeback(slot, active, n_active, next_active, next_n, active_cap,
-                                   row_bytes, C, bank, bank_version, version, stream),
+def pfc_bank_patch(prev_slots, next_slots, row_bytes, prev_active, prev_n, next_active, next_n,
+                   active_cap, stream):
+    n, p, q, rb = _bank_arrays(prev_slots, next_slots, row_bytes)
+    _check(_lib.pfc_bank_patch(n, p, q, rb, prev_active, prev_n, next_active, next_n,
+                               active_cap, stream), "pfc_bank_patch")
+
+
+def pfc_bank_writeback(slots, banks, row_bytes, active, n_active, next_active, next_n,
+                       active_cap, C, bank_version, version, stream):
+    n, s, b, rb = _bank_arrays(slots, banks, row_bytes)
+    _check(_lib.pfc_bank_writeback(n, s, b, rb, active, n_active, next_active, next_n,
+                                   active_cap, C, bank_version, version, stream),
            "pfc_bank_writeback")

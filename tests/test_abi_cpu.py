@@ -166,20 +166,25 @@ def test_backward_rejects_before_launch(kw, status):
 
 
 def _stage_args(**kw):
-    a = dict(bank=FAKE, C=1000, row_bytes=256, next_active=FAKE, next_n=FAKE, prev_active=0,
-             prev_n=0, prev2_active=0, prev2_n=0, active_cap=100, slot=FAKE, bank_version=0,
-             row_version=0, version=1, stale=0, stream=0)
+    a = dict(banks=[FAKE], slots=[FAKE + 16], row_bytes=[256], C=1000, next_active=FAKE,
+             next_n=FAKE, prev_active=0, prev_n=0, prev2_active=0, prev2_n=0, active_cap=100,
+             bank_version=0, row_version=0, version=1, stale=0, stream=0)
     a.update(kw)
     return a
 
 
 @pytest.mark.parametrize("kw", [
-    dict(bank=0), dict(slot=0), dict(next_active=0), dict(next_n=0),
-    dict(C=0), dict(row_bytes=8), dict(row_bytes=24), dict(row_bytes=1 << 17),
+    dict(banks=[0]), dict(slots=[0]), dict(next_active=0), dict(next_n=0),
+    dict(C=0), dict(row_bytes=[8]), dict(row_bytes=[24]), dict(row_bytes=[1 << 17]),
     dict(active_cap=0),
     dict(prev_active=FAKE),                   # a previous list without its count
     dict(prev2_n=FAKE),
     dict(bank_version=FAKE),                  # versions come in pairs
+    dict(banks=[], slots=[], row_bytes=[]),   # no array
+    dict(banks=[FAKE] * 4, slots=[FAKE + 16] * 4, row_bytes=[256] * 4),   # more than three
+    dict(banks=[FAKE, 0], slots=[FAKE + 16, FAKE + 32], row_bytes=[256, 512]),
+    dict(banks=[FAKE, FAKE + 48], slots=[FAKE + 16, FAKE + 32], row_bytes=[256, 0]),
+    dict(slots=[FAKE]),                       # a bank copied onto itself
 ])
 def test_bank_stage_rejects_before_launch(kw):
     with pytest.raises(pfc.PfcError) as e:
@@ -187,26 +192,33 @@ def test_bank_stage_rejects_before_launch(kw):
     assert e.value.status == pfc.PFC_ERR_INVALID_ARG
 
 
+def test_bank_array_lists_must_match():
+    with pytest.raises(ValueError):
+        pfc.pfc_bank_stage(**_stage_args(row_bytes=[256, 512]))
+
+
 @pytest.mark.parametrize("kw", [
-    dict(prev_slot=0), dict(next_slot=0), dict(prev_active=0), dict(next_n=0),
-    dict(next_slot=FAKE), dict(row_bytes=0),
+    dict(prev_slots=[0]), dict(next_slots=[0]), dict(prev_active=0), dict(next_n=0),
+    dict(next_slots=[FAKE]), dict(row_bytes=[0]),
+    dict(prev_slots=[], next_slots=[], row_bytes=[]),
 ])
 def test_bank_patch_rejects_before_launch(kw):
-    a = dict(prev_slot=FAKE + 16, prev_active=FAKE, prev_n=FAKE, next_active=FAKE, next_n=FAKE,
-             active_cap=100, row_bytes=256, next_slot=FAKE + 32, stream=0)
-    if kw.get("next_slot") == FAKE:
-        kw = dict(prev_slot=FAKE, next_slot=FAKE)           # a slot patched onto itself
-    a.update(kw)
+    a = dict(prev_slots=[FAKE], next_slots=[FAKE + 32], row_bytes=[256], prev_active=FAKE,
+             prev_n=FAKE, next_active=FAKE, next_n=FAKE, active_cap=100, stream=0)
+    a.update(kw)                              # next_slots=[FAKE]: a slot patched onto itself
     with pytest.raises(pfc.PfcError) as e:
         pfc.pfc_bank_patch(**a)
     assert e.value.status == pfc.PFC_ERR_INVALID_ARG
 
 
-@pytest.mark.parametrize("kw", [dict(slot=0), dict(bank=0), dict(C=-1), dict(row_bytes=100),
-                                dict(next_active=FAKE)])
+@pytest.mark.parametrize("kw", [dict(slots=[0]), dict(banks=[0]), dict(C=-1),
+                                dict(row_bytes=[100]), dict(next_active=FAKE),
+                                dict(slots=[FAKE] * 4, banks=[FAKE + 16] * 4,
+                                     row_bytes=[256] * 4)])
 def test_bank_writeback_rejects_before_launch(kw):
-    a = dict(slot=FAKE, active=FAKE, n_active=FAKE, next_active=0, next_n=0, active_cap=100,
-             row_bytes=256, C=1000, bank=FAKE, bank_version=0, version=1, stream=0)
+    a = dict(slots=[FAKE], banks=[FAKE + 16], row_bytes=[256], active=FAKE, n_active=FAKE,
+             next_active=0, next_n=0, active_cap=100, C=1000, bank_version=0, version=1,
+             stream=0)
     a.update(kw)
     with pytest.raises(pfc.PfcError) as e:
         pfc.pfc_bank_writeback(**a)

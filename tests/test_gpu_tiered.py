@@ -231,12 +231,12 @@ def test_bank_rejects_pageable_memory(dev):
     ids = torch.arange(cap, dtype=torch.int32, device=dev)
     n = torch.full((1,), cap, dtype=torch.int32, device=dev)
     with pytest.raises(pfc.PfcError) as e:
-        pfc.pfc_bank_stage(pageable.data_ptr(), 1000, d * 4, ids.data_ptr(), n.data_ptr(), 0, 0,
-                           0, 0, cap, slot.data_ptr(), 0, 0, 1, 0, 0)
+        pfc.pfc_bank_stage([pageable.data_ptr()], [slot.data_ptr()], [d * 4], 1000,
+                           ids.data_ptr(), n.data_ptr(), 0, 0, 0, 0, cap, 0, 0, 1, 0, 0)
     assert e.value.status == pfc.PFC_ERR_INVALID_ARG
     with pytest.raises(pfc.PfcError) as e:
-        pfc.pfc_bank_writeback(slot.data_ptr(), ids.data_ptr(), n.data_ptr(), 0, 0, cap, d * 4,
-                               1000, pageable.data_ptr(), 0, 1, 0)
+        pfc.pfc_bank_writeback([slot.data_ptr()], [pageable.data_ptr()], [d * 4],
+                               ids.data_ptr(), n.data_ptr(), 0, 0, cap, 1000, 0, 1, 0)
     assert e.value.status == pfc.PFC_ERR_INVALID_ARG
     torch.cuda.synchronize()
 
