@@ -70,6 +70,9 @@ def roofline_entry(name, cfg, K, avg_ms, traffic):
         entry = {"bound": "mfma", "achieved": achieved, "peak": peak_tf, "unit": "TFLOP/s"}
     entry["frac"] = entry["achieved"] / entry["peak"]
     entry["traffic"] = traffic
+    # The HBM rate the counters imply (every byte the kernel moves, its own
+    # intermediates included), next to the algorithmic rate above.
+    entry["traffic_GBps"] = traffic / sec / 1e9 if traffic else None
     entry["kernel"] = name
     entry["avg_ms"] = avg_ms
     return entry

@@ -30,6 +30,9 @@ def test_roofline_and_gather_entries(bench, name):
     nbytes = cm.update_bytes(K, cfg["d"], cfg["dtype"], cfg["master"])
     if dw["bound"] == "hbm":
         assert dw["achieved"] == pytest.approx(nbytes / 2e-3 / 1e9)
+    assert dw["traffic_GBps"] is None
+    dwt = bench.roofline_entry("dw_update", cfg, K, 2.0, 3.0e9)
+    assert dwt["traffic"] == 3.0e9 and dwt["traffic_GBps"] == pytest.approx(1500.0)
     g = bench.gather_entry(cfg, K, stage_ms, None)
     elt = cm.DTYPE_BYTES[cfg["dtype"]]
     assert g["bytes"] == K * cfg["d"] * elt
