@@ -458,11 +458,14 @@ __global__ void __launch_bounds__(256) k_scales(const float* __restrict__ gmax,
 
 // Sum the split partials of a row in split order, add the row's target term
 // g_t * W[S_t] / ||w_t||, and apply the normalisation backward:
-// dx = (dX_hat - x_hat (x_hat . dX_hat)) / ||x||, dX_hat = (s/B) * sum.
+// dx = (dX_hat - x_hat (x_hat . dX_hat)) / ||x||, dX_hat = (s/B) * sum.  A
+// mapped label outside [0, |S|) counts as unowned: no target term, and no
+// row of W or of the id list is read for it.
 template <typename Tag>
 __global__ void __launch_bounds__(256) k_dx_final(
     const float* __restrict__ dx_part, int n_split, const void* __restrict__ X,
     const void* __restrict__ W, const int32_t* __restrict__ active,
+    const int32_t* __restrict__ n_active_p,
     const int32_t* __restrict__ yhat, const float* __restrict__ row_lse,
     const float* __restrict__ inv_x, const float* __restrict__ inv_w,
     const float* __restrict__ tgtc, int B, int d, Margin mg, float sB, float* __restrict__ dX) {
@@ -472,7 +475,8 @@ __global__ void __launch_bounds__(256) k_dx_final(
   const int n = blockIdx.x;
   const int t = threadIdx.x, lane = t & 63;
   const float ix = inv_x[n];
-  const int yt = yhat[n];
+  const int K = *n_active_p;
+  const int yt = yhat[n] < K ? yhat[n] : -1;
   float gt = 0.0f;
   int64_t wbase = 0;
   if (yt >= 0) {
@@ -1226,8 +1230,8 @@ void launch_bwd16(const StepArgs& a, const StepWs& w, const Margin& mg, float sB
   timing_stop(4, stream);
   timing_start(5, stream);
   hipLaunchKernelGGL(k_dx_final<Tag>, dim3((unsigned)B), dim3(256), 0, stream,
-                     w.dx_part, w.n_split, a.X, a.W, a.active, a.labels_mapped, a.row_lse,
-                     w.inv_x, w.inv_w, w.tgtc, B, (int)a.d, mg, sB, a.dX);
+                     w.dx_part, w.n_split, a.X, a.W, a.active, a.n_active, a.labels_mapped,
+                     a.row_lse, w.inv_x, w.inv_w, w.tgtc, B, (int)a.d, mg, sB, a.dX);
   timing_stop(5, stream);
   timing_start(6, stream);
   if (a.W_master)

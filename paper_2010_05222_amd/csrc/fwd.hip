@@ -334,7 +334,7 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
   for (int nb = 0; nb < 2; ++nb) {
     const int n = n0 + 64 * wn + 32 * nb + l32;
     ixr[nb] = n < B ? inv_x[n] : 0.0f;
-    yhr[nb] = n < B ? yhat[n] : -1;
+    yhr[nb] = n < B && yhat[n] < K ? yhat[n] : -1;   // past |S|: unowned
   }
 
   float wss[4] = {0.0f, 0.0f, 0.0f, 0.0f};  // partial ||w||^2 of the lane's class rows
@@ -496,7 +496,8 @@ __global__ void __launch_bounds__(256) k_lse16(const float2* __restrict__ stats,
     sm = (red[0] + red[1]) + (red[2] + red[3]);
     const float lse = (mx + log2f(sm)) * 0.6931471805599453f;
     row_lse[n] = lse;
-    loss_part[n] = yhat[n] >= 0 ? lse - tgt[n] : 0.0f;
+    const int yh = yhat[n];
+    loss_part[n] = yh >= 0 && yh < *n_active_p ? lse - tgt[n] : 0.0f;   // past |S|: unowned
   }
 }
 
@@ -552,7 +553,7 @@ __global__ void __launch_bounds__(256) k_lse32(const float* __restrict__ cos32, 
   if (lane == 0) {
     const float lse = acc.x + __logf(acc.y);
     row_lse[n] = lse;
-    loss_part[n] = yh >= 0 ? lse - ft : 0.0f;
+    loss_part[n] = yh >= 0 && yh < K ? lse - ft : 0.0f;
   }
 }
 

@@ -544,13 +544,17 @@ __global__ void k_remap(const int64_t* labels, int64_t B, int64_t C, int64_t a,
     return;
   }
   const int32_t c = (int32_t)(y - a);
-  int32_t lo = 0, hi = *n_active;  // first index with active[idx] >= c
+  const int32_t k = *n_active;
+  int32_t lo = 0, hi = k;  // first index with active[idx] >= c
   while (lo < hi) {
     const int32_t mid = lo + ((hi - lo) >> 1);
     if (active[mid] < c) lo = mid + 1;
     else hi = mid;
   }
-  labels_mapped[n] = lo;
+  // Every in-shard label is a positive, which the sampler always keeps; a
+  // label not found in S is nevertheless mapped to -1 (unowned), never to a
+  // position whose id is another class or lies past |S|.
+  labels_mapped[n] = (lo < k && active[lo] == c) ? lo : -1;
 }
 
 }  // namespace

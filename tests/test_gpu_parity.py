@@ -262,3 +262,48 @@ def test_batch_at_limit_fp32(dev):
     """The largest batch of the fp32 path (4096 rows); here |P| > b, so S = P."""
     out = _case(dev, 4096, 128, 3000, 0.5, "f32", "cosface", 0.4, seed=21)
     assert out["K"] == out["n_pos"] > 1500
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_mapped_label_past_active_set_is_unowned(dev, dtype):
+    """A labels_mapped entry at or past |S| (never produced by the sampler,
+    but accepted by the forward and backward calls) counts as an unowned
+    label: no target term and a zero loss term, as the oracle computes for a
+    label of -1.  The id list is valid past |S| here, so the call reads no
+    out-of-range class either way."""
+    from _gpu_util import make_problem, row_rel_err, MAX_ABS, REL_ROW
+    B, d, C, r, seed = 200, 128, 1000, 0.05, 41
+    labels = np.random.default_rng(41).integers(0, 30, size=B)   # 30 classes: |S| = 50 < cap
+    print(f"\ncase B={B} d={d} C={C} r={r} dtype={dtype} seed={seed} mapped label past |S|",
+          flush=True)
+    Xd, Wd, Md, Pd, Ld = make_problem(B, d, C, dtype, seed, labels=labels, device=dev)
+    shard = _shard(B, d, C, r, dtype, "arcface", 0.5, 0, dev)
+    X64 = Xd.double().cpu().numpy()
+    W0 = Wd.double().cpu().numpy()
+    M0 = Md.double().cpu().numpy()
+    shard.sample(Ld, seed)
+    torch.cuda.synchronize()
+    K = int(shard.n_active.item())
+    assert K + 5 < shard.cap, (K, shard.cap)
+    shard.active[K + 5] = 0
+    row = 7
+    shard.labels_mapped[row] = K + 5
+    shard.forward(Xd, Wd)
+    shard.backward(Xd, Wd, Md, None)
+    torch.cuda.synchronize()
+
+    active = shard.active[:K].cpu().numpy()
+    mapped = shard.labels_mapped.cpu().numpy().copy()
+    mapped[row] = -1
+    Ws = W0[active]
+    fw = O.forward(X64, Ws, mapped, shard.s, shard.m, "arcface")
+    loss_ref = O.batch_loss(fw["row_loss"], B)
+    dx_ref = O.grad_x(X64, Ws, mapped, fw["lse"], B, shard.s, shard.m, "arcface")
+    g_ref = O.grad_w(X64, Ws, np.arange(K), mapped, fw["lse"], B, shard.s, shard.m, "arcface")
+    loss = float(shard.loss.item())
+    dx = shard.dX.cpu().numpy().astype(np.float64)
+    g = Md.double().cpu().numpy()[active] - shard.mu * M0[active]
+    assert abs(loss - loss_ref) <= 1e-3 * abs(loss_ref), (loss, loss_ref)
+    assert np.max(np.abs(dx - dx_ref)) <= MAX_ABS[dtype]
+    assert np.max(row_rel_err(dx, dx_ref)) <= REL_ROW[dtype]
+    assert np.max(np.abs(g - g_ref)) <= MAX_ABS[dtype]
