@@ -134,8 +134,10 @@ int pfc_sample_noalloc(const int64_t* labels, int64_t B, int64_t C,
  * (Sec. 3.1, Eq. sampled_probability, Sec. 3.2.1).
  *
  * X       [B x d] in x_dtype;  W [C x d] in w_dtype (the persistent shard).
- * active, n_active, labels_mapped: outputs of pfc_sample for this batch; a
- *         labels_mapped entry outside [0, n_active) counts as an unowned
+ * active, n_active, labels_mapped: outputs of pfc_sample for this batch.
+ *         The kernels rely on what pfc_sample guarantees and do not check
+ *         it: n_active in [0, active_cap], active[0, n_active) ids in [0, C).
+ *         A labels_mapped entry outside [0, n_active) counts as an unowned
  *         label (no target term, loss term 0).
  * compute must equal w_dtype and x_dtype (fp32, bf16 or fp16 operands; the
  *         contraction always accumulates in fp32).
