@@ -319,6 +319,9 @@ def main():
                     help="also run a plain 1 GiB device copy (counter calibration)")
     ap.add_argument("--tiered", action="store_true",
                     help="keep the class bank in pinned host memory (staged per step)")
+    ap.add_argument("--serial", action="store_true",
+                    help="draw each step's active set in the step itself, rather than on a "
+                         "side stream beside the previous step")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -331,7 +334,7 @@ def main():
     import torch
     import workloads
     from paper_2010_05222_amd import pfc as abi
-    from paper_2010_05222_amd.head import PfcShard
+    from paper_2010_05222_amd.head import PfcPipeline
 
     cfg = workloads.config(args.workload)
     dev = torch.device("cuda:0")
@@ -344,11 +347,14 @@ def main():
 
     W, master = workloads.make_weights_device(cfg, dev)
     M = torch.zeros((C, d), dtype=torch.float32, device=dev)
-    shard = PfcShard(B, d, C, cfg["r"], dtype=cfg["dtype"], class_offset=cfg["a"], s=cfg["s"],
-                     m=cfg["m"], margin=cfg["margin"], lr=cfg["lr"], mu=cfg["mu"], device=dev)
+    pipe = PfcPipeline(B, d, C, cfg["r"], dtype=cfg["dtype"], class_offset=cfg["a"], s=cfg["s"],
+                       m=cfg["m"], margin=cfg["margin"], lr=cfg["lr"], mu=cfg["mu"], device=dev)
+    shard = pipe.parts[0]
     n_extra = args.warmup + args.kernel_steps * len(abi.KERNEL_NAMES)
     batches = []
-    for t in range(args.steps):
+    # One batch more than the timed steps: the last step draws the next active
+    # set, so the timed region holds exactly `steps` samplings either way.
+    for t in range(args.steps + 1):
         X, L = workloads.make_batch(cfg, t)
         batches.append((torch.from_numpy(X).to(tdt).to(dev), torch.from_numpy(L).to(dev), t))
     extra = []
@@ -358,15 +364,27 @@ def main():
                       10**6 + i))
     torch.cuda.synchronize()
     log(f"[bench] inputs resident: W {W.numel() * W.element_size() / 2**30:.2f} GiB, "
-        f"momentum {M.numel() * 4 / 2**30:.2f} GiB, workspace {shard.ws_bytes / 2**30:.2f} GiB")
+        f"momentum {M.numel() * 4 / 2**30:.2f} GiB, workspace 2 x "
+        f"{shard.ws_bytes / 2**30:.2f} GiB")
+
+    serial_shard = shard
 
     def run(batch):
         X, L, seed = batch
-        shard.step(X, L, W, M, seed, master)
+        serial_shard.step(X, L, W, M, seed, master)
 
     it = iter(extra)
-    for _ in range(args.warmup):
-        run(next(it))
+    if args.serial:
+        for _ in range(args.warmup):
+            run(next(it))
+    else:
+        # Warm both buffer sets of the pipeline.
+        warm = [next(it) for _ in range(args.warmup)]
+        if warm:
+            pipe.begin(warm[0][1], warm[0][2])
+            for i, (X, _, _) in enumerate(warm):
+                nxt = warm[i + 1] if i + 1 < len(warm) else None
+                pipe.step(X, W, M, nxt[1] if nxt else None, nxt[2] if nxt else None, master)
     torch.cuda.synchronize()
     log("[bench] warm-up done")
 
@@ -388,14 +406,24 @@ def main():
 
     # Timed region: exactly `steps` steps; the dominant kernel bracketed by HIP events.
     # Per-step HIP events on the step's stream give the median / p99 step time.
+    # By default step t+1's active set is drawn on a side stream beside step t
+    # (PfcPipeline): the first step's before the region, one past the last
+    # inside it.
+    timed = batches[:args.steps]
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in batches]
+          for _ in timed]
+    if not args.serial:
+        pipe.begin(batches[0][1], batches[0][2])
     abi.pfc_timing_begin(dom_id, args.steps)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for b, (e0, e1) in zip(batches, ev):
+    for t, (e0, e1) in enumerate(ev):
         e0.record()
-        run(b)
+        if args.serial:
+            run(timed[t])
+        else:
+            X, _, _ = timed[t]
+            shard = pipe.step(X, W, M, batches[t + 1][1], batches[t + 1][2], master)
         e1.record()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
@@ -473,6 +501,8 @@ def main():
                    "global_batch": B, "d": d, "C_shard": C, "r": cfg["r"], "active": K,
                    "margin": cfg["margin"], "w_dtype": cfg["dtype"], "momentum": "f32",
                    "contractions": contraction_precision(cfg["dtype"]),
+                   "sampling": ("in the step" if args.serial else
+                                "step t+1's active set drawn on a side stream beside step t"),
                    "parallelism": "one class shard on one GPU"},
         "roofline": roof,
         "cpu_baseline": cpu,

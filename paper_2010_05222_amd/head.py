@@ -97,6 +97,75 @@ class PfcShard:
         self.backward(X, W, M, W_master)
 
 
+class PfcPipeline:
+    """A training loop's steps on one resident shard, with each step's
+    sampling moved off the critical path: the active set of step t+1 depends
+    only on its labels and seed, so it is drawn on a side stream while step t
+    runs, into the second of two sets of step buffers (active set, mapped
+    labels, outputs and workspace).  Results are those of PfcShard.step, bit
+    for bit.
+
+        pipe = PfcPipeline(B, d, C, r, ...)
+        pipe.begin(labels[0], seeds[0])
+        for t in range(T):
+            out = pipe.step(X[t], W, M, labels[t + 1] if t + 1 < T else None,
+                            seeds[t + 1] if t + 1 < T else None)
+            # out.loss, out.row_lse, out.dX belong to step t (valid on the
+            # current stream until step t + 2)
+    """
+
+    def __init__(self, B, d, C, r, **kw):
+        self.parts = [PfcShard(B, d, C, r, **kw) for _ in range(2)]
+        self.device = self.parts[0].device
+        self.side = torch.cuda.Stream(device=self.device)
+        self.done = [None, None]    # event: the last step that used each buffer set
+        self.ready = [False, False]
+        self.pending = [None, None]  # event: sampling into each buffer set
+        self.t = 0
+
+    def _sample(self, k, labels, seed):
+        main = torch.cuda.current_stream(self.device)
+        mark = torch.cuda.Event()
+        mark.record(main)                     # the labels were made on the current stream
+        self.side.wait_event(mark)
+        if self.done[k] is not None:
+            self.side.wait_event(self.done[k])
+        with torch.cuda.stream(self.side):
+            self.parts[k].sample(labels, seed)
+        labels.record_stream(self.side)
+        ev = torch.cuda.Event()
+        ev.record(self.side)
+        self.pending[k] = ev
+        self.ready[k] = True
+
+    def begin(self, labels, seed):
+        """Draws the active set of the first step."""
+        self.t = 0
+        self.ready = [False, False]
+        self._sample(0, labels, seed)
+
+    def step(self, X, W, M, labels_next=None, seed_next=None, W_master=None):
+        """Step t on the current stream (its sampling was drawn by the previous
+        call, or by begin()); step t+1's sampling is drawn beside it."""
+        a, b = self.t % 2, (self.t + 1) % 2
+        if not self.ready[a]:
+            raise RuntimeError("PfcPipeline.step: no active set drawn (call begin(), and pass "
+                               "the next step's labels to every step but the last)")
+        self.ready[a] = False
+        main = torch.cuda.current_stream(self.device)
+        main.wait_event(self.pending[a])
+        if labels_next is not None:
+            self._sample(b, labels_next, seed_next)
+        cur = self.parts[a]
+        cur.forward(X, W)
+        cur.backward(X, W, M, W_master)
+        ev = torch.cuda.Event()
+        ev.record(main)
+        self.done[a] = ev
+        self.t += 1
+        return cur
+
+
 class TieredShard:
     """A class shard whose bank lives in pinned host memory (Sec. 3.3.3, the
     paragraph on asynchronous hierarchical class storage, Fig. async_pipeline).

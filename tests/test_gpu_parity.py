@@ -307,3 +307,36 @@ def test_mapped_label_past_active_set_is_unowned(dev, dtype):
     assert np.max(np.abs(dx - dx_ref)) <= MAX_ABS[dtype]
     assert np.max(row_rel_err(dx, dx_ref)) <= REL_ROW[dtype]
     assert np.max(np.abs(g - g_ref)) <= MAX_ABS[dtype]
+
+
+def test_pipeline_equals_serial_steps(dev):
+    """PfcPipeline (each step's active set drawn on a side stream beside the
+    previous step) gives the serial steps' loss, row_lse, dX, W and momentum
+    bit for bit over four steps with different batches and seeds."""
+    from paper_2010_05222_amd.head import PfcPipeline
+    from _gpu_util import make_problem
+    B, d, C, r, T = 96, 256, 5000, 0.1, 4
+    print(f"\ncase B={B} d={d} C={C} r={r} bf16 pipeline vs serial, {T} steps", flush=True)
+    Xd, Wd, Md, _, _ = make_problem(B, d, C, "bf16", 51, device=dev)
+    rng = np.random.default_rng(52)
+    Ls = [torch.from_numpy(rng.integers(0, C, size=B)).to(dev) for _ in range(T)]
+    Xs = [torch.roll(Xd, 7 * t, 0).contiguous() for t in range(T)]
+    W1, M1, W2, M2 = Wd.clone(), Md.clone(), Wd.clone(), Md.clone()
+    shard = _shard(B, d, C, r, "bf16", "arcface", 0.5, 0, dev)
+    serial = []
+    for t in range(T):
+        shard.step(Xs[t], Ls[t], W1, M1, 100 + t)
+        serial.append((shard.loss.clone(), shard.row_lse.clone(), shard.dX.clone()))
+    pipe = PfcPipeline(B, d, C, r, dtype="bf16", s=64.0, m=0.5, margin="arcface", lr=0.1,
+                       mu=0.9, device=dev)
+    pipe.begin(Ls[0], 100)
+    for t in range(T):
+        last = t + 1 == T
+        out = pipe.step(Xs[t], W2, M2, None if last else Ls[t + 1], None if last else 101 + t)
+        got = (out.loss.clone(), out.row_lse.clone(), out.dX.clone())
+        for a, b in zip(got, serial[t]):
+            assert torch.equal(a, b), t
+    torch.cuda.synchronize()
+    assert torch.equal(W1, W2) and torch.equal(M1, M2)
+    with pytest.raises(RuntimeError):
+        pipe.step(Xs[0], W2, M2)          # no active set drawn for a fifth step
