@@ -319,6 +319,9 @@ def main():
                     help="also run a plain 1 GiB device copy (counter calibration)")
     ap.add_argument("--tiered", action="store_true",
                     help="keep the class bank in pinned host memory (staged per step)")
+    ap.add_argument("--tau", type=float, default=None,
+                    help="PFC* conflict threshold (a negative whose cosine exceeds it leaves "
+                         "the row's denominator); default: plain PFC")
     ap.add_argument("--serial", action="store_true",
                     help="draw each step's active set in the step itself, rather than on a "
                          "side stream beside the previous step")
@@ -348,7 +351,8 @@ def main():
     W, master = workloads.make_weights_device(cfg, dev)
     M = torch.zeros((C, d), dtype=torch.float32, device=dev)
     pipe = PfcPipeline(B, d, C, cfg["r"], dtype=cfg["dtype"], class_offset=cfg["a"], s=cfg["s"],
-                       m=cfg["m"], margin=cfg["margin"], lr=cfg["lr"], mu=cfg["mu"], device=dev)
+                       m=cfg["m"], margin=cfg["margin"], lr=cfg["lr"], mu=cfg["mu"], device=dev,
+                       tau=args.tau)
     shard = pipe.parts[0]
     n_extra = args.warmup + args.kernel_steps * len(abi.KERNEL_NAMES)
     batches = []
@@ -501,6 +505,7 @@ def main():
                    "global_batch": B, "d": d, "C_shard": C, "r": cfg["r"], "active": K,
                    "margin": cfg["margin"], "w_dtype": cfg["dtype"], "momentum": "f32",
                    "contractions": contraction_precision(cfg["dtype"]),
+                   "tau": args.tau,
                    "sampling": ("in the step" if args.serial else
                                 "step t+1's active set drawn on a side stream beside step t"),
                    "parallelism": "one class shard on one GPU"},
