@@ -3,33 +3,38 @@
 // target margin and the row-wise log-sum-exp cross-entropy over S
 // (Sec. 3.1, Eq. sampled_probability; max / sum decomposition of Sec. 3.2.1).
 //
-// 16-bit path: one MFMA GEMM workgroup per 256 active classes (MFMA M) x 128
-// batch rows (MFMA N), d streamed in 32-wide chunks through a three-stage
-// direct-to-LDS ring; two workgroups share a CU.  Classes sit on the MFMA M
-// axis so that each lane holds one batch row and 64 of its classes: the row
+// 16-bit path: one MFMA GEMM workgroup per 128 active classes (MFMA M, one
+// 128-class group of the logit store) x 256 batch rows (MFMA N), d streamed
+// in 32-wide chunks through a three-stage direct-to-LDS ring; two workgroups
+// share a CU.  A stage holds 8 KB of gathered W rows (64-byte pieces of 128
+// different rows) and 16 KB of batch rows (one contiguous run): of the two
+// operands the gathered one moves fewer bytes, as its short pieces cost the
+// L2 more per byte than the contiguous run.  Classes sit on the MFMA M axis
+// so that each lane holds one batch row and 64 of its classes: the row
 // max / sum-exp of the epilogue is mostly in-register.  The epilogue scales
 // by 1/||x_n|| and 1/||w_j|| (the class-row norms are summed from the
 // contraction's own class fragments), applies the margin at the target and
 // the optional PFC* conflict filter, and writes each logit once, as its fp16
 // softmax numerator E = 2^(f - m) relative to the maximum m of its row and
-// 128-class group (the tile is assembled in the idle LDS ring and stored as
-// whole rows), with one (max, sum E) pair per (row, class tile).  A small
+// 128-class group, the tile's (the tile is assembled in the idle LDS ring
+// and stored as whole rows), with one (max, sum E) pair per (row, class
+// tile).  A small
 // kernel merges the pairs into lse_n and the loss.
 #include "pfc_gemm.h"
 
 namespace pfc {
 namespace {
 
-constexpr int kFwdBM = 256;       // classes per tile (MFMA M)
-constexpr int kFwdBN = 128;       // batch rows per tile (MFMA N)
+constexpr int kFwdBM = 128;       // classes per tile (MFMA M): one 128-class group
+constexpr int kFwdBN = 256;       // batch rows per tile (MFMA N)
 constexpr int kFwdKC = 32;        // slice of d per pipeline stage
-constexpr int kFwdThreads = 256;  // 4 waves: 2 (classes) x 2 (rows), 128 x 64 each
+constexpr int kFwdThreads = 256;  // 4 waves, one per 64 batch rows, 128 classes x 64 each
 constexpr int kFwdStageA = kFwdBM * kFwdKC;  // uint16 elements per stage, class operand
 constexpr int kFwdStageB = kFwdBN * kFwdKC;  // uint16 elements per stage, batch operand
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kEpsNormW = 1e-12f;  // ||w|| floor of the normalisation
 
-// Three-stage LDS ring per operand (24 KB per stage; 75 KB in all, so two
+// Three-stage LDS ring per operand (24 KB per stage; 72 KB in all, so two
 // workgroups share a CU and one's epilogue overlaps the other's MFMA loop).
 // One array per stage, so the compiler can keep the direct-to-LDS loads of
 // later stages in flight while a stage is read.  Row r of a stage holds 32
@@ -40,7 +45,7 @@ __shared__ __attribute__((aligned(1024))) uint16_t fA0[kFwdStageA], fA1[kFwdStag
     fA2[kFwdStageA];
 __shared__ __attribute__((aligned(1024))) uint16_t fB0[kFwdStageB], fB1[kFwdStageB],
     fB2[kFwdStageB];
-__shared__ float2 fRed[2][kFwdBN];
+__shared__ float2 fRed[1][kFwdBN];
 __shared__ __attribute__((aligned(16))) float fIw[kFwdBM];
 __shared__ float fNrm[2][kFwdBM];
 
@@ -57,28 +62,29 @@ __device__ __forceinline__ uint16_t* fwd_b() {
   else return fB2;
 }
 
-// Row r (0..127) of the epilogue's cosine tile, rows of 256 elements: rows
-// 0..95 in the class-operand stages (32 each), 96..127 in two batch-operand
-// stages (16 each).
+// Row r (0..255) of the epilogue's cosine tile, rows of 128 elements: rows
+// 0..95 in the class-operand stages (32 each), 96..255 in the batch-operand
+// stages (64 each).  Every caller's r >> 5 is wave-uniform.
 __device__ __forceinline__ uint16_t* fwd_tile_row(int r) {
   uint16_t* base;
   if (r < 32) base = fA0 + r * kFwdBM;
   else if (r < 64) base = fA1 + (r - 32) * kFwdBM;
   else if (r < 96) base = fA2 + (r - 64) * kFwdBM;
-  else if (r < 112) base = fB0 + (r - 96) * kFwdBM;
-  else base = fB1 + (r - 112) * kFwdBM;
+  else if (r < 160) base = fB0 + (r - 96) * kFwdBM;
+  else if (r < 224) base = fB1 + (r - 160) * kFwdBM;
+  else base = fB2 + (r - 224) * kFwdBM;
   return base;
 }
 
-// DMA of one stage: class operand rows 16 (4 wave + u) + lane / 4 (u < 4),
-// batch operand rows 16 (2 wave + u) + lane / 4 (u < 2).
+// DMA of one stage: class operand rows 16 (2 wave + u) + lane / 4 (u < 2),
+// batch operand rows 16 (4 wave + u) + lane / 4 (u < 4).
 template <int S>
-__device__ __forceinline__ void fwd_issue(const uint16_t* const ap[4], const uint16_t* const bp[2],
+__device__ __forceinline__ void fwd_issue(const uint16_t* const ap[2], const uint16_t* const bp[4],
                                           int k0, int64_t kb, int wave) {
 #pragma unroll
-  for (int u = 0; u < 4; ++u) dma16(ap[u] + k0, fwd_a<S>() + (4 * wave + u) * 16 * kFwdKC);
+  for (int u = 0; u < 2; ++u) dma16(ap[u] + k0, fwd_a<S>() + (2 * wave + u) * 16 * kFwdKC);
 #pragma unroll
-  for (int u = 0; u < 2; ++u) dma16(bp[u] + kb, fwd_b<S>() + (2 * wave + u) * 16 * kFwdKC);
+  for (int u = 0; u < 4; ++u) dma16(bp[u] + kb, fwd_b<S>() + (4 * wave + u) * 16 * kFwdKC);
 }
 
 // a0^2 + a1^2 + acc for a packed pair of 16-bit values (v_dot2_f32_*).
@@ -268,14 +274,14 @@ __device__ __forceinline__ void fwd_epilogue_rows_plain(f32x16_t (&acc)[4][2], i
   *sm_out = sm;
 }
 
-// Tile: 256 active classes x 128 batch rows, the whole of d (= 32 * NK).
+// Tile: 128 active classes x 256 batch rows, the whole of d (= 32 * NK).
 // Epilogue, per (row, class): c = acc / (||x|| ||w||) and the base-2 logit
 // s c log2 e (the margined logit at the target, which also goes to tgt[n],
-// its cosine to tgtc[n]); per (row, 128-class group) the maximum m, written
-// to gmax, and E = 2^(f - m) in fp16; per (row, class tile) the pair
-// (max, sum E), merged by k_lse16.  The batch operand comes from the
-// column-blocked copy of X (block k = [ld_xb][32]), so a stage's 128 batch
-// rows are one contiguous 8 KB run.
+// its cosine to tgtc[n]); per row the tile's maximum m (the row's reference
+// for this 128-class group), written to gmax, and E = 2^(f - m) in fp16, and
+// the pair (m, sum E), merged by k_lse16.  The batch operand comes from the
+// column-blocked copy of X (block k = [ld_xb][32]), so a stage's 256 batch
+// rows are one contiguous 16 KB run.
 template <typename Tag, int NK, bool FILT>
 __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
     const uint16_t* __restrict__ Xb, int64_t ld_xb, const uint16_t* __restrict__ W,
@@ -298,23 +304,23 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
   const int n0 = rt * kFwdBN;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = 0, wn = wave;   // every wave: all 128 classes, its 64 batch rows
   const int half = lane >> 5, l32 = lane & 31;
 
   // Per-lane source rows of the DMA segments; rows past the end are clamped
   // to a valid row (their results are masked in the epilogue).
   const int cidx = (lane & 3) ^ ((lane >> 4) & 3);
-  const uint16_t* ap[4];
-  const uint16_t* bp[2];
+  const uint16_t* ap[2];
+  const uint16_t* bp[4];
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int row = 16 * (4 * wave + u) + (lane >> 2);
+  for (int u = 0; u < 2; ++u) {
+    const int row = 16 * (2 * wave + u) + (lane >> 2);
     const int64_t jr = j0 + row < K ? j0 + row : K - 1;
     ap[u] = W + (int64_t)active[jr] * D + 8 * cidx;
   }
 #pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int row = 16 * (2 * wave + u) + (lane >> 2);
+  for (int u = 0; u < 4; ++u) {
+    const int row = 16 * (4 * wave + u) + (lane >> 2);
     const int nr = n0 + row < B ? n0 + row : B - 1;
     bp[u] = Xb + (int64_t)nr * kFwdKC + 8 * cidx;
   }
@@ -361,22 +367,24 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb) {
       const float s = wss[mb] + __shfl_xor(wss[mb], 32, 64);
-      if (half == 0) fNrm[wn][128 * wm + 32 * mb + l32] = s;
+      if (half == 0 && wn < 2) fNrm[wn][128 * wm + 32 * mb + l32] = s;
     }
     wait_lgkm0();
     stage_barrier();
-    const float inv = 1.0f / fmaxf(sqrtf(fNrm[0][tid] + fNrm[1][tid]), kEpsNormW);
-    fIw[tid] = inv;
-    if (rt == 0) {
-      const bool jok = j0 + tid < (int64_t)K;
-      inv_w[j0 + tid] = jok ? inv : 0.0f;
-      const float m = wave_max(jok ? inv : 0.0f);
-      if (lane == 0) atomicMax(reinterpret_cast<int*>(inv_w_max), __float_as_int(m));
+    if (tid < kFwdBM) {   // waves 0 and 1: one class each
+      const float inv = 1.0f / fmaxf(sqrtf(fNrm[0][tid] + fNrm[1][tid]), kEpsNormW);
+      fIw[tid] = inv;
+      if (rt == 0) {
+        const bool jok = j0 + tid < (int64_t)K;
+        inv_w[j0 + tid] = jok ? inv : 0.0f;
+        const float m = wave_max(jok ? inv : 0.0f);
+        if (lane == 0) atomicMax(reinterpret_cast<int*>(inv_w_max), __float_as_int(m));
+      }
     }
   }
 
-  // ---- epilogue.  The fp16 256-class x 128-row tile of E values is
-  // assembled in the (now idle) LDS ring (rows of 512 B, 16-byte block b of
+  // ---- epilogue.  The fp16 128-class x 256-row tile of E values is
+  // assembled in the (now idle) LDS ring (rows of 256 B, 16-byte block b of
   // row r at position b ^ (r & 15): conflict-free writes from the MFMA layout
   // and reads along rows), then written out in whole rows.
   wait_lgkm0();
@@ -398,8 +406,8 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
     const int n = n0 + nl;
     if (half == 0) {
       fRed[wm][nl] = make_float2(mx, sm);
-      // reference of the row's 128-class group 2 ct + wm
-      if (n < B) gmax[(2 * ct + wm) * ld_g + n] = mx == -INFINITY ? 0.0f : mx;
+      // reference of the row's 128-class group, the tile's
+      if (n < B) gmax[ct * ld_g + n] = mx == -INFINITY ? 0.0f : mx;
     }
   };
   // Two separate paths over both row blocks, so that the masking work of
@@ -433,68 +441,65 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
   }
   wait_lgkm0();
   stage_barrier();
-  // Wave w writes rows 32 w .. 32 w + 31, two rows (2 x 512 B) per store;
+  // Wave w writes rows 64 w .. 64 w + 63, four rows (4 x 256 B) per store;
   // all of its LDS reads are issued before the first store.  The stores are
   // non-temporal: the logit store is read back only by later kernels, after
   // gigabytes of other traffic, so it should not take L2 space from the
   // operands this kernel re-reads.
   {
-    const int b = lane & 31;
+    const int b = lane & 15;
     u32x4_t v[16];
     static_for<0, 16>([&](auto ii) {
       constexpr int i = decltype(ii)::value;
-      const int r = 32 * wave + 2 * i + (lane >> 5);
+      const int r = 64 * wave + 4 * i + (lane >> 4);
       ds_read_128<0>(v[i], lds_addr(fwd_tile_row(r) + 8 * (b ^ (r & 15))));
     });
     lgkm_wait<0>(v);
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      const int r = 32 * wave + 2 * i + (lane >> 5);
+      const int r = 64 * wave + 4 * i + (lane >> 4);
       const int n = n0 + r;
       if (n < B)
         __builtin_nontemporal_store(
             v[i], reinterpret_cast<u32x4_t*>(lbuf + (int64_t)n * ld_cos + j0 + 8 * b));
     }
   }
-  if (tid < kFwdBN) {
-    const int n = n0 + tid;
-    if (n < B) stats[(int64_t)n * n_ctiles + ct] = lse_merge2(fRed[0][tid], fRed[1][tid]);
+  for (int r = tid; r < kFwdBN; r += kFwdThreads) {
+    const int n = n0 + r;
+    if (n < B) stats[(int64_t)n * n_ctiles + ct] = fRed[0][r];
   }
 }
 
 // Merge the per-tile (max, sum) pairs of a row: lse_n, and the row's loss
-// term.  One workgroup per row: the row maximum M over the tiles, then
-// sum_tiles sum_t * 2^(max_t - M), each a fixed-order reduction.
+// term.  One workgroup per row, one pass over the row's pairs: each thread
+// merges its pairs in tile order (base 2), the waves' pairs meet through
+// lane moves and LDS in a fixed order.
 __global__ void __launch_bounds__(256) k_lse16(const float2* __restrict__ stats, int64_t n_ctiles,
                                                const int32_t* __restrict__ n_active_p,
                                                const int32_t* __restrict__ yhat,
                                                const float* __restrict__ tgt, int B,
                                                float* __restrict__ row_lse,
                                                float* __restrict__ loss_part) {
-  __shared__ float red[4];
+  __shared__ float2 red[4];
   const int n = blockIdx.x;
   const int t = threadIdx.x, lane = t & 63;
   const int64_t nct = ceil_div((int64_t)*n_active_p, (int64_t)kFwdBM);
   const float2* row = stats + (int64_t)n * n_ctiles;
-  float mx = -INFINITY;
-  for (int64_t c = t; c < nct; c += 256) mx = fmaxf(mx, row[c].x);
-  mx = wave_max(mx);
-  if (lane == 0) red[t >> 6] = mx;
-  __syncthreads();
-  mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-  __syncthreads();
-  float sm = 0.0f;
-  if (mx != -INFINITY)
-    for (int64_t c = t; c < nct; c += 256) {
-      const float2 v = row[c];
-      sm += v.y * exp2f(v.x - mx);
-    }
-  sm = wave_sum(sm);
-  if (lane == 0) red[t >> 6] = sm;
+  float2 acc = make_float2(-INFINITY, 0.0f);
+  for (int64_t c = t; c < nct; c += 256) acc = lse_merge2(acc, row[c]);
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    float2 o;
+    o.x = __shfl_xor(acc.x, off, 64);
+    o.y = __shfl_xor(acc.y, off, 64);
+    acc = lse_merge2(acc, o);
+  }
+  if (lane == 0) red[t >> 6] = acc;
   __syncthreads();
   if (t == 0) {
-    sm = (red[0] + red[1]) + (red[2] + red[3]);
-    const float lse = (mx + log2f(sm)) * 0.6931471805599453f;
+    acc = lse_merge2(lse_merge2(red[0], red[1]), lse_merge2(red[2], red[3]));
+    const float lse = acc.x == -INFINITY ? -INFINITY
+                                         : (acc.x + log2f(acc.y)) * 0.6931471805599453f;
     row_lse[n] = lse;
     const int yh = yhat[n];
     loss_part[n] = yh >= 0 && yh < *n_active_p ? lse - tgt[n] : 0.0f;   // past |S|: unowned

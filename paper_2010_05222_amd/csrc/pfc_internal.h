@@ -45,7 +45,7 @@ struct SampleWs {
 // ----------------------------------------------------------------- step
 
 // Class tile of the forward contraction (one softmax-statistics pair per row and tile).
-constexpr int kFwdClassTile = 256;
+constexpr int kFwdClassTile = 128;
 // Class group of the logit store: the forward keeps one base-2 reference per
 // (row, group of 128 active classes).
 constexpr int kLogitGroup = 128;
