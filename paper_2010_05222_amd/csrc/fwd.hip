@@ -486,7 +486,17 @@ __global__ void __launch_bounds__(256) k_lse16(const float2* __restrict__ stats,
   const int64_t nct = ceil_div((int64_t)*n_active_p, (int64_t)kFwdBM);
   const float2* row = stats + (int64_t)n * n_ctiles;
   float2 acc = make_float2(-INFINITY, 0.0f);
-  for (int64_t c = t; c < nct; c += 256) acc = lse_merge2(acc, row[c]);
+  // Eight loads in flight per thread, merged in tile order.
+  for (int64_t c0 = t; c0 < nct; c0 += 256 * 8) {
+    float2 v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int64_t c = c0 + 256 * k;
+      v[k] = c < nct ? row[c] : make_float2(-INFINITY, 0.0f);
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc = lse_merge2(acc, v[k]);
+  }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) {
     float2 o;
