@@ -40,7 +40,7 @@ typedef enum {
   PFC_OK = 0,
   PFC_ERR_INVALID_ARG = 1,  /* a size, pointer or hyper-parameter is out of range */
   PFC_ERR_CAPACITY = 2,     /* active_cap smaller than the largest possible |S| */
-  PFC_ERR_WORKSPACE = 3,    /* ws is NULL or smaller than required */
+  PFC_ERR_WORKSPACE = 3,    /* ws is NULL, not 256-byte aligned, or smaller than required */
   PFC_ERR_UNSUPPORTED = 4,  /* dtype combination not implemented */
   PFC_ERR_HIP = 5,          /* a HIP launch failed */
   PFC_ERR_SCRATCH = 6       /* larger than the static scratch of pfc_sample_noalloc */
@@ -65,7 +65,8 @@ typedef enum {
  * b = r*C when r*C is an integer (within 1e-9 relative), else ceil(r*C); the
  * active set has |S| = max(b, |P|) <= max(b, min(B, C)) classes, which is the
  * `active_cap` every other call must be given.  Also reports the workspace
- * size needed by a step with these sizes and compute dtype.
+ * size needed by a step with these sizes and compute dtype; every call that
+ * takes `ws` needs it at a 256-byte aligned device address (hipMalloc's are).
  *
  * 1 <= B <= PFC_MAX_BATCH; 1 <= C <= PFC_MAX_CLASSES; 0 < r <= 1;
  * 8 <= d <= 1024 with d a multiple of 8 (else PFC_ERR_INVALID_ARG); compute
@@ -110,7 +111,7 @@ int pfc_sample(const int64_t* labels, int64_t B, int64_t C,
  * memory (code under HIP graph capture, tight serving loops, harnesses that
  * forbid hipMalloc).  Same arguments, outputs and selection rule as
  * pfc_sample, minus ws / ws_bytes: the sampler's scratch is a file-scope
- * device array of the library, about 30 MiB on every device the library runs
+ * device array of the library, about 21 MiB on every device the library runs
  * on, held until the process ends.  Its address is looked up on the first
  * call on each device (that call must run with the device current).
  *

@@ -75,7 +75,6 @@ WsLayout ws_layout(int64_t B, int64_t d, int64_t C, int64_t cap, int compute) {
   L.off_hist = take((size_t)(1 << kTopBitsMax) * 4);
   L.off_state = take(sizeof(SampleState));
   L.off_digits = take((size_t)round_up(C, kCompactPer) * 2);   // read 16 at a time
-  L.off_cand = take((size_t)C * 4);
   L.off_cand_key = take((size_t)C * 8);
   L.off_grp_sure = take((size_t)L.n_groups * 4);
   L.off_grp_tie = take((size_t)L.n_groups * 4);
@@ -127,7 +126,6 @@ SampleWs sample_ws(void* ws, const WsLayout& L) {
   w.hist = (uint32_t*)(b + L.off_hist);
   w.state = (SampleState*)(b + L.off_state);
   w.digits = (uint16_t*)(b + L.off_digits);
-  w.cand = (uint32_t*)(b + L.off_cand);
   w.cand_key = (uint64_t*)(b + L.off_cand_key);
   w.grp_sure = (uint32_t*)(b + L.off_grp_sure);
   w.grp_tie = (uint32_t*)(b + L.off_grp_tie);
@@ -191,7 +189,7 @@ int pfc_sample(const int64_t* labels, int64_t B, int64_t C, int64_t class_offset
   if (!(isfinite(r) && r > 0.0 && r <= 1.0)) return PFC_ERR_INVALID_ARG;
   if (active_cap < cap_of(B, C, r)) return PFC_ERR_CAPACITY;
   const WsLayout L = ws_layout(B, 8, C, active_cap, PFC_F32);
-  if (!ws) return PFC_ERR_WORKSPACE;
+  if (!ws || ((uintptr_t)ws & 255) != 0) return PFC_ERR_WORKSPACE;
   if (ws_bytes < L.sample_bytes) return PFC_ERR_WORKSPACE;
   (void)hipGetLastError();
   const hipError_t e = launch_sample(labels, B, C, class_offset, budget_of(r, C), seed, L.top_bits,
@@ -215,7 +213,7 @@ int pfc_forward_loss(const void* X, int x_dtype, int64_t B, int64_t d, const voi
   if (st != PFC_OK) return st;
   if (tau != tau) return PFC_ERR_INVALID_ARG;   // NaN
   const WsLayout L = ws_layout(B, d, C, active_cap, compute_dtype);
-  if (!ws || ws_bytes < L.bytes) return PFC_ERR_WORKSPACE;
+  if (!ws || ((uintptr_t)ws & 255) != 0 || ws_bytes < L.bytes) return PFC_ERR_WORKSPACE;
   StepArgs a{};
   a.X = X;
   a.W = const_cast<void*>(W);
@@ -254,7 +252,7 @@ int pfc_backward_update(const void* X, int x_dtype, int64_t B, int64_t d, void* 
   if (st != PFC_OK) return st;
   if (!finite_pos(lr) || !isfinite(mu) || mu < 0.0f || mu >= 1.0f) return PFC_ERR_INVALID_ARG;
   const WsLayout L = ws_layout(B, d, C, active_cap, compute_dtype);
-  if (!ws || ws_bytes < L.bytes) return PFC_ERR_WORKSPACE;
+  if (!ws || ((uintptr_t)ws & 255) != 0 || ws_bytes < L.bytes) return PFC_ERR_WORKSPACE;
   StepArgs a{};
   a.X = X;
   a.W = W;

@@ -16,7 +16,6 @@ enum SampleMode : uint32_t { kSelectNone = 0, kSelectKeys = 1, kSelectAll = 2 };
 struct SampleState {
   uint32_t n_pos;       // |P|: distinct owned labels
   uint32_t mode;        // SampleMode
-  uint32_t cand_count;  // candidates collected in the threshold's top bucket
   uint32_t top_digit;   // value of the top key bits holding the threshold
   int64_t n_neg;        // max(b - |P|, 0)
   int64_t k_rem;        // keys equal to `thresh` still to take (class order)
@@ -34,10 +33,11 @@ struct SampleWs {
   uint32_t* hist;        // 2^kTopBitsMax bins
   SampleState* state;
   uint16_t* digits;      // C top-bit digits of the keys (only in kSelectKeys mode)
-  uint32_t* cand;        // C candidate class ids (worst case)
-  uint64_t* cand_key;    // their full keys
+  uint64_t* cand_key;    // C: the full keys of compaction group g's non-positive classes
+                         // in the threshold's top bucket at [g * kCompactClasses, + count)
   uint32_t* grp_sure;    // per compaction group: classes surely selected
-  uint32_t* grp_tie;     // per compaction group: non-positive keys == thresh
+  uint32_t* grp_tie;     // per compaction group: its candidate count, then (once the
+                         // threshold is resolved) its non-positive keys == thresh
   uint32_t* grp_out;     // per compaction group: output offset
   uint32_t* grp_tie_off; // per compaction group: ties before the group
 };
@@ -89,7 +89,7 @@ constexpr int kDwGates = 512;
 struct WsLayout {
   size_t bytes;
   size_t sample_bytes;   // prefix used by the sampler
-  size_t off_bitmap, off_hist, off_state, off_digits, off_cand, off_cand_key;
+  size_t off_bitmap, off_hist, off_state, off_digits, off_cand_key;
   size_t off_grp_sure, off_grp_tie, off_grp_out, off_grp_tie_off;
   size_t off_inv_x, off_xb, off_xblk, off_wmax, off_inv_w, off_cos, off_stats, off_tgt, off_tgtc,
       off_gmax, off_gscale, off_dx, off_loss, off_act_pad, off_dw_gate;

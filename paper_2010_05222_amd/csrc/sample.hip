@@ -67,10 +67,6 @@ __device__ __forceinline__ uint64_t class_key(uint64_t seed, int64_t a, int64_t 
   return philox4x64_10((uint64_t)(g >> 2), seed).v[g & 3];
 }
 
-__device__ __forceinline__ bool is_positive(const uint32_t* bitmap, int64_t c) {
-  return (bitmap[c >> 5] >> (c & 31)) & 1u;
-}
-
 // Digits of the 16 classes c0 .. c0 + 15 (c0 a multiple of 16; the digit
 // array is padded to whole groups of 16): two 16-byte loads.
 __device__ __forceinline__ void load_digits16(const uint16_t* digits, int64_t c0, uint32_t (&w)[8]) {
@@ -183,7 +179,6 @@ __global__ void k_sample_clear(uint32_t* bitmap, int64_t nwords, uint32_t* hist,
   if (tid == 0) {
     st->n_pos = 0;
     st->mode = kSelectNone;
-    st->cand_count = 0;
     st->top_digit = 0;
     st->n_neg = 0;
     st->k_rem = 0;
@@ -191,8 +186,13 @@ __global__ void k_sample_clear(uint32_t* bitmap, int64_t nwords, uint32_t* hist,
   }
 }
 
+// Marks the positives and counts them once each.  The key histogram counts
+// non-positive classes only; the key pass adds every class, so each
+// positive's digit is taken off here (unsigned counts: the sum is exact once
+// both passes are done, whatever their order inside the histogram).
 __global__ void k_mark_positives(const int64_t* labels, int64_t B, int64_t C,
-                                 int64_t a, uint32_t* bitmap, SampleState* st) {
+                                 int64_t a, uint64_t seed, int top_bits, uint32_t* bitmap,
+                                 uint32_t* hist, SampleState* st) {
   const int64_t n = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (n >= B) return;
   const int64_t y = labels[n];
@@ -200,7 +200,10 @@ __global__ void k_mark_positives(const int64_t* labels, int64_t B, int64_t C,
   const int64_t c = y - a;
   const uint32_t bit = 1u << (c & 31);
   const uint32_t old = atomicOr(&bitmap[c >> 5], bit);
-  if (!(old & bit)) atomicAdd(&st->n_pos, 1u);
+  if (!(old & bit)) {
+    atomicAdd(&st->n_pos, 1u);
+    atomicSub(&hist[(uint32_t)(class_key(seed, a, c) >> (64 - top_bits))], 1u);
+  }
 }
 
 __global__ void k_sample_plan(SampleState* st, int64_t budget, int64_t C) {
@@ -223,32 +226,52 @@ __global__ void k_sample_plan(SampleState* st, int64_t budget, int64_t C) {
   }
 }
 
-// One Philox block per thread: global ids 4q .. 4q+3, q = q_lo + thread.
-__global__ void __launch_bounds__(256) k_keys_hist(uint64_t seed, int64_t a, int64_t C,
-                                                   int top_bits, const uint32_t* bitmap,
-                                                   uint16_t* digits, uint32_t* hist,
-                                                   const SampleState* st) {
+// Digits of the four classes of Philox block q into `digits` and the
+// workgroup's histogram.  With the shard starting on a block boundary the
+// four digits are one 8-byte store.
+__device__ __forceinline__ void keys_block(const U64x4& w, int64_t q, int64_t a, int64_t C,
+                                           int top_bits, uint16_t* digits, uint32_t* lhist) {
+  const int64_t c0 = 4 * q - a;
+  uint32_t dg[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) dg[i] = (uint32_t)(w.v[i] >> (64 - top_bits));
+  if ((a & 3) == 0 && c0 + 3 < C) {
+    *reinterpret_cast<uint2*>(digits + c0) = make_uint2(dg[0] | (dg[1] << 16), dg[2] | (dg[3] << 16));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) atomicAdd(&lhist[dg[i]], 1u);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t c = c0 + i;
+      if (c < 0 || c >= C) continue;
+      digits[c] = (uint16_t)dg[i];
+      atomicAdd(&lhist[dg[i]], 1u);
+    }
+  }
+}
+
+// Grid-stride over the Philox blocks of the shard (global ids 4q .. 4q + 3),
+// two independent blocks per thread and iteration; each workgroup builds one
+// histogram of its share (every class; the positives were taken off before)
+// and flushes it once.  The loop reads nothing from memory.
+__global__ void __launch_bounds__(1024) k_keys_hist(uint64_t seed, int64_t a, int64_t C,
+                                                    int top_bits, uint16_t* digits,
+                                                    uint32_t* hist, const SampleState* st) {
   if (st->mode != kSelectKeys) return;
   __shared__ uint32_t lhist[1 << kTopBitsMax];
   const int nbins = 1 << top_bits;
   for (int i = threadIdx.x; i < nbins; i += blockDim.x) lhist[i] = 0u;
   __syncthreads();
-  // Grid-stride over the Philox blocks of the shard: each workgroup builds
-  // one histogram of its share and flushes it once.
-  const int64_t q_lo = a >> 2;
   const int64_t q_hi = (a + C - 1) >> 2;
-  for (int64_t q = q_lo + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q <= q_hi;
-       q += (int64_t)gridDim.x * blockDim.x) {
-    const U64x4 w = philox4x64_10((uint64_t)q, seed);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int64_t c = 4 * q + i - a;
-      if (c < 0 || c >= C) continue;
-      const uint32_t dg = (uint32_t)(w.v[i] >> (64 - top_bits));
-      digits[c] = (uint16_t)dg;
-      if (!is_positive(bitmap, c)) atomicAdd(&lhist[dg], 1u);
-    }
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  int64_t q = (a >> 2) + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  for (; q + stride <= q_hi; q += 2 * stride) {
+    const U64x4 w0 = philox4x64_10((uint64_t)q, seed);
+    const U64x4 w1 = philox4x64_10((uint64_t)(q + stride), seed);
+    keys_block(w0, q, a, C, top_bits, digits, lhist);
+    keys_block(w1, q + stride, a, C, top_bits, digits, lhist);
   }
+  if (q <= q_hi) keys_block(philox4x64_10((uint64_t)q, seed), q, a, C, top_bits, digits, lhist);
   __syncthreads();
   // Flush starting at a per-workgroup offset so that workgroups finishing
   // together hit different bins.
@@ -275,84 +298,107 @@ __global__ void __launch_bounds__(1024) k_select_top(const uint32_t* hist, int t
   if (threadIdx.x == 0) {
     st->top_digit = (uint32_t)found[0];
     st->k_rem -= found[1];
-    st->cand_count = 0;
   }
 }
 
 // One workgroup per compaction group (kCompactClasses classes, kCompactPer per
 // thread).  Counts the group's classes that the top-bit digit already selects
 // (positives, and non-positives below the threshold's bucket; every class when
-// all are taken, the positives when no negative is), and collects the
-// non-positive classes of the bucket with their full keys (one slot
-// reservation per wave).  The bucket's classes are added to their groups'
-// counts once the threshold is known (k_refine).
+// all are taken, the positives when no negative is), and writes the full keys
+// of the group's non-positive classes in that bucket to the group's own part
+// of cand_key (offsets from one workgroup scan, no atomics).  The bucket's
+// classes are added to their groups' counts once the threshold is known
+// (k_refine).
 __global__ void __launch_bounds__(kCompactThreads) k_collect(
     const uint16_t* digits, const uint32_t* bitmap, int64_t C, uint64_t seed, int64_t a,
-    SampleState* st, uint32_t* cand, uint64_t* cand_key, uint32_t* grp_sure, uint32_t* grp_tie) {
+    const SampleState* st, uint64_t* cand_key, uint32_t* grp_sure, uint32_t* grp_tie) {
   __shared__ uint32_t smem[kCompactThreads / 64];
   const uint32_t mode = st->mode;
   const uint32_t digit = st->top_digit;
   const int64_t c0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * kCompactPer;
   uint32_t take = 0, base_bits = 0;
   if (c0 < C) {
+    // The digits are read whatever the mode (the array always holds whole
+    // groups of 16), so that these loads need not wait for the state's.
+    uint32_t w[8];
+    load_digits16(digits, c0, w);
     const uint32_t pos = (bitmap[c0 >> 5] >> (c0 & 31)) & 0xFFFFu;
     const uint32_t live = C - c0 >= kCompactPer ? 0xFFFFu : (1u << (C - c0)) - 1u;
+    uint32_t below = 0, equal = 0;
+#pragma unroll
+    for (int i = 0; i < kCompactPer; ++i) {
+      const uint32_t dg = digit_of(w, i);
+      below |= (uint32_t)(dg < digit) << i;
+      equal |= (uint32_t)(dg == digit) << i;
+    }
     if (mode == kSelectAll) {
       base_bits = live;
     } else if (mode == kSelectNone) {
       base_bits = pos & live;
     } else {
-      uint32_t w[8];
-      load_digits16(digits, c0, w);
-#pragma unroll
-      for (int i = 0; i < kCompactPer; ++i) {
-        const uint32_t dg = digit_of(w, i);
-        if (dg < digit) base_bits |= 1u << i;
-        else if (dg == digit) take |= 1u << i;
-      }
-      base_bits = (base_bits | pos) & live;
-      take &= ~pos & live;
+      base_bits = (below | pos) & live;
+      take = equal & ~pos & live;
     }
   }
+  // Both counts in one scan: selected classes in the low half, candidates in
+  // the high half (each at most kCompactClasses per group, so no carry).
   uint32_t tot;
-  block_exclusive_scan((uint32_t)__popc(base_bits), smem, &tot);
+  const uint32_t pre = block_exclusive_scan(
+      (uint32_t)__popc(base_bits) | ((uint32_t)__popc(take) << 16), smem, &tot);
   if (threadIdx.x == 0) {
-    grp_sure[blockIdx.x] = tot;
-    grp_tie[blockIdx.x] = 0u;
+    grp_sure[blockIdx.x] = tot & 0xFFFFu;
+    grp_tie[blockIdx.x] = tot >> 16;
   }
-  const uint32_t n = (uint32_t)__popc(take);
-  if (__ballot(n != 0) == 0) return;
-  // The wave's exclusive prefix of the counts, and one reservation by lane 63.
-  uint32_t incl = n;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const uint32_t v = __shfl_up(incl, off, 64);
-    if (lane_id() >= off) incl += v;
-  }
-  uint32_t base = 0;
-  if (lane_id() == 63) base = atomicAdd(&st->cand_count, incl);
-  base = __shfl(base, 63, 64) + incl - n;
+  uint64_t* out = cand_key + (int64_t)blockIdx.x * kCompactClasses + (pre >> 16);
   while (take) {
     const int i = __ffs(take) - 1;
     take &= take - 1;
-    cand[base] = (uint32_t)(c0 + i);
-    cand_key[base] = class_key(seed, a, c0 + i);
-    ++base;
+    *out++ = class_key(seed, a, c0 + i);
   }
 }
 
+// Candidates the refinement keeps in LDS (64 KB of keys); more stay in memory.
+constexpr int kRefineLds = 8192;
+
 // One workgroup: resolve the remaining 64 - top_bits bits of the threshold
-// among the collected candidates, 11 bits per round.
-__global__ void __launch_bounds__(1024) k_refine(const uint32_t* cand, const uint64_t* cand_key,
+// among the collected candidates, 11 bits per round.  Thread t owns groups
+// t, t + 1024, ...; the candidates are first gathered in that order into LDS
+// when they fit.
+__global__ void __launch_bounds__(1024) k_refine(const uint64_t* cand_key, int64_t n_groups,
                                                  int top_bits, SampleState* st,
                                                  uint32_t* grp_sure, uint32_t* grp_tie) {
   if (st->mode != kSelectKeys) return;
   constexpr int kBits = 11;
   __shared__ uint32_t lh[1 << kBits];
+  __shared__ uint64_t lkeys[kRefineLds];
   __shared__ uint64_t scan_smem[16];
   __shared__ int64_t found[3];
   __shared__ uint64_t sole;
-  const uint32_t n = st->cand_count;
+  uint64_t mine = 0;
+  for (int64_t g = threadIdx.x; g < n_groups; g += blockDim.x) mine += grp_tie[g];
+  uint64_t total;
+  const uint64_t base = block_exclusive_scan64(mine, scan_smem, &total);
+  const bool in_lds = total <= (uint64_t)kRefineLds;
+  if (in_lds) {
+    uint64_t p = base;
+    for (int64_t g = threadIdx.x; g < n_groups; g += blockDim.x) {
+      const uint32_t cnt = grp_tie[g];
+      for (uint32_t j = 0; j < cnt; ++j) lkeys[p + j] = cand_key[g * kCompactClasses + j];
+      p += cnt;
+    }
+  }
+  __syncthreads();
+  // Calls f on every candidate key once (across the workgroup).
+  auto for_each_key = [&](auto&& f) {
+    if (in_lds) {
+      for (uint64_t i = threadIdx.x; i < total; i += blockDim.x) f(lkeys[i]);
+    } else {
+      for (int64_t g = threadIdx.x; g < n_groups; g += blockDim.x) {
+        const uint32_t cnt = grp_tie[g];
+        for (uint32_t j = 0; j < cnt; ++j) f(cand_key[g * kCompactClasses + j]);
+      }
+    }
+  };
   uint64_t prefix = st->top_digit;
   int known = top_bits;
   int64_t k = st->k_rem;
@@ -361,11 +407,10 @@ __global__ void __launch_bounds__(1024) k_refine(const uint32_t* cand, const uin
     const int shift = 64 - known - bits;
     for (int i = threadIdx.x; i < (1 << kBits); i += blockDim.x) lh[i] = 0u;
     __syncthreads();
-    for (uint32_t i = threadIdx.x; i < n; i += blockDim.x) {
-      const uint64_t key = cand_key[i];
+    for_each_key([&](uint64_t key) {
       if ((key >> (64 - known)) == prefix)
         atomicAdd(&lh[(key >> shift) & ((1u << bits) - 1u)], 1u);
-    }
+    });
     __syncthreads();
     find_kth_bin(lh, 1 << kBits, k, scan_smem, found);
     prefix = (prefix << bits) | (uint64_t)found[0];
@@ -373,10 +418,9 @@ __global__ void __launch_bounds__(1024) k_refine(const uint32_t* cand, const uin
     known += bits;
     if (found[2] == 1 && known < 64) {
       // The bin holds a single key (k is then 1): that key is the threshold.
-      for (uint32_t i = threadIdx.x; i < n; i += blockDim.x) {
-        const uint64_t key = cand_key[i];
+      for_each_key([&](uint64_t key) {
         if ((key >> (64 - known)) == prefix) sole = key;
-      }
+      });
       __syncthreads();
       prefix = sole;
       known = 64;
@@ -388,12 +432,22 @@ __global__ void __launch_bounds__(1024) k_refine(const uint32_t* cand, const uin
     st->k_rem = k;
   }
   // The bucket's classes join their groups' counts: below the threshold they
-  // are selected, equal to it they are ties (taken in class order).
-  for (uint32_t i = threadIdx.x; i < n; i += blockDim.x) {
-    const uint64_t key = cand_key[i];
-    const uint32_t g = cand[i] / (uint32_t)kCompactClasses;
-    if (key < prefix) atomicAdd(&grp_sure[g], 1u);
-    else if (key == prefix) atomicAdd(&grp_tie[g], 1u);
+  // are selected, equal to it they are ties (taken in class order).  Each
+  // thread updates only the groups it owns.
+  uint64_t p = base;
+  for (int64_t g = threadIdx.x; g < n_groups; g += blockDim.x) {
+    const uint32_t cnt = grp_tie[g];
+    uint32_t below = 0, equal = 0;
+    for (uint32_t j = 0; j < cnt; ++j) {
+      const uint64_t key = in_lds ? lkeys[p + j] : cand_key[g * kCompactClasses + j];
+      below += key < prefix;
+      equal += key == prefix;
+    }
+    p += cnt;
+    if (cnt) {
+      grp_sure[g] += below;
+      grp_tie[g] = equal;
+    }
   }
 }
 
@@ -406,32 +460,36 @@ __device__ __forceinline__ void class_flags(const uint16_t* digits, const uint32
                                             uint32_t* tie) {
   const uint32_t mode = st->mode;
   const uint32_t top = st->top_digit;
+  const uint64_t thresh = st->thresh;
   uint32_t s = 0, t = 0, need = 0;
   if (c0 >= C) {
     *sure = 0;
     *tie = 0;
     return;
   }
-  // c0 is a multiple of 16: one bitmap word holds the classes' bits.
+  // c0 is a multiple of 16: one bitmap word holds the classes' bits.  The
+  // digits are read whatever the mode, beside the state's loads.
+  uint32_t w[8];
+  load_digits16(digits, c0, w);
   const uint32_t pos = (bitmap[c0 >> 5] >> (c0 & 31)) & 0xFFFFu;
-  uint32_t w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  if (mode == kSelectKeys) load_digits16(digits, c0, w);
+  const uint32_t live = C - c0 >= kCompactPer ? 0xFFFFu : (1u << (C - c0)) - 1u;
+  uint32_t below = 0, equal = 0;
 #pragma unroll
   for (int i = 0; i < kCompactPer; ++i) {
-    if (c0 + i >= C) continue;
-    if ((pos >> i) & 1u) {
-      s |= 1u << i;
-    } else if (mode == kSelectAll) {
-      s |= 1u << i;
-    } else if (mode == kSelectKeys) {
-      const uint32_t dg = digit_of(w, i);
-      if (dg < top) s |= 1u << i;
-      else if (dg == top) need |= 1u << i;
-    }
+    const uint32_t dg = digit_of(w, i);
+    below |= (uint32_t)(dg < top) << i;
+    equal |= (uint32_t)(dg == top) << i;
+  }
+  if (mode == kSelectAll) {
+    s = live;
+  } else if (mode == kSelectKeys) {
+    s = (below | pos) & live;
+    need = equal & ~pos & live;
+  } else {
+    s = pos & live;
   }
   // Classes in the threshold's bucket (rare): one key generator in a loop.
   if (need) {
-    const uint64_t thresh = st->thresh;
     do {
       const int i = __ffs(need) - 1;
       need &= need - 1;
@@ -508,6 +566,9 @@ __global__ void __launch_bounds__(kCompactThreads) k_compact_write(
     int32_t* active) {
   __shared__ uint32_t smem[kCompactThreads / 64];
   const int64_t c0 = ((int64_t)blockIdx.x * kCompactThreads + threadIdx.x) * kCompactPer;
+  const int64_t tie_off = grp_tie_off[blockIdx.x];
+  const int64_t out_off = grp_out[blockIdx.x];
+  const int64_t k_rem = st->k_rem;
   uint32_t s, t;
   class_flags(digits, bitmap, C, seed, a, st, c0, &s, &t);
   // Class-order ranks: thread t owns classes kCompactPer t .. + kCompactPer - 1,
@@ -515,15 +576,14 @@ __global__ void __launch_bounds__(kCompactThreads) k_compact_write(
   // counts plus the bits below it in the thread.
   uint32_t ttot;
   const uint32_t tpre = block_exclusive_scan((uint32_t)__popc(t), smem, &ttot);
-  const int64_t tie_base = (int64_t)grp_tie_off[blockIdx.x] + tpre;
-  const int64_t k_rem = st->k_rem;
+  const int64_t tie_base = tie_off + tpre;
   uint32_t sel = s;
 #pragma unroll
   for (int i = 0; i < kCompactPer; ++i)
     if (((t >> i) & 1u) && tie_base + __popc(t & ((1u << i) - 1u)) < k_rem) sel |= 1u << i;
   uint32_t stot;
   const uint32_t spre = block_exclusive_scan((uint32_t)__popc(sel), smem, &stot);
-  const int64_t out_base = (int64_t)grp_out[blockIdx.x] + spre;
+  const int64_t out_base = out_off + spre;
   uint32_t rest = sel;
   while (rest) {
     const int i = __ffs(rest) - 1;
@@ -533,28 +593,54 @@ __global__ void __launch_bounds__(kCompactThreads) k_compact_write(
   }
 }
 
-__global__ void k_remap(const int64_t* labels, int64_t B, int64_t C, int64_t a,
-                        const int32_t* active, const int32_t* n_active,
-                        int32_t* labels_mapped) {
-  const int64_t n = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (n >= B) return;
+// One wave per batch row.  S is written group by group, so a class of
+// compaction group g can only sit in [grp_out[g], grp_out[g + 1]) (clamped to
+// |S|).  The wave finds the first index f there whose id is >= the label
+// (searchsorted): [lo, hi) is the part not yet decided (ids before lo are
+// < the label, ids from hi on are >=); 64 probes per round shrink it to under
+// 64 entries (one round for a group's at most 4,096), and one read of those
+// plus index hi gives f and the id found there.
+__global__ void __launch_bounds__(256) k_remap(const int64_t* labels, int64_t B, int64_t C,
+                                               int64_t a, const int32_t* active,
+                                               const int32_t* n_active, const uint32_t* grp_out,
+                                               int64_t n_groups, int32_t* labels_mapped) {
+  const int64_t n = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = lane_id();
+  if (n >= B) return;   // wave-uniform
   const int64_t y = labels[n];
   if (y < a || y >= a + C) {
-    labels_mapped[n] = -1;
+    if (lane == 0) labels_mapped[n] = -1;
     return;
   }
   const int32_t c = (int32_t)(y - a);
-  const int32_t k = *n_active;
-  int32_t lo = 0, hi = k;  // first index with active[idx] >= c
-  while (lo < hi) {
-    const int32_t mid = lo + ((hi - lo) >> 1);
-    if (active[mid] < c) lo = mid + 1;
-    else hi = mid;
+  const int64_t k = *n_active;
+  const int64_t g = c / kCompactClasses;
+  const int64_t g_lo = grp_out[g];
+  const int64_t g_hi = g + 1 < n_groups ? (int64_t)grp_out[g + 1] : k;
+  const int64_t end = g_hi < k ? g_hi : k;
+  int64_t lo = g_lo < end ? g_lo : end;
+  int64_t hi = end;
+  while (hi - lo > 63) {
+    const int64_t len = hi - lo;
+    const int64_t p = lo + (len * lane) / 64;   // strictly increasing in [lo, hi), p_0 = lo
+    const int nl = __popcll(__ballot(active[p] < c));   // sorted: true on lanes 0 .. nl - 1
+    const int64_t p_last = __shfl(p, nl > 0 ? nl - 1 : 0, 64);
+    const int64_t p_next = __shfl(p, nl < 64 ? nl : 63, 64);
+    if (nl == 0) {
+      hi = lo;
+    } else {
+      lo = p_last + 1;
+      if (nl < 64) hi = p_next;
+    }
   }
+  const int64_t m = (hi < end ? hi + 1 : end) - lo;   // <= 64
+  const int32_t v = lane < m ? active[lo + lane] : INT32_MAX;
+  const int f = __popcll(__ballot(lane < m && v < c));
+  const int32_t vf = __shfl(v, f < 64 ? f : 63, 64);
   // Every in-shard label is a positive, which the sampler always keeps; a
   // label not found in S is nevertheless mapped to -1 (unowned), never to a
   // position whose id is another class or lies past |S|.
-  labels_mapped[n] = (lo < k && active[lo] == c) ? lo : -1;
+  if (lane == 0) labels_mapped[n] = (f < m && vf == c) ? (int32_t)(lo + f) : -1;
 }
 
 }  // namespace
@@ -569,25 +655,25 @@ hipError_t launch_sample(const int64_t* labels, int64_t B, int64_t C, int64_t a,
   hipLaunchKernelGGL(k_sample_clear, dim3(clear_blocks > 0 ? clear_blocks : 1), dim3(256), 0,
                      stream, w.bitmap, nwords, w.hist, w.state);
   hipLaunchKernelGGL(k_mark_positives, dim3((unsigned)ceil_div(B, 256)), dim3(256), 0, stream,
-                     labels, B, C, a, w.bitmap, w.state);
+                     labels, B, C, a, seed, top_bits, w.bitmap, w.hist, w.state);
   hipLaunchKernelGGL(k_sample_plan, dim3(1), dim3(64), 0, stream, w.state, budget, C);
   const int64_t n_blocks_philox = ((a + C - 1) >> 2) - (a >> 2) + 1;
-  const int64_t hist_wgs = ceil_div(n_blocks_philox, 256);
-  hipLaunchKernelGGL(k_keys_hist, dim3((unsigned)(hist_wgs < 512 ? hist_wgs : 512)), dim3(256), 0,
-                     stream, seed, a, C, top_bits, w.bitmap, w.digits, w.hist, w.state);
+  // One workgroup of 1024 threads per CU at most: each flushes a histogram.
+  const int64_t hist_wgs = ceil_div(n_blocks_philox, 1024);
+  hipLaunchKernelGGL(k_keys_hist, dim3((unsigned)(hist_wgs < 256 ? hist_wgs : 256)), dim3(1024), 0,
+                     stream, seed, a, C, top_bits, w.digits, w.hist, w.state);
   hipLaunchKernelGGL(k_select_top, dim3(1), dim3(1024), 0, stream, w.hist, top_bits, w.state);
   hipLaunchKernelGGL(k_collect, dim3((unsigned)n_groups), dim3(kCompactThreads), 0, stream,
-                     w.digits, w.bitmap, C, seed, a, w.state, w.cand, w.cand_key, w.grp_sure,
-                     w.grp_tie);
-  hipLaunchKernelGGL(k_refine, dim3(1), dim3(1024), 0, stream, w.cand, w.cand_key, top_bits,
+                     w.digits, w.bitmap, C, seed, a, w.state, w.cand_key, w.grp_sure, w.grp_tie);
+  hipLaunchKernelGGL(k_refine, dim3(1), dim3(1024), 0, stream, w.cand_key, n_groups, top_bits,
                      w.state, w.grp_sure, w.grp_tie);
   hipLaunchKernelGGL(k_compact_scan, dim3(1), dim3(1024), 0, stream, w.grp_sure, w.grp_tie,
                      n_groups, w.state, cap, w.grp_out, w.grp_tie_off, n_active);
   hipLaunchKernelGGL(k_compact_write, dim3((unsigned)n_groups), dim3(kCompactThreads), 0, stream,
                      w.digits, w.bitmap, C, seed, a, w.state, w.grp_out, w.grp_tie_off, cap,
                      active);
-  hipLaunchKernelGGL(k_remap, dim3((unsigned)ceil_div(B, 256)), dim3(256), 0, stream, labels, B,
-                     C, a, active, n_active, labels_mapped);
+  hipLaunchKernelGGL(k_remap, dim3((unsigned)ceil_div(B, 4)), dim3(256), 0, stream, labels, B,
+                     C, a, active, n_active, w.grp_out, n_groups, labels_mapped);
   timing_stop(0, stream);
   return hipGetLastError();
 }

@@ -15,9 +15,9 @@ namespace {
 
 // Largest sampler prefix of the workspace layout (ws_layout) for
 // C <= PFC_NOALLOC_MAX_CLASSES, rounded up: bitmap C/8 + histogram 16 KiB +
-// state + digits 2C + candidates 4C + candidate keys 8C + four group arrays
-// (28.3 MiB at C = 2^21).
-constexpr size_t kScratchBytes = (size_t)30 << 20;
+// state + digits 2C + candidate keys 8C + four group arrays (20.3 MiB at
+// C = 2^21).
+constexpr size_t kScratchBytes = (size_t)21 << 20;
 
 // One copy per device; every call on a device shares it.
 __device__ __align__(256) unsigned char scratch[kScratchBytes];

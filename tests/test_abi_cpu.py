@@ -105,6 +105,7 @@ def _sample_args(**kw):
     (dict(r=0.0), pfc.PFC_ERR_INVALID_ARG),
     (dict(active_cap=99), pfc.PFC_ERR_CAPACITY),
     (dict(ws=0), pfc.PFC_ERR_WORKSPACE),
+    (dict(ws=FAKE + 16), pfc.PFC_ERR_WORKSPACE),          # not 256-byte aligned
     (dict(ws_bytes=1024), pfc.PFC_ERR_WORKSPACE),
 ])
 def test_sample_rejects_before_launch(kw, status):
@@ -133,6 +134,7 @@ def _fwd_args(**kw):
     (dict(active_cap=0), pfc.PFC_ERR_CAPACITY),
     (dict(active_cap=1001), pfc.PFC_ERR_CAPACITY),
     (dict(ws_bytes=4096), pfc.PFC_ERR_WORKSPACE),
+    (dict(ws=FAKE + 128), pfc.PFC_ERR_WORKSPACE),         # not 256-byte aligned
 ])
 def test_forward_rejects_before_launch(kw, status):
     with pytest.raises(pfc.PfcError) as e:
@@ -158,6 +160,7 @@ def _bwd_args(**kw):
     (dict(mu=-0.5), pfc.PFC_ERR_INVALID_ARG),
     (dict(d=256, x_dtype=0, w_dtype=1, compute_dtype=1), pfc.PFC_ERR_UNSUPPORTED),
     (dict(ws=0), pfc.PFC_ERR_WORKSPACE),
+    (dict(ws=FAKE + 8), pfc.PFC_ERR_WORKSPACE),           # not 256-byte aligned
 ])
 def test_backward_rejects_before_launch(kw, status):
     with pytest.raises(pfc.PfcError) as e:

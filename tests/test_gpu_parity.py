@@ -160,6 +160,34 @@ def test_sampler_full_size(dev, name):
     assert np.array_equal(shard.labels_mapped.cpu().numpy(), mapped_ref)
 
 
+# Shards that do not start on a Philox block (class_offset not a multiple of
+# four), ragged last groups, every selection mode (keys; all classes at r = 1;
+# positives only when they exceed the budget), duplicated and unowned labels.
+@pytest.mark.parametrize("B,C,a,r,seed", [
+    (64, 9001, 3, 0.1, 21),
+    (300, 70001, 1000001, 0.05, 22),
+    (8, 17, 2, 0.5, 23),
+    (256, 5000, 6, 0.01, 24),       # |P| > budget: positives only
+    (40, 2003, 5, 1.0, 25),         # every class
+    (1000, 12289, 4097, 0.3, 26),   # most labels in one 4,096-class group
+])
+def test_sampler_offsets_and_modes(dev, B, C, a, r, seed):
+    rng = np.random.default_rng(seed)
+    labels = rng.integers(max(a - 50, 0), a + C + 50, size=B)  # some outside the shard
+    if C > 8192:
+        labels[: B // 2] = rng.integers(a + 4096, a + 8192, size=B // 2)
+    labels[::7] = labels[0]                                    # duplicates
+    print(f"\nsampler B={B} C={C} a={a} r={r} seed={seed}", flush=True)
+    shard = _shard(B, 128, C, r, "bf16", "arcface", 0.5, class_offset=a, dev=dev)
+    shard.sample(torch.from_numpy(labels.astype(np.int64)).to(dev), seed)
+    torch.cuda.synchronize()
+    active_ref, mapped_ref, info = O.sample_active(labels, C, a, r, seed)
+    K = int(shard.n_active.item())
+    assert K == len(active_ref) == max(O.budget(r, C), info["n_pos"])
+    assert np.array_equal(shard.active[:K].cpu().numpy(), active_ref)
+    assert np.array_equal(shard.labels_mapped.cpu().numpy(), mapped_ref)
+
+
 def test_many_rows_per_class(dev):
     # Every row is labelled with one of three classes of the same 128-class
     # tile: each quarter of the batch holds more target rows of that tile than
