@@ -61,10 +61,14 @@ __device__ __forceinline__ U64x4 philox4x64_10(uint64_t c0, uint64_t seed) {
   return out;
 }
 
-// Key of class c of the shard starting at global class a.
+// Key of class c of the shard starting at global class a.  The word is
+// picked with selects: indexing the block's words by a run-time value would
+// place them in LDS, and that costs more than the generator here.
 __device__ __forceinline__ uint64_t class_key(uint64_t seed, int64_t a, int64_t c) {
   const int64_t g = a + c;
-  return philox4x64_10((uint64_t)(g >> 2), seed).v[g & 3];
+  const U64x4 w = philox4x64_10((uint64_t)(g >> 2), seed);
+  const int i = (int)(g & 3);
+  return i == 0 ? w.v[0] : i == 1 ? w.v[1] : i == 2 ? w.v[2] : w.v[3];
 }
 
 // Digits of the 16 classes c0 .. c0 + 15 (c0 a multiple of 16; the digit
