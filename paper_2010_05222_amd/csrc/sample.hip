@@ -361,14 +361,18 @@ __global__ void __launch_bounds__(kCompactThreads) k_collect(
   }
 }
 
-// Candidates the refinement keeps in LDS (64 KB of keys); more stay in memory.
-constexpr int kRefineLds = 8192;
+// The refinement's workgroup and the candidates it keeps in LDS (32 KB of
+// keys; more stay in memory).  It is small enough (40 KB of LDS, two waves
+// per SIMD) to share a CU with one workgroup of the step's big kernels, so a
+// sampler running beside a step does not wait for a whole kernel to drain.
+constexpr int kRefineThreads = 512;
+constexpr int kRefineLds = 4096;
 
 // One workgroup: resolve the remaining 64 - top_bits bits of the threshold
 // among the collected candidates, 11 bits per round.  Thread t owns groups
-// t, t + 1024, ...; the candidates are first gathered in that order into LDS
-// when they fit.
-__global__ void __launch_bounds__(1024) k_refine(const uint64_t* cand_key, int64_t n_groups,
+// t, t + kRefineThreads, ...; the candidates are first gathered in that
+// order into LDS when they fit.
+__global__ void __launch_bounds__(kRefineThreads) k_refine(const uint64_t* cand_key, int64_t n_groups,
                                                  int top_bits, SampleState* st,
                                                  uint32_t* grp_sure, uint32_t* grp_tie) {
   if (st->mode != kSelectKeys) return;
@@ -669,7 +673,7 @@ hipError_t launch_sample(const int64_t* labels, int64_t B, int64_t C, int64_t a,
   hipLaunchKernelGGL(k_select_top, dim3(1), dim3(1024), 0, stream, w.hist, top_bits, w.state);
   hipLaunchKernelGGL(k_collect, dim3((unsigned)n_groups), dim3(kCompactThreads), 0, stream,
                      w.digits, w.bitmap, C, seed, a, w.state, w.cand_key, w.grp_sure, w.grp_tie);
-  hipLaunchKernelGGL(k_refine, dim3(1), dim3(1024), 0, stream, w.cand_key, n_groups, top_bits,
+  hipLaunchKernelGGL(k_refine, dim3(1), dim3(kRefineThreads), 0, stream, w.cand_key, n_groups, top_bits,
                      w.state, w.grp_sure, w.grp_tie);
   hipLaunchKernelGGL(k_compact_scan, dim3(1), dim3(1024), 0, stream, w.grp_sure, w.grp_tie,
                      n_groups, w.state, cap, w.grp_out, w.grp_tie_off, n_active);
