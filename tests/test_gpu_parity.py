@@ -188,6 +188,33 @@ def test_sampler_offsets_and_modes(dev, B, C, a, r, seed):
     assert np.array_equal(shard.labels_mapped.cpu().numpy(), mapped_ref)
 
 
+def test_sampler_refinement_beyond_lds(dev):
+    """A shard of 20M classes: the threshold's top-digit bucket holds more
+    candidates than the refinement keeps in LDS (4,096), so it works on them
+    in memory.  Bit-exact active set and remap."""
+    from oracle import philox
+    B, C, a, r, seed = 1024, 20_000_000, 0, 0.01, 31
+    rng = np.random.default_rng(seed)
+    labels = rng.integers(0, C, size=B)
+    active_ref, mapped_ref, info = O.sample_active(labels, C, a, r, seed)
+    # The bucket of the n_neg-th smallest non-positive key (12 top bits at this C).
+    is_pos = np.zeros(C, dtype=bool)
+    is_pos[info["positives"]] = True
+    pool = np.nonzero(~is_pos)[0]
+    digits = philox.class_keys(seed, pool + a) >> np.uint64(52)
+    thresh_digit = np.sort(digits)[info["n_neg"] - 1]
+    bucket = int(np.count_nonzero(digits == thresh_digit))
+    assert bucket > 4096, bucket
+    print(f"\nsampler C={C} r={r}: bucket of {bucket} candidates", flush=True)
+    shard = _shard(B, 128, C, r, "bf16", "arcface", 0.5, class_offset=a, dev=dev)
+    shard.sample(torch.from_numpy(labels.astype(np.int64)).to(dev), seed)
+    torch.cuda.synchronize()
+    K = int(shard.n_active.item())
+    assert K == len(active_ref) == max(O.budget(r, C), info["n_pos"])
+    assert np.array_equal(shard.active[:K].cpu().numpy(), active_ref)
+    assert np.array_equal(shard.labels_mapped.cpu().numpy(), mapped_ref)
+
+
 def test_many_rows_per_class(dev):
     # Every row is labelled with one of three classes of the same 128-class
     # tile: each quarter of the batch holds more target rows of that tile than
