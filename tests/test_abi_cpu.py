@@ -47,10 +47,11 @@ def test_workspace_and_capacity_of_each_workload(name):
     nbytes, cap = pfc.pfc_workspace_bytes(cfg["B"], cfg["d"], cfg["C"], cfg["r"], code)
     b = O.budget(cfg["r"], cfg["C"])
     assert cap == max(b, min(cfg["B"], cfg["C"]))
-    # Dominated by the quantised cosines [B x cap] and the sampler keys [C].
+    # Dominated by the logit store [B x cap] and the sampler's per-class
+    # digits (2 B) and candidate keys (8 B).
     elt = 4 if code == pfc.PFC_F32 else 2
-    assert nbytes >= cfg["B"] * cap * elt + cfg["C"] * 12
-    assert nbytes < 2 * (cfg["B"] * cap * elt + cfg["C"] * 12) + (256 << 20)
+    assert nbytes >= cfg["B"] * cap * elt + cfg["C"] * 10
+    assert nbytes < 2 * (cfg["B"] * cap * elt + cfg["C"] * 10) + (256 << 20)
 
 
 def test_batch_limit_matches_header():
