@@ -45,11 +45,20 @@ __global__ void __launch_bounds__(256) k_prep_x16(const uint16_t* __restrict__ X
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n0 = blockIdx.x * kPrepRows;
   if (blockIdx.x == 0 && threadIdx.x == 0) *inv_w_max = 0.0f;
-  for (int r = wave; r < kPrepRows; r += 4) {
+  // Each wave's eight rows: all loads first (one memory round trip, not eight).
+  const bool c_ok = lane < d / 8;   // d <= 512: one 16-byte piece per lane
+  uint4 rows[kPrepRows / 4];
+#pragma unroll
+  for (int k = 0; k < kPrepRows / 4; ++k) {
+    const int n = n0 + wave + 4 * k;
+    rows[k] = make_uint4(0, 0, 0, 0);
+    if (n < B && c_ok) rows[k] = *reinterpret_cast<const uint4*>(X + (int64_t)n * d + 8 * lane);
+  }
+#pragma unroll
+  for (int k = 0; k < kPrepRows / 4; ++k) {
+    const int r = wave + 4 * k;
     const int n = n0 + r;
-    const bool c_ok = lane < d / 8;   // d <= 512: one 16-byte piece per lane
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (n < B && c_ok) v = *reinterpret_cast<const uint4*>(X + (int64_t)n * d + 8 * lane);
+    const uint4 v = rows[k];
     const float ss = wave_sum(sumsq8<Tag>(v));
     const float ix = 1.0f / fmaxf(sqrtf(ss), kEpsNorm);
     if (lane == 0 && n < B) inv_x[n] = ix;
