@@ -304,12 +304,18 @@ def test_conflict_filter_empty_denominator(dev, dtype):
     assert bool((shard.dX[empty] == 0).all())
 
 
-def test_batch_at_limit_16bit(dev):
-    """The largest batch the ABI accepts (PFC_MAX_BATCH = 8192), fp16 at d = 512;
-    the positives (~7,400 distinct labels) nearly fill the budget of 8,000."""
+@pytest.mark.parametrize("d,dtype,margin,m,seed", [
+    (512, "f16", "arcface", 0.5, 20),
+    (256, "bf16", "cosface", 0.4, 22),
+    (128, "bf16", "arcface", 0.5, 23),
+])
+def test_batch_at_limit_16bit(dev, d, dtype, margin, m, seed):
+    """The largest batch the ABI accepts (PFC_MAX_BATCH = 8192) at each feature
+    width of the 16-bit path; the positives (~7,400 distinct labels) nearly
+    fill the budget of 8,000."""
     from paper_2010_05222_amd import pfc
     assert pfc.PFC_MAX_BATCH == 8192
-    out = _case(dev, 8192, 512, 40000, 0.2, "f16", "arcface", 0.5, seed=20, random_m=False)
+    out = _case(dev, 8192, d, 40000, 0.2, dtype, margin, m, seed=seed, random_m=False)
     assert out["K"] == 8000
 
 
