@@ -92,6 +92,17 @@ def test_f16_d128(dev):
     _case(dev, 150, 128, 4100, 0.1, "f16", "cosface", 0.4, seed=19)
 
 
+@pytest.mark.parametrize("d", [8, 1000, 1024])
+def test_f32_feature_widths(dev, d):
+    # The fp32 path takes any d that is a multiple of 8 up to 1024: the
+    # smallest, one that is not a multiple of 32 or 64, and the largest.
+    # At d = 8 the class rows (std 0.01) have norm ~0.028, so 1/||w|| ~ 35
+    # and the class gradients reach ~72, where one fp32 ulp is 7.6e-6: the
+    # max-abs bar is applied relative to max |ref| there (as for B = 1);
+    # the row-relative bound is unchanged.
+    _case(dev, 40, d, 1500, 0.2, "f32", "arcface", 0.5, seed=27, abs_scaled=(d == 8))
+
+
 def test_positives_exceed_budget(dev):
     out = _case(dev, 512, 128, 1000, 0.05, "bf16", "cosface", 0.4, seed=6)
     assert out["K"] == out["n_pos"] > 50
