@@ -31,14 +31,16 @@ def _shard(B, d, C, r, dtype, margin, m, class_offset=0, dev="cuda:0", tau=None)
 
 
 def _case(dev, B, d, C, r, dtype, margin, m, seed, class_offset=0, label_span=None,
-          random_m=True, master=False, labels=None, tau=None, conflicts=0, abs_scaled=False):
+          random_m=True, master=False, labels=None, tau=None, conflicts=0, abs_scaled=False,
+          degenerate=False):
     from _gpu_util import make_problem, run_and_compare
     print(f"\ncase B={B} d={d} C={C} r={r} dtype={dtype} margin={margin} seed={seed} "
           f"offset={class_offset} master={master} tau={tau}", flush=True)
     Xd, Wd, Md, Pd, Ld = make_problem(B, d, C, dtype, seed, class_offset, label_span, random_m,
                                       master, labels, dev, conflicts)
     shard = _shard(B, d, C, r, dtype, margin, m, class_offset, dev, tau)
-    out = run_and_compare(shard, Xd, Wd, Md, Pd, Ld, seed, margin, abs_scaled=abs_scaled)
+    out = run_and_compare(shard, Xd, Wd, Md, Pd, Ld, seed, margin, abs_scaled=abs_scaled,
+                          degenerate=degenerate)
     print(out, flush=True)
     return out
 
@@ -101,6 +103,19 @@ def test_f32_feature_widths(dev, d):
     # max-abs bar is applied relative to max |ref| there (as for B = 1);
     # the row-relative bound is unchanged.
     _case(dev, 40, d, 1500, 0.2, "f32", "arcface", 0.5, seed=27, abs_scaled=(d == 8))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_single_class_shard(dev, dtype):
+    # The smallest shard: one class, taken at r = 1.  Rows labelled with it
+    # have a one-term softmax (probability 1, loss 0, no gradient); the
+    # others are unowned and their only logit gets the full gradient, so the
+    # class gradient reaches ~30.  References that are exactly zero and that
+    # magnitude take the degenerate-case and scaled bars.
+    labels = np.array([0, 3, 0, 9, 0, 0, 5, 0, 2, 0, 0, 4])
+    out = _case(dev, 12, 128, 1, 1.0, dtype, "arcface", 0.5, seed=28, labels=labels,
+                abs_scaled=True, degenerate=True)
+    assert out["K"] == 1
 
 
 def test_positives_exceed_budget(dev):
