@@ -196,6 +196,7 @@ def test_sampler_full_size(dev, name):
     (256, 5000, 6, 0.01, 24),       # |P| > budget: positives only
     (40, 2003, 5, 1.0, 25),         # every class
     (1000, 12289, 4097, 0.3, 26),   # most labels in one 4,096-class group
+    (64, 9001, 2**40 + 3, 0.1, 29), # global ids above 2^32: the counter's high word
 ])
 def test_sampler_offsets_and_modes(dev, B, C, a, r, seed):
     rng = np.random.default_rng(seed)
