@@ -1,7 +1,8 @@
 """pfc_sample_noalloc (no workspace; static device scratch) against
 pfc_sample (caller workspace): bit-identical active sets, |S| and remapped
 labels on two calls in a row, the second smaller than the first, both through
-the C ABI.  The second call reuses the scratch the first one left behind."""
+the C ABI.  The second call reuses the scratch the first one left behind.
+Also captured into a HIP graph and replayed with new labels."""
 
 import numpy as np
 import pytest
@@ -81,3 +82,41 @@ def test_noalloc_rejects_oversized_shard(dev):
         pfc.pfc_sample_noalloc(L.data_ptr(), 4, (1 << 21) + 1, 0, 0.1, 0, out.data_ptr(),
                                (1 << 21), out.data_ptr(), out.data_ptr(), 0)
     assert e.value.status == pfc.PFC_ERR_SCRATCH
+
+
+def test_noalloc_under_graph_capture(dev):
+    """The entry point allocates and synchronises nothing, so a caller can
+    capture it into a HIP graph: replays, with new labels written into the
+    captured input between them, each equal a direct call on those labels
+    and the oracle."""
+    from paper_2010_05222_amd import pfc
+    B, C, a, r, seed = 256, 40000, 0, 0.1, 8
+    _, cap = pfc.pfc_workspace_bytes(B, 128, C, r, pfc.PFC_BF16)
+    rng = np.random.default_rng(33)
+    L = _labels(rng, B, 0, C, dev)
+    act = torch.full((cap,), -9, dtype=torch.int32, device=dev)
+    n = torch.zeros(1, dtype=torch.int32, device=dev)
+    mapped = torch.full((B,), -9, dtype=torch.int32, device=dev)
+    _noalloc(L, B, C, a, r, seed, cap, dev)   # a direct call first (scratch address looked up)
+    torch.cuda.synchronize()
+    print(f"\nnoalloc under graph capture: B={B} C={C} r={r} seed={seed}", flush=True)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        pfc.pfc_sample_noalloc(L.data_ptr(), B, C, a, r, seed, act.data_ptr(), cap, n.data_ptr(),
+                               mapped.data_ptr(), torch.cuda.current_stream(dev).cuda_stream)
+    for rep in range(3):
+        L.copy_(_labels(rng, B, 0, C, dev))   # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = (act.clone(), n.clone(), mapped.clone())
+        ref = _noalloc(L, B, C, a, r, seed, cap, dev)
+        torch.cuda.synchronize()
+        K = int(ref[1].item())
+        assert int(got[1].item()) == K
+        assert torch.equal(got[0][:K], ref[0][:K])
+        assert torch.equal(got[2], ref[2])
+        active_ref, mapped_ref, _ = O.sample_active(L.cpu().numpy(), C, a, r, seed)
+        assert np.array_equal(got[0][:K].cpu().numpy(), active_ref)
+        assert np.array_equal(got[2].cpu().numpy(), mapped_ref)
+        print(f"replay {rep}: |S|={K} equal to a direct call and to the oracle", flush=True)
