@@ -112,7 +112,7 @@ WsLayout ws_layout(int64_t B, int64_t d, int64_t C, int64_t cap, int compute) {
   L.off_tgtc = take((size_t)B * 4);
   L.off_gmax = take(compute == PFC_F32 ? 0 : (size_t)L.n_lgroups * L.ld_g * 4);
   L.off_gscale = take(compute == PFC_F32 ? 0 : (size_t)L.n_lgroups * L.ld_g * 4);
-  L.n_act_pad = round_up(cap, 32);
+  L.n_act_pad = round_up(cap, 128);   // whole forward class tiles (and dX chunks)
   L.off_act_pad = take(compute == PFC_F32 ? 0 : (size_t)L.n_act_pad * 4);
   L.off_dw_gate = take(compute == PFC_F32 ? 0 : (size_t)kDwGates * 4);
   L.bytes = off;

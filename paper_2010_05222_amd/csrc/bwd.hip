@@ -422,25 +422,15 @@ __global__ void __launch_bounds__(128 * WI) k_dx16(
 // with an empty denominator (lse = -inf: its label is outside the shard and the
 // PFC* filter dropped every logit, so all its E are 0) gets scale 0, and with
 // it no gradient.  Groups past |S| are never read and are skipped.
-// Also writes the padded copy of the active row ids that the dX kernel reads
-// a chunk at a time: act_pad[j] = active[min(j, |S| - 1)] (0 if S is empty).
 __global__ void __launch_bounds__(256) k_scales(const float* __restrict__ gmax,
                                                 const float* __restrict__ row_lse, int B,
                                                 int64_t ld_g, int64_t n_groups,
                                                 const int32_t* __restrict__ n_active_p,
-                                                float* __restrict__ gscale,
-                                                const int32_t* __restrict__ active,
-                                                int32_t* __restrict__ act_pad, int64_t n_pad) {
-  // Four consecutive entries per thread (ld_g and n_pad are multiples of 4,
-  // so the four rows share one group and the 16-byte accesses are aligned).
+                                                float* __restrict__ gscale) {
+  // Four consecutive entries per thread (ld_g is a multiple of 4, so the four
+  // rows share one group and the 16-byte accesses are aligned).
   const int64_t i = 4 * ((int64_t)blockIdx.x * blockDim.x + threadIdx.x);
   const int64_t K = *n_active_p;
-  if (i < n_pad) {
-    int o[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) o[e] = K > 0 ? active[i + e < K ? i + e : K - 1] : 0;
-    *reinterpret_cast<int4*>(act_pad + i) = make_int4(o[0], o[1], o[2], o[3]);
-  }
   if (i >= n_groups * ld_g) return;
   const int64_t g = i / ld_g;
   const int n = (int)(i - g * ld_g);
@@ -1221,8 +1211,7 @@ void launch_bwd16(const StepArgs& a, const StepWs& w, const Margin& mg, float sB
   timing_start(4, stream);
   // Row scales of the logit store from the lse the gradient is normalised with.
   hipLaunchKernelGGL(k_scales, dim3((unsigned)ceil_div(w.n_groups * w.ld_g, 4 * 256)), dim3(256), 0,
-                     stream, w.gmax, a.row_lse, B, w.ld_g, w.n_groups, a.n_active, w.gscale,
-                     a.active, w.act_pad, w.n_act_pad);
+                     stream, w.gmax, a.row_lse, B, w.ld_g, w.n_groups, a.n_active, w.gscale);
   hipLaunchKernelGGL((k_dx16<Tag, WI>), dim3((unsigned)(8 * per_xcd)), dim3(128 * WI), 0, stream,
                      (const uint16_t*)a.W, w.act_pad, a.n_active, w.inv_w, w.inv_w_max,
                      (const uint16_t*)w.lbuf, w.ld_cos, w.gscale, w.ld_g, B, n_rt, w.n_split,

@@ -47,6 +47,7 @@ __shared__ __attribute__((aligned(1024))) uint16_t fB0[kFwdStageB], fB1[kFwdStag
     fB2[kFwdStageB];
 __shared__ float2 fRed[1][kFwdBN];
 __shared__ __attribute__((aligned(16))) float fIw[kFwdBM];
+__shared__ int32_t fIds[kFwdBM];   // the tile's class-row ids
 __shared__ float fNrm[2][kFwdBM];
 
 template <int S>
@@ -79,12 +80,20 @@ __device__ __forceinline__ uint16_t* fwd_tile_row(int r) {
 // DMA of one stage: class operand rows 16 (2 wave + u) + lane / 4 (u < 2),
 // batch operand rows 16 (4 wave + u) + lane / 4 (u < 4).
 template <int S>
-__device__ __forceinline__ void fwd_issue(const uint16_t* const ap[2], const uint16_t* const bp[4],
-                                          int k0, int64_t kb, int wave) {
+__device__ __forceinline__ void fwd_issue_a(const uint16_t* const ap[2], int k0, int wave) {
 #pragma unroll
   for (int u = 0; u < 2; ++u) dma16(ap[u] + k0, fwd_a<S>() + (2 * wave + u) * 16 * kFwdKC);
+}
+template <int S>
+__device__ __forceinline__ void fwd_issue_b(const uint16_t* const bp[4], int64_t kb, int wave) {
 #pragma unroll
   for (int u = 0; u < 4; ++u) dma16(bp[u] + kb, fwd_b<S>() + (4 * wave + u) * 16 * kFwdKC);
+}
+template <int S>
+__device__ __forceinline__ void fwd_issue(const uint16_t* const ap[2], const uint16_t* const bp[4],
+                                          int k0, int64_t kb, int wave) {
+  fwd_issue_a<S>(ap, k0, wave);
+  fwd_issue_b<S>(bp, kb, wave);
 }
 
 // a0^2 + a1^2 + acc for a packed pair of 16-bit values (v_dot2_f32_*).
@@ -285,7 +294,7 @@ __device__ __forceinline__ void fwd_epilogue_rows_plain(f32x16_t (&acc)[4][2], i
 template <typename Tag, int NK, bool FILT>
 __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
     const uint16_t* __restrict__ Xb, int64_t ld_xb, const uint16_t* __restrict__ W,
-    const int32_t* __restrict__ active, const int32_t* __restrict__ n_active_p,
+    const int32_t* __restrict__ act_pad, const int32_t* __restrict__ n_active_p,
     const int32_t* __restrict__ yhat, const float* __restrict__ inv_x,
     float* __restrict__ inv_w, float* __restrict__ inv_w_max, int B, int64_t ld_cos,
     int64_t n_ctiles, int n_rt, int64_t n_tiles, int64_t per_xcd, Margin mg, float tau,
@@ -298,32 +307,46 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
   if (t >= n_tiles) return;
   const int64_t ct = t / n_rt;
   const int rt = (int)(t % n_rt);
-  const int K = *n_active_p;
   const int64_t j0 = ct * kFwdBM;
-  if (j0 >= K) return;
   const int n0 = rt * kFwdBN;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = 0, wn = wave;   // every wave: all 128 classes, its 64 batch rows
   const int half = lane >> 5, l32 = lane & 31;
 
-  // Per-lane source rows of the DMA segments; rows past the end are clamped
-  // to a valid row (their results are masked in the epilogue).
+  // Per-lane source rows of the DMA segments.  The class rows come from the
+  // padded id list (entries past |S| repeat the last active id, so their
+  // results are valid numbers, masked in the epilogue), which needs no wait
+  // for |S|: the ids of the wave's 32 class rows go straight to LDS first,
+  // then the batch rows of the first two stages are requested (rows past the
+  // end clamped to a valid row), then the ids are read back and the class
+  // rows requested.
   const int cidx = (lane & 3) ^ ((lane >> 4) & 3);
+  if (lane < 32)
+    __builtin_amdgcn_global_load_lds(act_pad + j0 + 32 * wave + lane, (lds_void_t)(fIds + 32 * wave),
+                                     4, 0, 0);
   const uint16_t* ap[2];
   const uint16_t* bp[4];
-#pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int row = 16 * (2 * wave + u) + (lane >> 2);
-    const int64_t jr = j0 + row < K ? j0 + row : K - 1;
-    ap[u] = W + (int64_t)active[jr] * D + 8 * cidx;
-  }
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
     const int row = 16 * (4 * wave + u) + (lane >> 2);
     const int nr = n0 + row < B ? n0 + row : B - 1;
     bp[u] = Xb + (int64_t)nr * kFwdKC + 8 * cidx;
   }
+  fwd_issue_b<0>(bp, 0, wave);
+  if constexpr (NK > 1) fwd_issue_b<1>(bp, (int64_t)kFwdKC * ld_xb, wave);
+  const int K = *n_active_p;
+  if (j0 >= K) {   // no active class in the tile: drain the wave's loads into LDS, leave
+    wait_vmcnt<0>();
+    return;
+  }
+  wait_vmcnt<(NK > 1 ? 8 : 4)>();   // the id load, older than the batch-row loads, has landed
+  uint32_t ids[2];
+  ds_read_32<0>(ids[0], lds_addr(fIds + 32 * wave + (lane >> 2)));
+  ds_read_32<64>(ids[1], lds_addr(fIds + 32 * wave + (lane >> 2)));
+  lgkm_wait<0>(ids[0], ids[1]);
+#pragma unroll
+  for (int u = 0; u < 2; ++u) ap[u] = W + (int64_t)ids[u] * D + 8 * cidx;
 
   f32x16_t acc[4][2];
 #pragma unroll
@@ -333,26 +356,32 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.0f;
 
-  // Epilogue inputs, requested before the main loop: each lane's row data.
+  // Epilogue inputs, requested before the main loop and not used before the
+  // epilogue (so nothing waits for them here): each lane's row data, from a
+  // valid row for rows past the batch (whose results are never stored).
   float ixr[2];
-  int yhr[2];
+  int yraw[2];
 #pragma unroll
   for (int nb = 0; nb < 2; ++nb) {
     const int n = n0 + 64 * wn + 32 * nb + l32;
-    ixr[nb] = n < B ? inv_x[n] : 0.0f;
-    yhr[nb] = n < B && yhat[n] < K ? yhat[n] : -1;   // past |S|: unowned
+    const int nc = n < B ? n : B - 1;
+    ixr[nb] = inv_x[nc];
+    yraw[nb] = yhat[nc];
   }
 
   float wss[4] = {0.0f, 0.0f, 0.0f, 0.0f};  // partial ||w||^2 of the lane's class rows
-  constexpr int kPerStage = 6;  // DMAs per thread per stage
-  fwd_issue<0>(ap, bp, 0, 0, wave);
-  if constexpr (NK > 1) fwd_issue<1>(ap, bp, kFwdKC, (int64_t)kFwdKC * ld_xb, wave);
+  constexpr int kPerStage = 6;  // DMAs per thread per stage (2 class-row, 4 batch-row)
+  fwd_issue_a<0>(ap, 0, wave);
+  if constexpr (NK > 1) fwd_issue_a<1>(ap, kFwdKC, wave);
   static_for<0, NK>([&](auto cc) {
     constexpr int c = decltype(cc)::value;
     constexpr int ahead = (NK - 1 - c) < 1 ? (NK - 1 - c) : 1;
+    // Loads still in flight that belong to later chunks: stage 1's class rows
+    // (issued last) at chunk 0, the next stage's six loads after that.
+    constexpr int later = c == 0 ? 2 * ahead : kPerStage * ahead;
     // This wave's loads of chunk c have landed; after the barrier everyone's
     // have, and every wave is done with chunk c - 1, whose stage is refilled.
-    wait_vmcnt<kPerStage * ahead>();
+    wait_vmcnt<later>();
     stage_barrier();
     if constexpr (c + 2 < NK) fwd_issue<(c + 2) % 3>(ap, bp, (c + 2) * kFwdKC, (int64_t)(c + 2) * kFwdKC * ld_xb, wave);
     fwd_compute<c % 3, Tag>(acc, wm, wn, lane, wss);
@@ -386,7 +415,8 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
   // ---- epilogue.  The fp16 128-class x 256-row tile of E values is
   // assembled in the (now idle) LDS ring (rows of 256 B, 16-byte block b of
   // row r at position b ^ (r & 15): conflict-free writes from the MFMA layout
-  // and reads along rows), then written out in whole rows.
+  // and reads along rows); each wave writes out its rows, 32 at a time, in
+  // whole rows as soon as they are done.
   wait_lgkm0();
   stage_barrier();  // all fragment reads of the ring are done
   const int64_t jlo = j0 + 128 * wm;
@@ -397,7 +427,8 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
   bool has_t[2];
 #pragma unroll
   for (int nb = 0; nb < 2; ++nb) {
-    const int yh = yhr[nb];
+    const int n = n0 + 64 * wn + 32 * nb + l32;
+    const int yh = n < B && yraw[nb] < K ? yraw[nb] : -1;   // past |S|: unowned
     tpos[nb] = yh - (int)(jlo + 4 * half);   // target's offset in this lane's class pattern
     has_t[nb] = yh >= jlo && yh < jlo + 128 && ((tpos[nb] & 4) == 0);
   }
@@ -408,6 +439,32 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
       fRed[wm][nl] = make_float2(mx, sm);
       // reference of the row's 128-class group, the tile's
       if (n < B) gmax[ct * ld_g + n] = mx == -INFINITY ? 0.0f : mx;
+    }
+  };
+  // Rows 64 wave + 32 nb .. + 31 of the tile, which this wave alone wrote:
+  // read back along rows (the wave's LDS accesses complete in order) and
+  // stored as whole 256-byte rows, four rows per store, while the wave goes
+  // on with its next row block.  The stores are non-temporal: the logit
+  // store is read back only by later kernels, after gigabytes of other
+  // traffic, so it should not take L2 space from the operands this kernel
+  // re-reads.
+  auto store_rows = [&](int nb) __attribute__((always_inline)) {
+    wait_lgkm0();
+    asm volatile("" ::: "memory");   // the tile writes above are not moved below the reads
+    const int b = lane & 15;
+    u32x4_t v[8];
+    static_for<0, 8>([&](auto ii) {
+      constexpr int i = decltype(ii)::value;
+      const int r = 64 * wave + 32 * nb + 4 * i + (lane >> 4);
+      ds_read_128<0>(v[i], lds_addr(fwd_tile_row(r) + 8 * (b ^ (r & 15))));
+    });
+    lgkm_wait<0>(v);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int n = n0 + 64 * wave + 32 * nb + 4 * i + (lane >> 4);
+      if (n < B)
+        __builtin_nontemporal_store(
+            v[i], reinterpret_cast<u32x4_t*>(lbuf + (int64_t)n * ld_cos + j0 + 8 * b));
     }
   };
   // Two separate paths over both row blocks, so that the masking work of
@@ -425,6 +482,7 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
         fwd_epilogue_rows_plain(acc, nb, ixr[nb] * (mg.s * kLog2e), iwp, fwd_tile_row(nl),
                                 16 * wm, nl & 15, half, &mx, &sm);
       finish(nb, mx, sm);
+      store_rows(nb);
     }
   } else {
 #pragma unroll
@@ -437,33 +495,11 @@ __global__ void __launch_bounds__(kFwdThreads, 2) k_fwd16(
                                           &sm, has_t[nb] ? tgt + n : nullptr,
                                           has_t[nb] ? tgtc + n : nullptr);
       finish(nb, mx, sm);
+      store_rows(nb);
     }
   }
-  wait_lgkm0();
-  stage_barrier();
-  // Wave w writes rows 64 w .. 64 w + 63, four rows (4 x 256 B) per store;
-  // all of its LDS reads are issued before the first store.  The stores are
-  // non-temporal: the logit store is read back only by later kernels, after
-  // gigabytes of other traffic, so it should not take L2 space from the
-  // operands this kernel re-reads.
-  {
-    const int b = lane & 15;
-    u32x4_t v[16];
-    static_for<0, 16>([&](auto ii) {
-      constexpr int i = decltype(ii)::value;
-      const int r = 64 * wave + 4 * i + (lane >> 4);
-      ds_read_128<0>(v[i], lds_addr(fwd_tile_row(r) + 8 * (b ^ (r & 15))));
-    });
-    lgkm_wait<0>(v);
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int r = 64 * wave + 4 * i + (lane >> 4);
-      const int n = n0 + r;
-      if (n < B)
-        __builtin_nontemporal_store(
-            v[i], reinterpret_cast<u32x4_t*>(lbuf + (int64_t)n * ld_cos + j0 + 8 * b));
-    }
-  }
+  // Row r of the pairs was written by lane r % 32 of wave r / 64, this
+  // thread's own wave: no barrier.
   for (int r = tid; r < kFwdBN; r += kFwdThreads) {
     const int n = n0 + r;
     if (n < B) stats[(int64_t)n * n_ctiles + ct] = fRed[0][r];
@@ -594,13 +630,13 @@ void launch_fwd16_nk(unsigned grid, hipStream_t stream, const StepArgs& a, const
                      int n_rt, int64_t n_tiles, int64_t per_xcd, const Margin& mg) {
   if (a.tau < 1.0f)
     hipLaunchKernelGGL((k_fwd16<Tag, NK, true>), dim3(grid), dim3(kFwdThreads), 0, stream,
-                       (const uint16_t*)w.xblk, w.ld_xt, (const uint16_t*)a.W, a.active, a.n_active,
+                       (const uint16_t*)w.xblk, w.ld_xt, (const uint16_t*)a.W, w.act_pad, a.n_active,
                        a.labels_mapped, w.inv_x, w.inv_w, w.inv_w_max, B, w.ld_cos, w.n_ctiles,
                        n_rt, n_tiles, per_xcd, mg, a.tau, (uint16_t*)w.lbuf, w.stats, w.tgt,
                        w.tgtc, w.gmax, w.ld_g);
   else
     hipLaunchKernelGGL((k_fwd16<Tag, NK, false>), dim3(grid), dim3(kFwdThreads), 0, stream,
-                       (const uint16_t*)w.xblk, w.ld_xt, (const uint16_t*)a.W, a.active, a.n_active,
+                       (const uint16_t*)w.xblk, w.ld_xt, (const uint16_t*)a.W, w.act_pad, a.n_active,
                        a.labels_mapped, w.inv_x, w.inv_w, w.inv_w_max, B, w.ld_cos, w.n_ctiles,
                        n_rt, n_tiles, per_xcd, mg, a.tau, (uint16_t*)w.lbuf, w.stats, w.tgt,
                        w.tgtc, w.gmax, w.ld_g);

@@ -77,7 +77,7 @@ struct StepWs {
   float* loss_part;      // [B] per-row loss terms
   int32_t* act_pad;      // [n_act_pad] the active row ids, padded with the last one
                          // (read a whole 32-class chunk at a time by the dX kernel)
-  int64_t n_act_pad;     // cap rounded up to 32
+  int64_t n_act_pad;     // cap rounded up to 128
   int32_t* dw_gate;      // [kDwGates] start gates of the class-gradient kernel: entry i holds
                          // the launch number once workgroup 2 i has finished its contraction
 };

@@ -34,14 +34,33 @@ __device__ __forceinline__ float sumsq8(const uint4& v) {
 // = [ld_xt][32]: entry (n, e) = X[n][32 k + e]), the forward's operand, whose
 // k-th chunk of a run of rows is then contiguous.  Rows n in [B, ld_xt) are
 // zero in both.  Also clears the running max of 1/||w_j||.
+// Workgroups past the first ld_xt / 32 write the padded copy of the active
+// row ids that the contraction kernels read a chunk or tile at a time, with
+// no wait on |S|: act_pad[j] = active[min(j, |S| - 1)] (0 if S is empty).
 constexpr int kPrepRows = 32;
+constexpr int kPadPerBlock = 4 * 256;   // act_pad entries per workgroup
 template <typename Tag>
 __global__ void __launch_bounds__(256) k_prep_x16(const uint16_t* __restrict__ X, int B, int d,
                                                   int64_t ld_xt, float* __restrict__ inv_x,
                                                   uint16_t* __restrict__ xbT,
                                                   uint16_t* __restrict__ xblk,
-                                                  float* __restrict__ inv_w_max) {
+                                                  float* __restrict__ inv_w_max,
+                                                  const int32_t* __restrict__ active,
+                                                  const int32_t* __restrict__ n_active_p,
+                                                  int32_t* __restrict__ act_pad, int64_t n_pad) {
   __shared__ uint16_t tile[kPrepRows][512 + 8];
+  const int64_t n_row_blocks = ld_xt / kPrepRows;
+  if (blockIdx.x >= n_row_blocks) {
+    // Four consecutive entries per thread (n_pad is a multiple of 4).
+    const int64_t i = (blockIdx.x - n_row_blocks) * kPadPerBlock + 4 * threadIdx.x;
+    if (i >= n_pad) return;
+    const int64_t K = *n_active_p;
+    int o[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = K > 0 ? active[i + e < K ? i + e : K - 1] : 0;
+    *reinterpret_cast<int4*>(act_pad + i) = make_int4(o[0], o[1], o[2], o[3]);
+    return;
+  }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n0 = blockIdx.x * kPrepRows;
   if (blockIdx.x == 0 && threadIdx.x == 0) *inv_w_max = 0.0f;
@@ -129,14 +148,18 @@ hipError_t launch_prep(const StepArgs& a, const StepWs& w, hipStream_t stream) {
                        (const float*)a.X, B, d, w.inv_x);
     hipLaunchKernelGGL(k_norm_w32, dim3(wblocks), dim3(256), 0, stream, (const float*)a.W, d,
                        a.active, a.n_active, a.cap, w.inv_w);
-  } else if (a.dtype == 1) {
-    hipLaunchKernelGGL(k_prep_x16<Bf16Tag>, dim3((unsigned)(w.ld_xt / kPrepRows)), dim3(256), 0,
-                       stream, (const uint16_t*)a.X, B, d, w.ld_xt, w.inv_x, (uint16_t*)w.xbT,
-                       (uint16_t*)w.xblk, w.inv_w_max);
   } else {
-    hipLaunchKernelGGL(k_prep_x16<F16Tag>, dim3((unsigned)(w.ld_xt / kPrepRows)), dim3(256), 0,
-                       stream, (const uint16_t*)a.X, B, d, w.ld_xt, w.inv_x, (uint16_t*)w.xbT,
-                       (uint16_t*)w.xblk, w.inv_w_max);
+    const unsigned grid = (unsigned)(w.ld_xt / kPrepRows + ceil_div(w.n_act_pad, kPadPerBlock));
+    if (a.dtype == 1)
+      hipLaunchKernelGGL(k_prep_x16<Bf16Tag>, dim3(grid), dim3(256), 0, stream,
+                         (const uint16_t*)a.X, B, d, w.ld_xt, w.inv_x, (uint16_t*)w.xbT,
+                         (uint16_t*)w.xblk, w.inv_w_max, a.active, a.n_active, w.act_pad,
+                         w.n_act_pad);
+    else
+      hipLaunchKernelGGL(k_prep_x16<F16Tag>, dim3(grid), dim3(256), 0, stream,
+                         (const uint16_t*)a.X, B, d, w.ld_xt, w.inv_x, (uint16_t*)w.xbT,
+                         (uint16_t*)w.xblk, w.inv_w_max, a.active, a.n_active, w.act_pad,
+                         w.n_act_pad);
   }
   timing_stop(1, stream);
   return hipGetLastError();
