@@ -158,6 +158,14 @@ __device__ __forceinline__ void fwd_compute(f32x16_t (&acc)[4][2], int wm, int w
   });
 }
 
+// The 8-byte piece (classes 32 mb + 8 g + 4 half .. + 3) of a tile row: its
+// 16-byte block b = bbase + 4 mb + g sits at position b ^ bsw (bbase a
+// multiple of 16, bsw < 16), split here into the mb and g parts of the XOR.
+__device__ __forceinline__ uint16_t* tile_block(uint16_t* trow, int bbase, int bsw, int mb, int g,
+                                                int half) {
+  return trow + 8 * bbase + 32 * (mb ^ (bsw >> 2)) + 8 * (g ^ (bsw & 3)) + 4 * half;
+}
+
 // Epilogue of one lane for one 32-row block (nb): the lane's row n and its
 // 64 classes j = jb + 32 mb + 8 g + e (jb = first class of the lane's
 // pattern, e < 4); with the partner lane (half ^ 1) they are the row's 128
@@ -216,7 +224,6 @@ __device__ __forceinline__ void fwd_epilogue_rows(f32x16_t (&acc)[4][2], int nb,
   for (int mb = 0; mb < 4; ++mb) {
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const int o = 32 * mb + 8 * g;
       float ev[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -226,7 +233,7 @@ __device__ __forceinline__ void fwd_epilogue_rows(f32x16_t (&acc)[4][2], int nb,
       uint2 packed;
       packed.x = pack_f16x2(ev[0], ev[1]);
       packed.y = pack_f16x2(ev[2], ev[3]);
-      *reinterpret_cast<uint2*>(trow + 8 * ((bbase + o / 8) ^ bsw) + 4 * half) = packed;
+      *reinterpret_cast<uint2*>(tile_block(trow, bbase, bsw, mb, g, half)) = packed;
     }
   }
   if (CHECK_T && tgt_out) sm += __builtin_amdgcn_exp2f(ft2 - mref);
@@ -265,7 +272,6 @@ __device__ __forceinline__ void fwd_epilogue_rows_plain(f32x16_t (&acc)[4][2], i
   for (int mb = 0; mb < 4; ++mb) {
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const int o = 32 * mb + 8 * g;
       float ev[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -275,7 +281,7 @@ __device__ __forceinline__ void fwd_epilogue_rows_plain(f32x16_t (&acc)[4][2], i
       uint2 packed;
       packed.x = pack_f16x2(ev[0], ev[1]);
       packed.y = pack_f16x2(ev[2], ev[3]);
-      *reinterpret_cast<uint2*>(trow + 8 * ((bbase + o / 8) ^ bsw) + 4 * half) = packed;
+      *reinterpret_cast<uint2*>(tile_block(trow, bbase, bsw, mb, g, half)) = packed;
     }
   }
   sm += __shfl_xor(sm, 32, 64);
