@@ -305,6 +305,45 @@ def measured_ceilings(dev, dtype):
             "gemm_dtype": dtype}
 
 
+def library_same_shape(dev, dtype, B, d, K, copy_gbps, update_bytes):
+    """The library's own GEMM (torch.matmul) on the step's three contraction
+    shapes, with contiguous random operands and none of the path's other work
+    (no gather, no epilogue, no update): [B,d]x[d,K] with a 16-bit [B,K]
+    result (the forward), [B,K]x[K,d] (dX), and [K,B]x[B,d] with the class
+    operand stored class-major (dW's contraction).  For dW the library figure
+    adds the update's compulsory bytes at the measured copy rate, as a
+    separate update kernel would need."""
+    import torch
+    tdt = {"bf16": torch.bfloat16, "f16": torch.float16}[dtype]
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    X = torch.randn((B, d), device=dev, generator=g).to(tdt)
+    W = (torch.randn((K, d), device=dev, generator=g) * 0.05).to(tdt)
+    G = (torch.rand((B, K), device=dev, generator=g) * 1e-3).to(tdt)
+    Gt = G.t().contiguous()
+    out = torch.empty((B, K), device=dev, dtype=tdt)
+
+    def ms_of(f, reps=10):
+        for _ in range(2):
+            f()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            f()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    res = {"forward_ms": ms_of(lambda: torch.matmul(X, W.t(), out=out)),
+           "dx_ms": ms_of(lambda: torch.matmul(G, W)),
+           "dw_gemm_ms": ms_of(lambda: torch.matmul(Gt, X))}
+    res["dw_gemm_plus_update_ms"] = res["dw_gemm_ms"] + update_bytes / (copy_gbps * 1e9) * 1e3
+    res["dtype"] = dtype
+    del X, W, G, Gt, out
+    torch.cuda.empty_cache()
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -478,6 +517,15 @@ def main():
         / ceil["gemm_8192_tflops"],
         "dw_update": dw_bytes / (stage_ms["dw_update"] * 1e-3) / 1e9 / ceil["copy_1GiB_GBps"],
     }
+    lib = vs_lib = None
+    if cfg["dtype"] in ("bf16", "f16"):
+        lib = library_same_shape(dev, cfg["dtype"], B, d, K, ceil["copy_1GiB_GBps"], dw_bytes)
+        vs_lib = {"fwd_gemm": lib["forward_ms"] / stage_ms["fwd_gemm"],
+                  "dx_gemm": lib["dx_ms"] / stage_ms["dx_gemm"],
+                  "dw_update": lib["dw_gemm_plus_update_ms"] / stage_ms["dw_update"]}
+        log(f"[bench] library GEMM on the same shapes: forward {lib['forward_ms']:.3f} ms, "
+            f"dX {lib['dx_ms']:.3f} ms, dW {lib['dw_gemm_ms']:.3f} ms "
+            f"(+ update at copy rate {lib['dw_gemm_plus_update_ms']:.3f} ms)")
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -516,6 +564,8 @@ def main():
         "gather": gather,
         "measured_ceilings": ceil,
         "stage_frac_of_measured_ceiling": vs_ceil,
+        "library_same_shape": lib,
+        "stage_speed_vs_library_same_shape": vs_lib,
         "step_mfma_frac": step_fl / (ms_per_step * 1e-3) / (cm.PEAK_TFLOPS[cfg["dtype"]] * 1e12),
         "update_hbm_frac": upd_b / (stage_ms["dw_update"] * 1e-3) / (cm.PEAK_HBM_GBPS * 1e9),
         "last_loss": loss,
